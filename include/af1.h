@@ -1,0 +1,173 @@
+/*
+ * af1.h -- C ABI of the AF1 binary-factorized linear layer on AMD MI355X
+ * (gfx950).
+ *
+ * The layer (paper "All for 1-Bit", Sec. 4.1, the deployable reconstruction
+ * with merged middle scale, label eq:final_reconstruction; App. A.2.1, the
+ * equivalent Diag form, label eq:double_factor_equiv) is
+ *
+ *     W_hat = Diag(s_out) * Bu * Diag(s_mid) * Bv * Diag(s_in)
+ *     y     = s_out .* ( Bu * ( s_mid .* ( Bv * ( s_in .* x ) ) ) )
+ *
+ * with sign factors Bu in {-1,+1}^{m x r} (the paper's A_pm1) and Bv in
+ * {-1,+1}^{r x n} (B_pm1), and 16-bit scale vectors s_out (a, length m),
+ * s_mid (m = m1 .* m2, length r) and s_in (b, length n).  m is d_out, n is
+ * d_in.  Storage per layer is r*(m+n) sign bits plus 16*(m+n+r) scale bits
+ * (App. A.3, label eq:app_af1_memory).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Sign storage: a rows x cols sign matrix is rows * (cols/32) uint32 words,
+ *   row-major; column j of a row is bit (j mod 32) of word (j div 32); bit 1
+ *   encodes -1 and bit 0 encodes +1.  cols must be a multiple of 32 (the
+ *   format has no padding bits).
+ * Scales: IEEE binary16 bit patterns (uint16_t).
+ * Activations and outputs: bfloat16 bit patterns (uint16_t), row-major
+ *   [batch, features], token-major, contiguous.
+ * Pointers: all array arguments are DEVICE pointers (hipMalloc / torch CUDA
+ *   tensors) and must be 16-byte aligned.  The caller owns every buffer; the
+ *   library allocates nothing, keeps no pointer after a call returns and
+ *   reads the descriptor struct only during the call.
+ * Streams: `stream` is a hipStream_t passed as void*; NULL means the null
+ *   stream.  Calls only enqueue work and return without synchronising.
+ * Errors: argument errors are detected on the host and returned before any
+ *   work is enqueued, with no side effect.  AF1_ERR_HIP means a launch was
+ *   rejected by the HIP runtime.  No C++ exception crosses this boundary.
+ *   Every entry point is reentrant; the library holds no mutable state.
+ * Shapes: m, n, r are multiples of 32 in [32, AF1_MAX_DIM].
+ */
+#ifndef AF1_H
+#define AF1_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Only the entry points below are exported from libaf1.so. */
+#define AF1_API __attribute__((visibility("default")))
+
+#define AF1_MAX_DIM (1 << 20)   /* largest m, n or r accepted */
+#define AF1_GEMV_MAX_BATCH 16   /* decode batch limit of af1_linear_gemv */
+#define AF1_GEMM_MAX_TOKENS (1 << 20)
+
+typedef enum af1_status {
+    AF1_OK = 0,
+    AF1_ERR_NULL = 1,        /* a required pointer is NULL */
+    AF1_ERR_SHAPE = 2,       /* dimension <= 0, not a multiple of 32, or too large */
+    AF1_ERR_BATCH = 3,       /* batch / token count outside the accepted range */
+    AF1_ERR_ALIGN = 4,       /* a device pointer is not 16-byte aligned */
+    AF1_ERR_WORKSPACE = 5,   /* workspace missing or smaller than the query returns */
+    AF1_ERR_ALIAS = 6,       /* an output buffer overlaps an input or the workspace */
+    AF1_ERR_HIP = 7,         /* the HIP runtime rejected a launch */
+    AF1_ERR_DTYPE = 8        /* unknown source element type */
+} af1_status;
+
+/* Element type of the dense matrix handed to af1_pack. */
+typedef enum af1_src_dtype {
+    AF1_SRC_F32 = 0,   /* IEEE binary32 */
+    AF1_SRC_BF16 = 1,  /* bfloat16 patterns */
+    AF1_SRC_F16 = 2,   /* IEEE binary16 patterns */
+    AF1_SRC_I8 = 3     /* int8 */
+} af1_src_dtype;
+
+/*
+ * One factorized linear layer (Sec. 4.1 / App. A.2.1; storage of App. A.3).
+ *   Bu    : m x r signs,  m * (r/32) words   (paper: A_pm1)
+ *   Bv    : r x n signs,  r * (n/32) words   (paper: B_pm1)
+ *   s_out : m binary16   (paper: a)
+ *   s_mid : r binary16   (paper: m = m1 .* m2, merged after optimisation)
+ *   s_in  : n binary16   (paper: b)
+ */
+typedef struct af1_factorized_linear {
+    int64_t m;
+    int64_t n;
+    int64_t r;
+    const uint32_t *Bu;
+    const uint32_t *Bv;
+    const uint16_t *s_out;
+    const uint16_t *s_mid;
+    const uint16_t *s_in;
+} af1_factorized_linear;
+
+/*
+ * af1_pack -- sign -> bit packing of a dense rows x cols matrix (the binary
+ * factors of App. A.3 are stored one bit per sign).
+ *   src      : device, rows*cols elements of `src_dtype`, row-major.
+ *   dst      : device, rows*(cols/32) uint32 words (written).
+ * The bit of an element is its IEEE sign bit for the floating types (so +0
+ * packs as +1, -0 as -1, NaN by its sign bit) and (v < 0) for int8.  The
+ * result is bit-exact and deterministic.  rows may be 0 (nothing enqueued);
+ * cols must be a positive multiple of 32; rows*cols < 2^40.
+ */
+AF1_API af1_status af1_pack(const void *src, int32_t src_dtype, int64_t rows,
+                    int64_t cols, uint32_t *dst, void *stream);
+
+/*
+ * af1_unpack -- inverse of af1_pack into dense int8 +-1 (a debugging and
+ * testing aid, not part of the forward path).
+ *   words : device, rows*(cols/32) uint32;  dst : device, rows*cols int8.
+ */
+AF1_API af1_status af1_unpack(const uint32_t *words, int64_t rows, int64_t cols,
+                      int8_t *dst, void *stream);
+
+/*
+ * af1_linear_gemv -- decode-regime forward of one factorized layer
+ * (App. A.2.1, Diag form, evaluated right to left).
+ *   x  : device, [b, n] bfloat16.       y : device, [b, m] bfloat16 (written).
+ *   b  : 1 .. AF1_GEMV_MAX_BATCH.
+ *   ws : device workspace of at least af1_gemv_workspace_bytes(m, n, r, b)
+ *        bytes.  It must be zero-filled before its first use (it holds
+ *        arrival counters); every call that completes leaves those counters
+ *        at zero again, so one workspace serves any sequence of calls on one
+ *        stream.  Calls that may overlap in time need distinct workspaces.
+ * Arithmetic: s_in .* x in fp32 (exact), both sign products accumulated in
+ * fp32, the rank-r intermediate kept in fp32, scales applied in fp32, y
+ * rounded to bfloat16 (round to nearest even).  y must not overlap x, the
+ * layer's arrays or ws.
+ */
+AF1_API size_t af1_gemv_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t b);
+AF1_API af1_status af1_linear_gemv(const af1_factorized_linear *L, const uint16_t *x,
+                           int64_t b, uint16_t *y, void *ws, size_t ws_bytes,
+                           void *stream);
+
+/*
+ * af1_linear_gemm -- prefill-regime forward for T tokens on the matrix cores.
+ *   x  : device, [T, n] bfloat16.       y : device, [T, m] bfloat16 (written).
+ *   T  : 1 .. AF1_GEMM_MAX_TOKENS.
+ *   ws : device workspace of at least af1_gemm_workspace_bytes(m, n, r, T)
+ *        bytes; holds the [T, r] intermediate.
+ * Arithmetic: both products run on fp16 MFMA with fp32 accumulation.  The
+ * sign of each factor entry is applied to the fp16 column scale (s_in for
+ * the first product, s_mid for the second), so every operand is exact:
+ * x enters as fp16 (exact for |x| < 65504), the intermediate is rounded
+ * once to fp16 before the second product (|values| must stay below 65504),
+ * s_out is applied in fp32 and y is rounded to bfloat16.
+ */
+AF1_API size_t af1_gemm_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T);
+AF1_API af1_status af1_linear_gemm(const af1_factorized_linear *L, const uint16_t *x,
+                           int64_t T, uint16_t *y, void *ws, size_t ws_bytes,
+                           void *stream);
+
+/* Deployable storage bits of one layer: r*(m+n) + 16*(m+n+r) (App. A.3,
+ * label eq:app_af1_memory).  Returns -1 for negative arguments. */
+AF1_API int64_t af1_storage_bits(int64_t m, int64_t n, int64_t r);
+
+/* Largest multiple of 32 rank whose storage bits do not exceed m*n (a
+ * strict 1.0 effective-BPW budget for this layer alone, App. A.3).  Returns
+ * 0 when no positive rank fits or an argument is not positive. */
+AF1_API int64_t af1_budget_rank(int64_t m, int64_t n);
+
+/* Static, NUL-terminated description of a status code. */
+AF1_API const char *af1_status_string(int32_t status);
+
+/* Library version string. */
+AF1_API const char *af1_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AF1_H */

@@ -1,0 +1,155 @@
+"""Python binding of ``libaf1.so`` (C ABI in include/af1.h).
+
+Argument marshalling only: every function forwards to the C entry point of
+the same name, passing device pointers taken from torch tensors (or plain
+integers) and the current HIP stream.  No computation happens here, and there
+is no fallback: if the library is missing, every call raises.
+"""
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libaf1.so")
+
+AF1_OK = 0
+AF1_ERR_NULL = 1
+AF1_ERR_SHAPE = 2
+AF1_ERR_BATCH = 3
+AF1_ERR_ALIGN = 4
+AF1_ERR_WORKSPACE = 5
+AF1_ERR_ALIAS = 6
+AF1_ERR_HIP = 7
+AF1_ERR_DTYPE = 8
+
+AF1_SRC_F32, AF1_SRC_BF16, AF1_SRC_F16, AF1_SRC_I8 = 0, 1, 2, 3
+AF1_GEMV_MAX_BATCH = 16
+AF1_MAX_DIM = 1 << 20
+
+_lib = None
+
+
+class Af1Error(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} (status {status})")
+
+
+class af1_factorized_linear(ctypes.Structure):
+    _fields_ = [("m", ctypes.c_int64), ("n", ctypes.c_int64), ("r", ctypes.c_int64),
+                ("Bu", ctypes.c_void_p), ("Bv", ctypes.c_void_p),
+                ("s_out", ctypes.c_void_p), ("s_mid", ctypes.c_void_p),
+                ("s_in", ctypes.c_void_p)]
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                           "(there is no fallback path)")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I64, I32, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+    L.af1_pack.argtypes = [P, I32, I64, I64, P, P]
+    L.af1_unpack.argtypes = [P, I64, I64, P, P]
+    L.af1_gemv_workspace_bytes.argtypes = [I64, I64, I64, I64]
+    L.af1_gemv_workspace_bytes.restype = SZ
+    L.af1_linear_gemv.argtypes = [ctypes.POINTER(af1_factorized_linear), P, I64, P, P, SZ, P]
+    L.af1_gemm_workspace_bytes.argtypes = [I64, I64, I64, I64]
+    L.af1_gemm_workspace_bytes.restype = SZ
+    L.af1_linear_gemm.argtypes = [ctypes.POINTER(af1_factorized_linear), P, I64, P, P, SZ, P]
+    L.af1_storage_bits.argtypes = [I64, I64, I64]
+    L.af1_storage_bits.restype = I64
+    L.af1_budget_rank.argtypes = [I64, I64]
+    L.af1_budget_rank.restype = I64
+    L.af1_status_string.argtypes = [I32]
+    L.af1_status_string.restype = ctypes.c_char_p
+    L.af1_version.restype = ctypes.c_char_p
+    for fn in ("af1_pack", "af1_unpack", "af1_linear_gemv", "af1_linear_gemm"):
+        getattr(L, fn).restype = I32
+    _lib = L
+    return L
+
+
+def _addr(t):
+    """Device address of a torch tensor, or an integer address as is."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(status, where):
+    if status != AF1_OK:
+        raise Af1Error(status, where)
+
+
+def status_string(status: int) -> str:
+    return lib().af1_status_string(int(status)).decode()
+
+
+def af1_version() -> str:
+    return lib().af1_version().decode()
+
+
+def make_layer(m, n, r, Bu, Bv, s_out, s_mid, s_in) -> af1_factorized_linear:
+    """The C descriptor of one factorized layer (device arrays)."""
+    return af1_factorized_linear(m, n, r, _addr(Bu), _addr(Bv), _addr(s_out),
+                                 _addr(s_mid), _addr(s_in))
+
+
+def af1_pack(src, src_dtype: int, rows: int, cols: int, dst, stream=None, check=True) -> int:
+    st = lib().af1_pack(_addr(src), src_dtype, rows, cols, _addr(dst), _stream(stream))
+    if check:
+        _check(st, "af1_pack")
+    return st
+
+
+def af1_unpack(words, rows: int, cols: int, dst, stream=None, check=True) -> int:
+    st = lib().af1_unpack(_addr(words), rows, cols, _addr(dst), _stream(stream))
+    if check:
+        _check(st, "af1_unpack")
+    return st
+
+
+def af1_gemv_workspace_bytes(m, n, r, b) -> int:
+    return int(lib().af1_gemv_workspace_bytes(m, n, r, b))
+
+
+def af1_linear_gemv(layer, x, b: int, y, ws, ws_bytes: int, stream=None, check=True) -> int:
+    ref = ctypes.byref(layer) if layer is not None else None
+    st = lib().af1_linear_gemv(ref, _addr(x), b, _addr(y), _addr(ws), ws_bytes, _stream(stream))
+    if check:
+        _check(st, "af1_linear_gemv")
+    return st
+
+
+def af1_gemm_workspace_bytes(m, n, r, T) -> int:
+    return int(lib().af1_gemm_workspace_bytes(m, n, r, T))
+
+
+def af1_linear_gemm(layer, x, T: int, y, ws, ws_bytes: int, stream=None, check=True) -> int:
+    ref = ctypes.byref(layer) if layer is not None else None
+    st = lib().af1_linear_gemm(ref, _addr(x), T, _addr(y), _addr(ws), ws_bytes, _stream(stream))
+    if check:
+        _check(st, "af1_linear_gemm")
+    return st
+
+
+def af1_storage_bits(m, n, r) -> int:
+    return int(lib().af1_storage_bits(m, n, r))
+
+
+def af1_budget_rank(m, n) -> int:
+    return int(lib().af1_budget_rank(m, n))

@@ -1,0 +1,160 @@
+// C ABI of the AF1 factorized binary linear (declared in include/af1.h).
+//
+// Every entry point validates its arguments on the host before it enqueues
+// anything: an argument error returns a status with no launch and no side
+// effect.  The launchers in af1_internal.h then only enqueue kernels on the
+// caller's stream.
+#include <stdint.h>
+
+#include "af1.h"
+#include "af1_internal.h"
+
+namespace {
+
+constexpr const char *kVersion = "af1-mi355x 0.1.0 (gfx950)";
+
+bool dim_ok(int64_t d) { return d >= 32 && d <= AF1_MAX_DIM && d % 32 == 0; }
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Span {
+  uintptr_t lo, hi;  // [lo, hi)
+};
+
+Span span(const void *p, uint64_t bytes) {
+  const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+  return Span{lo, lo + (uintptr_t)bytes};
+}
+
+bool overlap(Span a, Span b) {
+  if (a.lo == a.hi || b.lo == b.hi) return false;
+  return a.lo < b.hi && b.lo < a.hi;
+}
+
+hipStream_t as_stream(void *s) { return static_cast<hipStream_t>(s); }
+
+// Checks shared by the two forward entry points.  `rows_in` is the batch /
+// token count, `ws_need` the workspace the chosen kernels require.
+af1_status check_forward(const af1_factorized_linear *L, const uint16_t *x,
+                         int64_t rows_in, int64_t max_rows, uint16_t *y,
+                         const void *ws, size_t ws_bytes, size_t ws_need) {
+  if (!L) return AF1_ERR_NULL;
+  if (!dim_ok(L->m) || !dim_ok(L->n) || !dim_ok(L->r)) return AF1_ERR_SHAPE;
+  if (!L->Bu || !L->Bv || !L->s_out || !L->s_mid || !L->s_in || !x || !y) return AF1_ERR_NULL;
+  if (rows_in < 1 || rows_in > max_rows) return AF1_ERR_BATCH;
+  if (!aligned16(L->Bu) || !aligned16(L->Bv) || !aligned16(L->s_out) ||
+      !aligned16(L->s_mid) || !aligned16(L->s_in) || !aligned16(x) || !aligned16(y) ||
+      (ws && !aligned16(ws)))
+    return AF1_ERR_ALIGN;
+  if (ws_need > 0 && (!ws || ws_bytes < ws_need)) return AF1_ERR_WORKSPACE;
+
+  const int64_t m = L->m, n = L->n, r = L->r;
+  const Span sy = span(y, (uint64_t)rows_in * m * 2);
+  const Span sws = span(ws, ws ? ws_need : 0);
+  const Span inputs[] = {span(x, (uint64_t)rows_in * n * 2), span(L->Bu, (uint64_t)m * r / 8),
+                         span(L->Bv, (uint64_t)r * n / 8), span(L->s_out, (uint64_t)m * 2),
+                         span(L->s_mid, (uint64_t)r * 2), span(L->s_in, (uint64_t)n * 2)};
+  for (const Span &in : inputs)
+    if (overlap(sy, in) || overlap(sws, in)) return AF1_ERR_ALIAS;
+  if (overlap(sy, sws)) return AF1_ERR_ALIAS;
+  return AF1_OK;
+}
+
+af1_status hip_status(hipError_t e) { return e == hipSuccess ? AF1_OK : AF1_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+af1_status af1_pack(const void *src, int32_t src_dtype, int64_t rows, int64_t cols,
+                    uint32_t *dst, void *stream) {
+  if (!src || !dst) return AF1_ERR_NULL;
+  if (src_dtype < AF1_SRC_F32 || src_dtype > AF1_SRC_I8) return AF1_ERR_DTYPE;
+  if (rows < 0 || cols < 32 || cols % 32 != 0 || cols > ((int64_t)1 << 40) ||
+      (rows > 0 && rows > (((int64_t)1 << 40) / cols)))
+    return AF1_ERR_SHAPE;
+  if (!aligned16(src) || !aligned16(dst)) return AF1_ERR_ALIGN;
+  static const int kElemBytes[] = {4, 2, 2, 1};
+  const uint64_t n = (uint64_t)rows * (uint64_t)cols;
+  if (overlap(span(src, n * kElemBytes[src_dtype]), span(dst, n / 8))) return AF1_ERR_ALIAS;
+  return hip_status(af1::launch_pack(src, src_dtype, rows, cols, dst, as_stream(stream)));
+}
+
+af1_status af1_unpack(const uint32_t *words, int64_t rows, int64_t cols, int8_t *dst,
+                      void *stream) {
+  if (!words || !dst) return AF1_ERR_NULL;
+  if (rows < 0 || cols < 32 || cols % 32 != 0 || cols > ((int64_t)1 << 40) ||
+      (rows > 0 && rows > (((int64_t)1 << 40) / cols)))
+    return AF1_ERR_SHAPE;
+  if (!aligned16(words) || !aligned16(dst)) return AF1_ERR_ALIGN;
+  const uint64_t n = (uint64_t)rows * (uint64_t)cols;
+  if (overlap(span(words, n / 8), span(dst, n))) return AF1_ERR_ALIAS;
+  return hip_status(af1::launch_unpack(words, rows, cols, dst, as_stream(stream)));
+}
+
+size_t af1_gemv_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t b) {
+  if (!dim_ok(m) || !dim_ok(n) || !dim_ok(r) || b < 1 || b > AF1_GEMV_MAX_BATCH) return 0;
+  return af1::gemv_workspace_bytes(m, n, r, b);
+}
+
+af1_status af1_linear_gemv(const af1_factorized_linear *L, const uint16_t *x, int64_t b,
+                           uint16_t *y, void *ws, size_t ws_bytes, void *stream) {
+  const size_t need = (L && dim_ok(L->m) && dim_ok(L->n) && dim_ok(L->r) && b >= 1 &&
+                       b <= AF1_GEMV_MAX_BATCH)
+                          ? af1::gemv_workspace_bytes(L->m, L->n, L->r, b)
+                          : 0;
+  const af1_status st = check_forward(L, x, b, AF1_GEMV_MAX_BATCH, y, ws, ws_bytes, need);
+  if (st != AF1_OK) return st;
+  return hip_status(af1::launch_gemv(L->m, L->n, L->r, L->Bu, L->Bv, L->s_out, L->s_mid,
+                                     L->s_in, x, b, y, ws, as_stream(stream)));
+}
+
+size_t af1_gemm_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
+  if (!dim_ok(m) || !dim_ok(n) || !dim_ok(r) || T < 1 || T > AF1_GEMM_MAX_TOKENS) return 0;
+  return af1::gemm_workspace_bytes(m, n, r, T);
+}
+
+af1_status af1_linear_gemm(const af1_factorized_linear *L, const uint16_t *x, int64_t T,
+                           uint16_t *y, void *ws, size_t ws_bytes, void *stream) {
+  const size_t need = (L && dim_ok(L->m) && dim_ok(L->n) && dim_ok(L->r) && T >= 1 &&
+                       T <= AF1_GEMM_MAX_TOKENS)
+                          ? af1::gemm_workspace_bytes(L->m, L->n, L->r, T)
+                          : 0;
+  const af1_status st = check_forward(L, x, T, AF1_GEMM_MAX_TOKENS, y, ws, ws_bytes, need);
+  if (st != AF1_OK) return st;
+  return hip_status(af1::launch_gemm(L->m, L->n, L->r, L->Bu, L->Bv, L->s_out, L->s_mid,
+                                     L->s_in, x, T, y, ws, as_stream(stream)));
+}
+
+int64_t af1_storage_bits(int64_t m, int64_t n, int64_t r) {
+  if (m < 0 || n < 0 || r < 0) return -1;
+  return r * (m + n) + 16 * (m + n + r);
+}
+
+int64_t af1_budget_rank(int64_t m, int64_t n) {
+  // r*(m+n) + 16*(m+n+r) <= m*n  <=>  r <= (m*n - 16*(m+n)) / (m+n+16)
+  if (m <= 0 || n <= 0) return 0;
+  const int64_t num = m * n - 16 * (m + n);
+  if (num <= 0) return 0;
+  const int64_t rmax = num / (m + n + 16);
+  return rmax - rmax % 32;
+}
+
+const char *af1_status_string(int32_t status) {
+  switch (status) {
+    case AF1_OK: return "ok";
+    case AF1_ERR_NULL: return "a required pointer is NULL";
+    case AF1_ERR_SHAPE: return "dimension <= 0, not a multiple of 32, or too large";
+    case AF1_ERR_BATCH: return "batch or token count outside the accepted range";
+    case AF1_ERR_ALIGN: return "a device pointer is not 16-byte aligned";
+    case AF1_ERR_WORKSPACE: return "workspace missing or too small";
+    case AF1_ERR_ALIAS: return "an output overlaps an input or the workspace";
+    case AF1_ERR_HIP: return "the HIP runtime rejected a launch";
+    case AF1_ERR_DTYPE: return "unknown source element type";
+    default: return "unknown status";
+  }
+}
+
+const char *af1_version(void) { return kVersion; }
+
+}  // extern "C"

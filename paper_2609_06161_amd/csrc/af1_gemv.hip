@@ -1,0 +1,519 @@
+// Decode-regime forward of the factorized binary linear (paper App. A.2.1,
+// Diag form, evaluated right to left; Sec. 4.1 deployable form):
+//
+//   stage 1:  t[b, k] = s_mid[k] * sum_j Bv[k, j] * (s_in[j] * x[b, j])
+//   stage 2:  y[b, i] = bf16( s_out[i] * sum_k Bu[i, k] * t[b, k] )
+//
+// Both stages are one kernel template: a +-1 row product against a vector
+// staged in LDS, then a per-row scale.  The products run on the gfx950
+// matrix cores (v_mfma_f32_16x16x32_bf16): rows of the sign matrix are the
+// M dimension, the batch is N (lanes with no batch row read zeros), the
+// input columns are K.
+//
+// Exactness.  A sign becomes the bf16 value +-1 (exact).  The fp32 input
+// (s_in*x is exact in fp32: 8 x 11 significant bits) is split into
+// hi = bf16(v) and lo = bf16(v - hi); two MFMAs per tile consume hi and lo,
+// so the operand error is below 2^-17 relative, and accumulation is fp32.
+//
+// Sign expansion.  Within a 32-bit word, columns p and p+16 (p = 0..15) are
+// paired: one shift moves bit p to bit 15 and bit p+16 to bit 31, and one
+// three-input bit operation merges those two sign bits into 0x3F80 (bf16
+// 1.0) -- two VALU ops per two operands.  The MFMA K order is free as long
+// as the A (signs) and B (inputs) operands agree, so the LDS copy of the
+// input is stored in the same (p, p+16) pairs.
+//
+// Latency.  A decode-size call is bound by launch and memory latency, not
+// bandwidth.  Each workgroup owns a 16-row tile; its 8 waves split the
+// columns into groups of 8 words.  Every wave first issues the loads of its
+// sign words (buffer loads: out-of-range lanes read zeros, no branches, so
+// no early waits), then the loads of its own slice of the input, converts
+// that slice to bf16 hi/lo pairs in LDS (waves read only what they wrote,
+// so no workgroup barrier is needed), and runs its MFMAs with the LDS
+// operand reads double-buffered.  The waves' 16x16 results are added
+// through LDS.  When b * K is too large for one LDS slab the columns are
+// split over workgroups ("slabs"); each slab writes a partial sum and the
+// last slab of a row tile to finish (atomic counter) adds the partials in
+// slab order, so the result is deterministic.
+#include <utility>
+
+#include "af1_device.h"
+#include "af1_internal.h"
+
+namespace af1 {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float float2v __attribute__((ext_vector_type(2)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWaves = 8;
+constexpr int kThreads = kWaves * 64;
+constexpr int kTileRows = 16;        // MFMA M
+constexpr int kGroupWords = 8;       // one 8-byte load per lane covers 16 rows x 8 words
+constexpr int kMaxGroups = 8;        // groups per wave (single pass)
+constexpr int kSlot = 144;           // LDS bytes per (batch row, word): 64 hi + 64 lo + 16 pad
+constexpr int kLdsBytes = 65536;
+constexpr int kRedBytes = kWaves * 64 * 16;
+// The LDS budget caps a slab at (kLdsBytes - kSlot) / kSlot = 454 words,
+// which the waves cover in a single pass.
+static_assert(kWaves * kMaxGroups * kGroupWords >= (kLdsBytes - kSlot) / kSlot, "one pass");
+// Staging: a unit is 8 columns (+ their partners 16 on) of one batch row;
+// a wave stages my_groups * 16 * b units, two per lane per pass.  Within the
+// LDS budget that is at most 4 passes (b = 16, one group).
+constexpr int kStageIters = 4;
+constexpr int kOob = (int)0x80000000u;  // a buffer offset past any resource
+
+// Calls f(std::integral_constant<int, I>) for I = 0 .. N-1, fully unrolled,
+// so that register arrays indexed by I stay in registers.
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// Buffer resource over [base, base + bytes): loads at offsets beyond `bytes`
+// return zero instead of faulting.  Word 3 selects raw 32-bit dword access.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, int64_t bytes) {
+  const int n = bytes > 0x7fffffff ? 0x7fffffff : (bytes < 0 ? 0 : (int)bytes);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, n, 0x00020000);
+}
+
+// Two fp32 -> packed bf16 (round to nearest even), one instruction on gfx950.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo_half, float hi_half) {
+  const float2v f = {lo_half, hi_half};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
+}
+
+struct UnitRaw {
+  u32x4 a, b, c, d;
+};
+
+// Raw data of one staging unit: columns c0 .. c0+7 and c0+16 .. c0+23 of one
+// batch row (x and s_in for the first stage, fp32 t for the second).  `off`
+// is the element offset of column c0 in the input, kOob for no unit.
+template <bool kInX>
+__device__ __forceinline__ UnitRaw load_unit(__amdgpu_buffer_rsrc_t xres,
+                                             __amdgpu_buffer_rsrc_t sres, int off, int col,
+                                             int part_off = 0) {
+  UnitRaw r;
+  if constexpr (kInX) {
+    const int xo = off == kOob ? kOob : off * 2;
+    const int so = off == kOob ? kOob : col * 2;
+    r.a = __builtin_amdgcn_raw_buffer_load_b128(xres, xo, 0, 0);
+    r.b = __builtin_amdgcn_raw_buffer_load_b128(xres, xo + 32, 0, 0);
+    r.c = __builtin_amdgcn_raw_buffer_load_b128(sres, so, 0, 0);
+    r.d = __builtin_amdgcn_raw_buffer_load_b128(sres, so + 32, 0, 0);
+  } else {
+    const int to = off == kOob ? kOob : (off + part_off) * 4;
+    r.a = __builtin_amdgcn_raw_buffer_load_b128(xres, to, 0, 0);
+    r.b = __builtin_amdgcn_raw_buffer_load_b128(xres, to + 16, 0, 0);
+    r.c = __builtin_amdgcn_raw_buffer_load_b128(xres, to + 64, 0, 0);
+    r.d = __builtin_amdgcn_raw_buffer_load_b128(xres, to + 80, 0, 0);
+  }
+  return r;
+}
+
+// fp32 values of a unit: v[d] = column c0+d, v[8+d] = column c0+16+d.  For
+// the fp32 input a second set of raw data (a second partial sum) is added.
+template <bool kInX>
+__device__ __forceinline__ void unit_values(const UnitRaw &r, float (&v)[16],
+                                            const UnitRaw *r2 = nullptr) {
+  if constexpr (kInX) {
+    const uint32_t xd[8] = {r.a.x, r.a.y, r.a.z, r.a.w, r.b.x, r.b.y, r.b.z, r.b.w};
+    const uint32_t sd[8] = {r.c.x, r.c.y, r.c.z, r.c.w, r.d.x, r.d.y, r.d.z, r.d.w};
+#pragma unroll
+    for (int d = 0; d < 8; ++d) {
+      v[2 * d] = bf16_to_f32(xd[d] & 0xffffu) * f16_to_f32((uint16_t)(sd[d] & 0xffffu));
+      v[2 * d + 1] = bf16_to_f32(xd[d] >> 16) * f16_to_f32((uint16_t)(sd[d] >> 16));
+    }
+  } else {
+    const u32x4 q4[4] = {r.a, r.b, r.c, r.d};
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[4 * k + e] = __uint_as_float(q4[k][e]);
+    if (r2) {
+      const u32x4 p4[4] = {r2->a, r2->b, r2->c, r2->d};
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[4 * k + e] += __uint_as_float(p4[k][e]);
+    }
+  }
+}
+
+// Store a unit as hi/lo pair dwords (pair 8h+d = columns c0+d and c0+16+d):
+// hi = bf16(v), lo = bf16(v - hi).
+__device__ __forceinline__ void store_unit(uint8_t *slot_base, int h, const float (&v)[16]) {
+  uint32_t hi[8], lo[8];
+#pragma unroll
+  for (int d = 0; d < 8; ++d) {
+    hi[d] = pack_bf16x2(v[d], v[8 + d]);
+    lo[d] = pack_bf16x2(v[d] - bf16_to_f32(hi[d] & 0xffffu), v[8 + d] - bf16_to_f32(hi[d] >> 16));
+  }
+  uint4 *slot = reinterpret_cast<uint4 *>(slot_base);
+  slot[2 * h] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+  slot[2 * h + 1] = make_uint4(hi[4], hi[5], hi[6], hi[7]);
+  slot[4 + 2 * h] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+  slot[4 + 2 * h + 1] = make_uint4(lo[4], lo[5], lo[6], lo[7]);
+}
+
+// Output modes of a stage launch.
+constexpr int kModeFinal = 0;     // one slab: write the scaled result
+constexpr int kModeLastSlab = 1;  // several slabs: the last one to finish adds them
+constexpr int kModePartial = 2;   // several slabs: each writes its scaled partial sum
+                                  // (the next stage adds them while staging)
+
+// Arguments are scalars, most urgent first, so that they are preloaded into
+// SGPRs at wave launch instead of being fetched from the kernarg segment.
+//
+// kHiLoCols (b <= 8): the bf16 hi and lo parts of batch row beta occupy MFMA
+// columns 2*beta and 2*beta+1, so one MFMA per tile covers both; otherwise
+// (b up to 16) columns are batch rows and hi and lo take one MFMA each.
+template <bool kInX, bool kOutY, bool kHiLoCols>
+__global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
+    const uint32_t *__restrict__ M, const void *__restrict__ in,
+    const uint16_t *__restrict__ s_in, const uint16_t *__restrict__ row_scale, int rows,
+    int wpr, int slab_words, int b, int nslabs, int mode, int in_parts,
+    void *__restrict__ out, float *__restrict__ part, uint32_t *__restrict__ cnt) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // scalar: wave-uniform
+  const int tile = blockIdx.x;
+  const int slab = blockIdx.y;
+  const int row0 = tile * kTileRows;
+  const int w_begin = slab * slab_words;
+  const int w_count = min(slab_words, wpr - w_begin);
+  const int ngroups = (w_count + kGroupWords - 1) / kGroupWords;
+  // this wave's groups: g = wave + kWaves * i, i < my_groups
+  const int my_groups = ngroups > wave ? (ngroups - wave + kWaves - 1) / kWaves : 0;
+  const size_t K = (size_t)wpr * 32;
+
+  // A-operand lanes: row rho, word pair q.  B-operand lanes: column n, pair q.
+  const int rho = lane & 15;
+  const int q = lane >> 4;
+  const int ncol = lane & 15;
+  const int beta = kHiLoCols ? (ncol >> 1) : ncol;
+  const int hl_col = kHiLoCols ? (ncol & 1) : 0;
+
+  // 1. Sign words of this wave's groups, issued before anything else as
+  //    unconditional buffer loads.  Lanes past the last row or the slab's
+  //    last word read data that never reaches a stored output: a ragged
+  //    group's tail meets the zero slot on the B side, and rows past `rows`
+  //    are not written.  Groups past my_groups use an out-of-range offset:
+  //    no branch, so the compiler has no join at which to wait for the loads.
+  const __amdgpu_buffer_rsrc_t mres =
+      buffer_rsrc(M + (size_t)row0 * wpr, (int64_t)(rows - row0) * wpr * 4);
+  u32x2 wv[kMaxGroups];
+#pragma unroll
+  for (int i = 0; i < kMaxGroups; ++i) {
+    const int wl = (wave + kWaves * i) * kGroupWords + 2 * q;
+    const int off = i < my_groups ? (rho * wpr + w_begin + wl) * 4 : kOob;
+    wv[i] = __builtin_amdgcn_raw_buffer_load_b64(mres, off, 0, 0);
+  }
+
+  // 2. Stage this wave's columns of the input as bf16 hi/lo (p, p+16) pairs,
+  //    one 144-byte slot per (batch row, word); slot 0 holds zeros for lanes
+  //    with no batch row and for the tail of a ragged group.  A wave reads
+  //    only slots it wrote itself, and a wave's LDS operations execute in
+  //    order, so no workgroup barrier is needed before the products.
+  uint8_t *xs = lds + kSlot;
+  if (lane < kSlot / 16) reinterpret_cast<uint4 *>(lds)[lane] = make_uint4(0u, 0u, 0u, 0u);
+  {
+    const int units_per_group = b * kGroupWords * 2;
+    const int nunits = my_groups * units_per_group;
+    const int part_elems = b * (int)K;  // stride between partial input arrays
+    const __amdgpu_buffer_rsrc_t xres =
+        buffer_rsrc(in, (int64_t)b * K * (kInX ? 2 : 4) * (kInX ? 1 : in_parts));
+    const __amdgpu_buffer_rsrc_t sres = buffer_rsrc(s_in, kInX ? (int64_t)K * 2 : 0);
+    const bool two_parts = !kInX && in_parts > 1;
+#pragma unroll
+    for (int it = 0; it < kStageIters; ++it) {
+      const int c0 = it * 2 * 64;
+      if (c0 >= nunits) break;  // wave-uniform
+      int slot_off[2], half[2], off[2], col[2];
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        const int cu = c0 + 64 * k + lane;
+        const int i = cu / units_per_group;
+        const int rem = cu - i * units_per_group;
+        const int bb = rem / (kGroupWords * 2);
+        const int r2 = rem - bb * (kGroupWords * 2);
+        const int wl = (wave + kWaves * i) * kGroupWords + (r2 >> 1);
+        const bool ok = cu < nunits && wl < w_count;
+        half[k] = r2 & 1;
+        col[k] = (w_begin + wl) * 32 + 8 * half[k];
+        off[k] = ok ? (int)(bb * K) + col[k] : kOob;
+        slot_off[k] = ok ? (bb * w_count + wl) * kSlot : -1;
+      }
+      const bool two = c0 + 64 < nunits;  // wave-uniform
+      const UnitRaw raw0 = load_unit<kInX>(xres, sres, off[0], col[0]);
+      UnitRaw raw1, raw0b, raw1b;
+      if (two) raw1 = load_unit<kInX>(xres, sres, off[1], col[1]);
+      if (two_parts) {
+        raw0b = load_unit<kInX>(xres, sres, off[0], col[0], part_elems);
+        if (two) raw1b = load_unit<kInX>(xres, sres, off[1], col[1], part_elems);
+      }
+      float v[16];
+      if (slot_off[0] >= 0) {
+        unit_values<kInX>(raw0, v, two_parts ? &raw0b : nullptr);
+        store_unit(xs + slot_off[0], half[0], v);
+      }
+      if (two && slot_off[1] >= 0) {
+        unit_values<kInX>(raw1, v, two_parts ? &raw1b : nullptr);
+        store_unit(xs + slot_off[1], half[1], v);
+      }
+    }
+  }
+  // Row scale of the output this thread writes at the end (loaded after the
+  // staging loads so that waiting for it waits for nothing else).
+  const int orow_l = tid >> 4;
+  const int obeta = tid & 15;
+  const int orow = row0 + orow_l;
+  const bool active = tid < kTileRows * 16 && obeta < b && orow < rows;
+  const uint32_t rscale_bits = __builtin_amdgcn_raw_buffer_load_b16(
+      buffer_rsrc(row_scale, (int64_t)rows * 2), orow * 2, 0, 0);
+  __builtin_amdgcn_wave_barrier();
+
+  // 3. Products.  Step s = (group i = s / 2, word u = s % 2); independent
+  //    accumulator chains per pair quad t (and per hi/lo when they are not
+  //    in columns); the B operands of the next step are read from LDS while
+  //    this step's MFMAs run.  Only lanes whose column carries a batch row
+  //    read LDS; the others keep zero operands.
+  uint32_t kSignMask, kOne;
+  asm volatile("v_mov_b32 %0, 0x80008000" : "=v"(kSignMask));
+  asm volatile("v_mov_b32 %0, 0x3f803f80" : "=v"(kOne));
+  constexpr int kChains = kHiLoCols ? 1 : 2;
+  constexpr int kReads = 4 * kChains;
+  floatx4 acc[4][kChains];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int hl = 0; hl < kChains; ++hl) acc[t][hl] = floatx4{0.f, 0.f, 0.f, 0.f};
+  const int nsteps = my_groups * 2;
+  const bool b_lane = beta < b;
+  auto b_ptr = [&](int st) -> const uint8_t * {
+    const int wl = (wave + kWaves * (st >> 1)) * kGroupWords + 2 * q + (st & 1);
+    return wl < w_count ? xs + ((size_t)beta * w_count + wl) * kSlot + 64 * hl_col : lds;
+  };
+  uint4 bop[2][kReads];
+#pragma unroll
+  for (int k = 0; k < kReads; ++k) bop[0][k] = bop[1][k] = make_uint4(0u, 0u, 0u, 0u);
+  if (nsteps > 0 && b_lane) {
+    const uint8_t *bs = b_ptr(0);
+#pragma unroll
+    for (int k = 0; k < kReads; ++k) bop[0][k] = *reinterpret_cast<const uint4 *>(bs + 16 * k);
+  }
+  static_for<kMaxGroups * 2>([&](auto ST) {
+    constexpr int st = decltype(ST)::value;
+    constexpr int cur = st & 1;
+    if (st < nsteps) {  // wave-uniform
+      if (st + 1 < nsteps && b_lane) {
+        const uint8_t *bs = b_ptr(st + 1);
+#pragma unroll
+        for (int k = 0; k < kReads; ++k)
+          bop[cur ^ 1][k] = *reinterpret_cast<const uint4 *>(bs + 16 * k);
+      }
+      const uint32_t w = wv[st >> 1][st & 1];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        uint4 a;
+        a.x = ((w << (15 - (4 * t + 0))) & kSignMask) | (kOne & ~kSignMask);
+        a.y = ((w << (15 - (4 * t + 1))) & kSignMask) | (kOne & ~kSignMask);
+        a.z = ((w << (15 - (4 * t + 2))) & kSignMask) | (kOne & ~kSignMask);
+        a.w = ((w << (15 - (4 * t + 3))) & kSignMask) | (kOne & ~kSignMask);
+        const bf16x8 av = __builtin_bit_cast(bf16x8, a);
+#pragma unroll
+        for (int hl = 0; hl < kChains; ++hl)
+          acc[t][hl] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              av, __builtin_bit_cast(bf16x8, bop[cur][4 * hl + t]), acc[t][hl], 0, 0, 0);
+      }
+    }
+  });
+  floatx4 tot = acc[0][0];
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int hl = 0; hl < kChains; ++hl)
+      if (t | hl) tot += acc[t][hl];
+
+  // 4. Add the waves' 16x16 tiles through LDS (after every wave is done
+  //    reading its staged operands).  Accumulator layout: lane l holds rows
+  //    4*(l/16) + i (i = 0..3) of column l mod 16.
+  __syncthreads();
+  float4 *red = reinterpret_cast<float4 *>(lds);
+  red[wave * 64 + lane] = make_float4(tot[0], tot[1], tot[2], tot[3]);
+  __syncthreads();
+  float sum = 0.f;
+  if (tid < kTileRows * 16) {
+    const float *redf = reinterpret_cast<const float *>(lds);
+    const int c0 = kHiLoCols ? 2 * obeta : obeta;
+    const int l0 = 16 * (orow_l >> 2) + (c0 & 15);
+#pragma unroll
+    for (int wv2 = 0; wv2 < kWaves; ++wv2) {
+      sum += redf[(wv2 * 64 + l0) * 4 + (orow_l & 3)];
+      if constexpr (kHiLoCols) sum += redf[(wv2 * 64 + l0 + 1) * 4 + (orow_l & 3)];
+    }
+  }
+
+  if (mode == kModeLastSlab) {
+    // Publish this slab's partial sum; the last slab of the tile to arrive
+    // adds all partials in slab order and resets the tile's counter.
+    if (active) part[((size_t)slab * b + obeta) * rows + orow] = sum;
+    __threadfence();
+    __syncthreads();
+    __shared__ uint32_t s_last;
+    if (tid == 0) s_last = (atomicAdd(&cnt[tile], 1u) == (uint32_t)(nslabs - 1));
+    __syncthreads();
+    if (!s_last) return;
+    __threadfence();
+    if (active) {
+      sum = 0.f;
+      for (int sl = 0; sl < nslabs; ++sl)
+        sum += __hip_atomic_load(&part[((size_t)sl * b + obeta) * rows + orow], __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (tid == 0) cnt[tile] = 0u;
+  }
+  if (active) {
+    const float v = sum * f16_to_f32((uint16_t)rscale_bits);
+    size_t o = (size_t)obeta * rows + orow;
+    if (mode == kModePartial) o += (size_t)slab * b * rows;
+    if constexpr (kOutY)
+      static_cast<uint16_t *>(out)[o] = f32_to_bf16(v);
+    else
+      static_cast<float *>(out)[o] = v;
+  }
+}
+
+// Largest slab (in words, a multiple of kGroupWords) whose staged input fits LDS.
+int slab_words_for(int64_t b, int64_t wpr) {
+  int64_t w = (kLdsBytes - kSlot) / (kSlot * b);
+  w -= w % kGroupWords;
+  if (w < kGroupWords) w = kGroupWords;
+  return (int)(w < wpr ? w : ((wpr + kGroupWords - 1) / kGroupWords) * kGroupWords);
+}
+
+size_t lds_bytes_for(int64_t b, int slab_words, int64_t wpr) {
+  const int64_t w = slab_words < wpr ? slab_words : wpr;
+  size_t stage = (size_t)kSlot * (1 + (size_t)b * w);
+  return stage > (size_t)kRedBytes ? stage : (size_t)kRedBytes;
+}
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+// How one stage splits its columns.  Slabs are forced when b * K does not
+// fit the LDS budget (the last slab of each tile adds the partials).  When a
+// single slab fits but the row tiles alone would leave most compute units
+// idle, the columns are split in two and the next stage adds the two
+// partial results while staging its input.
+struct StagePlan {
+  int slab_words, nslabs, mode;
+};
+
+StagePlan plan_stage(int64_t rows, int64_t wpr, int64_t b, bool allow_partial) {
+  StagePlan p{slab_words_for(b, wpr), 0, kModeFinal};
+  p.nslabs = (int)((wpr + p.slab_words - 1) / p.slab_words);
+  if (p.nslabs > 1) {
+    p.mode = kModeLastSlab;
+    return p;
+  }
+  const int64_t tiles = (rows + kTileRows - 1) / kTileRows;
+  const int64_t groups = (wpr + kGroupWords - 1) / kGroupWords;
+  if (allow_partial && tiles < 192 && groups >= 2 && b <= 8) {
+    p.slab_words = (int)(((groups + 1) / 2) * kGroupWords);
+    p.nslabs = (int)((wpr + p.slab_words - 1) / p.slab_words);
+    p.mode = p.nslabs > 1 ? kModePartial : kModeFinal;
+  }
+  return p;
+}
+
+struct WsLayout {
+  StagePlan p1, p2;
+  size_t t, part1, cnt1, part2, cnt2, total;
+};
+
+WsLayout ws_layout(int64_t m, int64_t n, int64_t r, int64_t b) {
+  WsLayout L{};
+  L.p1 = plan_stage(r, n / 32, b, true);
+  L.p2 = plan_stage(m, r / 32, b, false);
+  const int tparts = L.p1.mode == kModePartial ? L.p1.nslabs : 1;
+  size_t off = 0;
+  L.t = off;
+  off += align256((size_t)tparts * b * r * 4);
+  L.part1 = off;
+  if (L.p1.mode == kModeLastSlab) off += align256((size_t)L.p1.nslabs * b * r * 4);
+  L.cnt1 = off;
+  if (L.p1.mode == kModeLastSlab) off += align256((size_t)((r + kTileRows - 1) / kTileRows) * 4);
+  L.part2 = off;
+  if (L.p2.mode == kModeLastSlab) off += align256((size_t)L.p2.nslabs * b * m * 4);
+  L.cnt2 = off;
+  if (L.p2.mode == kModeLastSlab) off += align256((size_t)((m + kTileRows - 1) / kTileRows) * 4);
+  L.total = off;
+  return L;
+}
+
+struct StageArgs {
+  const uint32_t *M;
+  const void *in;
+  const uint16_t *s_in;
+  const uint16_t *row_scale;
+  int rows, wpr, b, in_parts;
+  void *out;
+  float *part;
+  uint32_t *cnt;
+};
+
+template <bool kInX, bool kOutY>
+hipError_t launch_stage(const StageArgs &a, const StagePlan &p, hipStream_t s) {
+  // The kernel stages at most kStageIters * 128 units per wave.
+  const int groups = (p.slab_words + kGroupWords - 1) / kGroupWords;
+  if ((int64_t)((groups + kWaves - 1) / kWaves) * a.b * kGroupWords * 2 > kStageIters * 128)
+    return hipErrorInvalidValue;
+  dim3 grid((unsigned)((a.rows + kTileRows - 1) / kTileRows), (unsigned)p.nslabs);
+  const size_t lds = lds_bytes_for(a.b, p.slab_words, a.wpr);
+  if (a.b <= 8)
+    gemv_stage_kernel<kInX, kOutY, true><<<grid, kThreads, lds, s>>>(
+        a.M, a.in, a.s_in, a.row_scale, a.rows, a.wpr, p.slab_words, a.b, p.nslabs, p.mode,
+        a.in_parts, a.out, a.part, a.cnt);
+  else
+    gemv_stage_kernel<kInX, kOutY, false><<<grid, kThreads, lds, s>>>(
+        a.M, a.in, a.s_in, a.row_scale, a.rows, a.wpr, p.slab_words, a.b, p.nslabs, p.mode,
+        a.in_parts, a.out, a.part, a.cnt);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t gemv_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t b) {
+  return ws_layout(m, n, r, b).total;
+}
+
+hipError_t launch_gemv(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
+                       const uint32_t *Bv, const uint16_t *s_out,
+                       const uint16_t *s_mid, const uint16_t *s_in,
+                       const uint16_t *x, int64_t b, uint16_t *y, void *ws,
+                       hipStream_t s) {
+  const WsLayout L = ws_layout(m, n, r, b);
+  uint8_t *base = static_cast<uint8_t *>(ws);
+  float *t = reinterpret_cast<float *>(base + L.t);
+  const StageArgs s1{Bv, x, s_in, s_mid, (int)r, (int)(n / 32), (int)b, 1, t,
+                     reinterpret_cast<float *>(base + L.part1),
+                     reinterpret_cast<uint32_t *>(base + L.cnt1)};
+  hipError_t e = launch_stage<true, false>(s1, L.p1, s);
+  if (e != hipSuccess) return e;
+  const int tparts = L.p1.mode == kModePartial ? L.p1.nslabs : 1;
+  const StageArgs s2{Bu, t, nullptr, s_out, (int)m, (int)(r / 32), (int)b, tparts, y,
+                     reinterpret_cast<float *>(base + L.part2),
+                     reinterpret_cast<uint32_t *>(base + L.cnt2)};
+  return launch_stage<false, true>(s2, L.p2, s);
+}
+
+}  // namespace af1

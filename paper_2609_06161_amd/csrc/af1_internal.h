@@ -1,0 +1,30 @@
+// Host-side launchers behind the C ABI.  Arguments are already validated by
+// af1_api.cpp; each launcher only enqueues kernels and reports whether the
+// HIP runtime accepted them.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace af1 {
+
+hipError_t launch_pack(const void *src, int dtype, int64_t rows, int64_t cols,
+                       uint32_t *dst, hipStream_t s);
+hipError_t launch_unpack(const uint32_t *words, int64_t rows, int64_t cols,
+                         int8_t *dst, hipStream_t s);
+
+size_t gemv_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t b);
+hipError_t launch_gemv(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
+                       const uint32_t *Bv, const uint16_t *s_out,
+                       const uint16_t *s_mid, const uint16_t *s_in,
+                       const uint16_t *x, int64_t b, uint16_t *y, void *ws,
+                       hipStream_t s);
+
+size_t gemm_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T);
+hipError_t launch_gemm(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
+                       const uint32_t *Bv, const uint16_t *s_out,
+                       const uint16_t *s_mid, const uint16_t *s_in,
+                       const uint16_t *x, int64_t T, uint16_t *y, void *ws,
+                       hipStream_t s);
+
+}  // namespace af1

@@ -1,0 +1,64 @@
+"""Device-resident factorized layer: the packed signs and fp16 scales held as
+torch CUDA tensors (plumbing only), plus the C descriptor that points at them.
+"""
+import numpy as np
+import torch
+
+from . import af1
+
+_VIEW = {np.dtype(np.uint32): np.int32, np.dtype(np.uint16): np.int16,
+         np.dtype(np.uint8): np.uint8, np.dtype(np.int8): np.int8,
+         np.dtype(np.float32): np.float32, np.dtype(np.float16): np.float16}
+
+
+def to_device(a: np.ndarray, device="cuda") -> torch.Tensor:
+    """Copy a host array to the device byte for byte (unsigned 32/16-bit
+    patterns travel as signed views of the same bits)."""
+    a = np.ascontiguousarray(a)
+    return torch.from_numpy(a.view(_VIEW[a.dtype])).to(device)
+
+
+def bf16_bits_to_f64(t: torch.Tensor) -> np.ndarray:
+    """Host float64 values of a tensor of bfloat16 bit patterns."""
+    u = t.detach().cpu().numpy().view(np.uint16).astype(np.uint32) << 16
+    return u.view(np.float32).astype(np.float64)
+
+
+class DeviceLayer:
+    def __init__(self, m, n, r, Bu, Bv, s_out, s_mid, s_in, device="cuda"):
+        self.m, self.n, self.r = int(m), int(n), int(r)
+        self.Bu = to_device(Bu, device)
+        self.Bv = to_device(Bv, device)
+        self.s_out = to_device(s_out, device)
+        self.s_mid = to_device(s_mid, device)
+        self.s_in = to_device(s_in, device)
+        self.desc = af1.make_layer(self.m, self.n, self.r, self.Bu, self.Bv,
+                                   self.s_out, self.s_mid, self.s_in)
+
+    @classmethod
+    def from_host(cls, lin, device="cuda"):
+        return cls(lin.m, lin.n, lin.r, lin.Bu, lin.Bv, lin.s_out, lin.s_mid, lin.s_in, device)
+
+    def storage_bytes(self) -> int:
+        return af1.af1_storage_bits(self.m, self.n, self.r) // 8
+
+    def gemv(self, x: torch.Tensor, y: torch.Tensor = None, ws: torch.Tensor = None, stream=None):
+        b = x.shape[0]
+        if y is None:
+            y = torch.empty((b, self.m), dtype=torch.int16, device=x.device)
+        need = af1.af1_gemv_workspace_bytes(self.m, self.n, self.r, b)
+        if ws is None:
+            # zero-filled: the decode path keeps arrival counters here
+            ws = torch.zeros(max(need, 256), dtype=torch.uint8, device=x.device)
+        af1.af1_linear_gemv(self.desc, x, b, y, ws, ws.numel(), stream)
+        return y
+
+    def gemm(self, x: torch.Tensor, y: torch.Tensor = None, ws: torch.Tensor = None, stream=None):
+        T = x.shape[0]
+        if y is None:
+            y = torch.empty((T, self.m), dtype=torch.int16, device=x.device)
+        need = af1.af1_gemm_workspace_bytes(self.m, self.n, self.r, T)
+        if ws is None:
+            ws = torch.empty(max(need, 256), dtype=torch.uint8, device=x.device)
+        af1.af1_linear_gemm(self.desc, x, T, y, ws, ws.numel(), stream)
+        return y

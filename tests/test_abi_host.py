@@ -1,0 +1,154 @@
+"""Host-only checks of the C ABI: the library loads, exports every entry
+point the header declares, its host arithmetic agrees with the oracle, and
+every argument error is returned before anything is enqueued (fake device
+addresses are safe here because no call below passes validation)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2609_06161_amd import af1, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "af1.h")
+
+BASE = 0x7F00_0000_0000          # fake, 16-byte aligned "device" addresses
+MB = 1 << 20
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(af1_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) >= 10
+    L = af1.lib()
+    for name in names:
+        assert hasattr(L, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", af1.LIB_PATH],
+                         capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (af1_\w+)", out))
+    assert set(names) == exported
+
+
+def test_version_and_status_strings():
+    assert "gfx950" in af1.af1_version()
+    for st in range(0, 9):
+        assert af1.status_string(st)
+    assert af1.status_string(99) == "unknown status"
+
+
+def test_storage_bits_matches_oracle(oracle):
+    rng = np.random.default_rng(0)
+    for _ in range(200):
+        m, n, r = (int(v) for v in rng.integers(1, 1 << 15, size=3))
+        assert af1.af1_storage_bits(m, n, r) == oracle.storage_bits(m, n, r)
+    assert af1.af1_storage_bits(-1, 2, 3) == -1
+
+
+def test_budget_rank_matches_oracle(oracle):
+    for name, (m, n, r) in synth.SHAPES.items():
+        assert af1.af1_budget_rank(m, n) == r, name
+    rng = np.random.default_rng(1)
+    for _ in range(300):
+        m, n = (int(v) for v in rng.integers(1, 40000, size=2))
+        assert af1.af1_budget_rank(m, n) == oracle.budget_rank(m, n), (m, n)
+    assert af1.af1_budget_rank(0, 5) == 0
+    assert af1.af1_budget_rank(32, 32) == 0      # scales alone exceed the budget
+
+
+# --------------------------------------------------------------------------
+# argument validation (no launch happens on any of these paths)
+# --------------------------------------------------------------------------
+
+def fake_layer(m=4096, n=4096, r=2016, base=BASE):
+    # Bu, Bv, s_out, s_mid, s_in laid out 64 MB apart
+    return af1.make_layer(m, n, r, base, base + 64 * MB, base + 128 * MB,
+                          base + 129 * MB, base + 130 * MB)
+
+
+X = BASE + 200 * MB
+Y = BASE + 300 * MB
+WS = BASE + 400 * MB
+
+
+def gemv(layer, x=X, b=1, y=Y, ws=WS, ws_bytes=1 << 30):
+    return af1.af1_linear_gemv(layer, x, b, y, ws, ws_bytes, stream=0, check=False)
+
+
+def gemm(layer, x=X, T=16, y=Y, ws=WS, ws_bytes=1 << 30):
+    return af1.af1_linear_gemm(layer, x, T, y, ws, ws_bytes, stream=0, check=False)
+
+
+@pytest.mark.parametrize("fn", [gemv, gemm])
+def test_forward_validation(fn):
+    assert fn(None) == af1.AF1_ERR_NULL
+    for m, n, r in [(0, 4096, 32), (4096, 4096, 33), (4096, 4064 + 16, 32),
+                    (af1.AF1_MAX_DIM + 32, 4096, 32), (-32, 64, 32)]:
+        assert fn(fake_layer(m, n, r)) == af1.AF1_ERR_SHAPE, (m, n, r)
+    L = fake_layer()
+    L.Bv = None
+    assert fn(L) == af1.AF1_ERR_NULL
+    assert fn(fake_layer(), x=None) == af1.AF1_ERR_NULL
+    assert fn(fake_layer(), y=None) == af1.AF1_ERR_NULL
+    assert fn(fake_layer(), x=X + 8) == af1.AF1_ERR_ALIGN
+    L = fake_layer()
+    L.s_mid = BASE + 129 * MB + 2
+    assert fn(L) == af1.AF1_ERR_ALIGN
+    # output overlapping an input or the workspace
+    assert fn(fake_layer(), y=X + 16) == af1.AF1_ERR_ALIAS
+    assert fn(fake_layer(), y=BASE + 128 * MB) == af1.AF1_ERR_ALIAS
+    assert fn(fake_layer(), y=WS) == af1.AF1_ERR_ALIAS
+    assert fn(fake_layer(), ws=BASE + 64 * MB) == af1.AF1_ERR_ALIAS
+
+
+def test_gemv_batch_and_workspace_validation():
+    L = fake_layer()
+    assert gemv(L, b=0) == af1.AF1_ERR_BATCH
+    assert gemv(L, b=17) == af1.AF1_ERR_BATCH
+    need = af1.af1_gemv_workspace_bytes(4096, 4096, 2016, 8)
+    assert need > 0
+    assert gemv(L, b=8, ws_bytes=need - 1) == af1.AF1_ERR_WORKSPACE
+    assert gemv(L, b=8, ws=None, ws_bytes=0) == af1.AF1_ERR_WORKSPACE
+    assert af1.af1_gemv_workspace_bytes(4096, 4096, 2016, 0) == 0
+    assert af1.af1_gemv_workspace_bytes(4096, 4096, 2016, 17) == 0
+    assert af1.af1_gemv_workspace_bytes(4096, 4096, 33, 1) == 0
+
+
+def test_gemm_token_and_workspace_validation():
+    L = fake_layer()
+    assert gemm(L, T=0) == af1.AF1_ERR_BATCH
+    assert gemm(L, T=(1 << 20) + 1) == af1.AF1_ERR_BATCH
+    need = af1.af1_gemm_workspace_bytes(4096, 4096, 2016, 2048)
+    assert need >= 2048 * 2016 * 2
+    assert gemm(L, T=2048, ws_bytes=need - 1) == af1.AF1_ERR_WORKSPACE
+
+
+def test_pack_validation():
+    P = af1.af1_pack
+    assert P(None, 0, 4, 64, Y, stream=0, check=False) == af1.AF1_ERR_NULL
+    assert P(X, 0, 4, 64, None, stream=0, check=False) == af1.AF1_ERR_NULL
+    assert P(X, 7, 4, 64, Y, stream=0, check=False) == af1.AF1_ERR_DTYPE
+    assert P(X, -1, 4, 64, Y, stream=0, check=False) == af1.AF1_ERR_DTYPE
+    assert P(X, 0, 4, 48, Y, stream=0, check=False) == af1.AF1_ERR_SHAPE
+    assert P(X, 0, 4, 0, Y, stream=0, check=False) == af1.AF1_ERR_SHAPE
+    assert P(X, 0, -1, 64, Y, stream=0, check=False) == af1.AF1_ERR_SHAPE
+    assert P(X + 4, 0, 4, 64, Y, stream=0, check=False) == af1.AF1_ERR_ALIGN
+    assert P(X, 0, 4, 64, X + 512, stream=0, check=False) == af1.AF1_ERR_ALIAS
+    U = af1.af1_unpack
+    assert U(None, 4, 64, Y, stream=0, check=False) == af1.AF1_ERR_NULL
+    assert U(X, 4, 40, Y, stream=0, check=False) == af1.AF1_ERR_SHAPE
+    assert U(X, 4, 64, Y + 1, stream=0, check=False) == af1.AF1_ERR_ALIGN
+    assert U(X, 4, 64, X + 16, stream=0, check=False) == af1.AF1_ERR_ALIAS
+
+
+def test_binding_raises_on_error():
+    with pytest.raises(af1.Af1Error) as ei:
+        af1.af1_linear_gemv(None, X, 1, Y, WS, 1 << 20, stream=0)
+    assert ei.value.status == af1.AF1_ERR_NULL
