@@ -215,8 +215,13 @@ __global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
 #pragma unroll
   for (int i = 0; i < kMaxGroups; ++i) {
     const int wl = (wave + kWaves * i) * kGroupWords + 2 * q;
+    // Two 4-byte loads, each range-checked on its own: with an odd number of
+    // words per row the second word of the last pair lies past the row
+    // (and, for the last row, past the buffer).  Out-of-slab words are
+    // harmless (they meet the zero slot), but must not hide a valid word.
     const int off = i < my_groups ? (rho * wpr + w_begin + wl) * 4 : kOob;
-    wv[i] = __builtin_amdgcn_raw_buffer_load_b64(mres, off, 0, 0);
+    wv[i].x = __builtin_amdgcn_raw_buffer_load_b32(mres, off, 0, 0);
+    wv[i].y = __builtin_amdgcn_raw_buffer_load_b32(mres, off == kOob ? kOob : off + 4, 0, 0);
   }
 
   // 2. Stage this wave's columns of the input as bf16 hi/lo (p, p+16) pairs,

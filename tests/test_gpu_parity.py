@@ -113,6 +113,37 @@ def test_gemv_named_shapes(oracle, name, b):
     assert err <= TOL
 
 
+def elementwise_ok(y, ref, rel=2 ** -7, abs_rms=1e-3):
+    """Every element within bf16-level error of its reference, relative to
+    the element and to its row's rms (abs_rms), so that a single wrong
+    element fails: dropping one 32-column word of a 2016-term sum moves an
+    element by about 0.13 rms."""
+    y = np.asarray(y, np.float64)
+    ref = np.asarray(ref, np.float64)
+    scale = np.sqrt(np.mean(ref ** 2, axis=1, keepdims=True))
+    bad = np.abs(y - ref) > rel * np.abs(ref) + abs_rms * scale
+    return not bad.any(), np.argwhere(bad)[:5]
+
+
+@pytest.mark.parametrize("m,n,r,b", [(4096, 4096, 2016, 1), (1056, 2080, 4064, 3),
+                                     (96, 1056, 96, 1)])
+def test_gemv_elementwise_including_last_rows(oracle, m, n, r, b):
+    """Odd word counts (r/32 = 63, 127; n/32 = 65, 33): the last row's last
+    word is read next to the end of its buffer."""
+    lin = synth.make_linear(77 + r, m, n, r, b)
+    ok, where = elementwise_ok(gpu_gemv(lin), oracle_y(oracle, lin))
+    assert ok, where
+
+
+@pytest.mark.parametrize("m,n,r,T", [(4096, 4096, 2016, 40), (1056, 2080, 4064, 33)])
+def test_gemm_elementwise_including_last_rows(oracle, m, n, r, T):
+    lin = synth.make_linear(91 + r, m, n, r, T)
+    # the intermediate is rounded once to fp16 (2^-12 relative, summed over r
+    # terms: about 2.4e-4 rms of absolute error, with rare 4-5 sigma tails)
+    ok, where = elementwise_ok(gpu_gemm(lin), oracle_y(oracle, lin), rel=2 ** -6, abs_rms=6e-3)
+    assert ok, where
+
+
 def test_gemv_zero_input_gives_exact_zero():
     lin = synth.make_linear(3, 1024, 1024, 480, 2)
     y = gpu_gemv(lin, np.zeros_like(lin.x))
