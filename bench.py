@@ -45,6 +45,11 @@ def parse():
     p.add_argument("--no-gemm", action="store_true")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
+    p.add_argument("--only", choices=("all", "gemv", "gemm"), default="all",
+                   help="profiling aid: run one part only")
+    p.add_argument("--calibrate-copy", action="store_true",
+                   help="profiling aid: first run a 64 MiB device copy five times, the "
+                        "known-size reference for scaling hardware byte counters")
     return p.parse_args()
 
 
@@ -163,6 +168,18 @@ def main():
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
 
+    if args.calibrate_copy:
+        src = torch.ones(64 << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    if args.only == "gemm":
+        out = bench_gemm(args, torch, stream)
+        print(json.dumps({"gemm": out}), flush=True)
+        return
+
     g = bench_gemv(args, torch, stream)
     us = g["ms_per_step"] * 1e3
     achieved = g["alg_bytes"] / (g["ms_per_step"] * 1e-3) / 1e9
@@ -190,10 +207,10 @@ def main():
                      "traffic": None,
                      "alg_bytes_per_launch": g["alg_bytes"]},
     }
-    if not args.no_gemm:
+    if not args.no_gemm and args.only == "all":
         result["gemm"] = bench_gemm(args, torch, stream)
         result["gemm"]["peak_tflops"] = MFMA_F16_PEAK_TFLOPS
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.only == "all":
         result["cpu_baseline"] = bench_cpu_oracle(args)
     print(json.dumps(result), flush=True)
 

@@ -6,26 +6,35 @@
 //
 // Both are "activations x signed column scale" contractions,
 //   C[t, n] = rowscale[n] * sum_c A[t, c] * (sign(W[n, c]) * colscale[c]),
-// with A fp16 (G1 converts the bf16 input on the way into LDS, exact for
-// |x| < 65504) and W bit-packed.  Flipping the sign bit of the fp16 column
-// scale keeps both MFMA operands exact; accumulation is fp32.
+// with A fp16 and W bit-packed.  Flipping the sign bit of the fp16 column
+// scale keeps both MFMA operands exact (x is converted bf16 -> fp16, exact
+// for |x| < 65504); accumulation is fp32.
+//
+// Pair order.  Within a 32-bit sign word, columns p and p+16 (p = 0..15)
+// form one MFMA operand dword, so one shift and one three-input bit
+// operation produce two fp16 operands (column-scale pair XOR the two sign
+// bits).  The activations are kept in the same order: inside every group
+// of 32 columns, column p sits at position 2p and column p+16 at 2p+1.  A
+// pre-pass writes x in that order (converting bf16 to fp16 once, instead
+// of once per weight-row tile), and G1 writes Z in that order, so both GEMMs
+// stage their activation tiles with plain copies.
 //
 // Tiling.  A 256-thread workgroup computes a 128 (tokens) x 256 (weight
-// rows) tile of C over K steps of 64 columns.  The activation tile is the
+// rows) tile of C over K steps of 128 columns.  The activation tile is the
 // only large operand (sign bits are 1/16 of its bytes per element), so the
 // tile is wide in weight rows.  Each of the four waves owns 64 weight rows
 // for all 128 tokens (4 x 2 blocks of v_mfma_f32_32x32x16_f16), so every
 // sign bit is expanded exactly once, in registers, straight into an MFMA
-// operand: within a 32-bit word, columns p and p+16 form one operand dword,
-// so one shift and one three-input bit operation produce two fp16 operands
-// (column-scale pair XOR the two sign bits).  The activation tile is stored
-// in LDS in the same (p, p+16) pair order, and so is the column scale.
+// operand.
 //
-// Pipeline.  LDS holds two activation tiles; each K step issues the global
-// loads of the next step (activations, sign words, column scale) before its
-// own MFMAs, then converts and stores the next tile and meets one barrier.
-// Tiles are assigned so that the workgroups on one XCD (blockIdx mod 8) work
-// on a contiguous range of tiles and share activation rows in their L2.
+// Pipeline.  LDS holds two sets of (activation tile, column-scale pairs,
+// sign words); each K step issues the global loads of the next step before
+// its own MFMAs, consumes them only after the MFMAs, and meets one barrier.
+// Per-step addresses move the scalar buffer base.  Columns past K
+// read a zero column scale, so they contribute nothing whatever the
+// activation or sign data they meet.  Tiles are assigned so that the
+// workgroups of one XCD (blockIdx mod 8) work on a contiguous range of
+// tiles and share activation rows in their L2.
 #include "af1_device.h"
 #include "af1_internal.h"
 
@@ -41,12 +50,18 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int BM = 128;          // tokens per tile
 constexpr int BN = 256;          // weight rows per tile
-constexpr int BK = 64;           // columns per K step (two sign words)
+constexpr int kWords = 4;        // sign words per K step
+constexpr int BK = 32 * kWords;  // columns per K step
 constexpr int kThreads = 256;
-constexpr int kRowBytes = 144;   // LDS bytes per token row: 64 fp16 + 16 pad
+constexpr int kRowBytes = BK * 2 + 16;             // LDS bytes per token row (+16 pad)
 constexpr int kATile = BM * kRowBytes;
-constexpr int kCsBytes = 128;    // column-scale pairs of one K step
+constexpr int kCsBytes = kWords * 16 * 4;          // column-scale pairs of one K step
+constexpr int kWBytes = BN * kWords * 4;           // sign words of one K step
+constexpr int kAChunks = BM * BK * 2 / 16 / kThreads;  // 16-byte activation chunks per thread
+constexpr int kLdsBytes = 2 * (kATile + kCsBytes + kWBytes);
 constexpr int kOob = (int)0x80000000u;
+static_assert(kAChunks * kThreads * 16 == BM * BK * 2, "activation chunks");
+static_assert(4 * kWords <= kThreads, "column-scale staging");
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, int64_t bytes) {
   const int n = bytes > 0x7fffffff ? 0x7fffffff : (bytes < 0 ? 0 : (int)bytes);
@@ -59,30 +74,44 @@ __device__ __forceinline__ uint32_t pack_f16x2(float lo_half, float hi_half) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, half2v));
 }
 
-// Pair dwords (column c+d, column c+16+d), d = 0..7, from the 16-byte loads
-// of columns c..c+7 (lo) and c+16..c+23 (hi).  bf16 input is converted to
-// fp16; fp16 input only has its halves interleaved.
-template <bool kBf16>
-__device__ __forceinline__ void make_pairs(const u32x4 &lo, const u32x4 &hi, uint32_t (&d)[8]) {
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const uint32_t a = lo[e], b = hi[e];
-    if constexpr (kBf16) {
-      d[2 * e] = pack_f16x2(__uint_as_float(a << 16), __uint_as_float(b << 16));
-      d[2 * e + 1] = pack_f16x2(__uint_as_float(a & 0xffff0000u), __uint_as_float(b & 0xffff0000u));
-    } else {
-      d[2 * e] = __builtin_amdgcn_perm(b, a, 0x05040100u);      // (a.lo, b.lo)
-      d[2 * e + 1] = __builtin_amdgcn_perm(b, a, 0x07060302u);  // (a.hi, b.hi)
-    }
-  }
+// Position of column c inside its 32-column group in pair order.
+__device__ __forceinline__ int pair_pos(int c) {
+  return (c & ~31) + 2 * (c & 15) + ((c >> 4) & 1);
 }
 
-template <bool kABf16, bool kOutBf16>
+// x (bf16, [T][K]) -> xp (fp16, [T][K], pair order).  One thread per 16
+// columns: 8 columns c .. c+7 and their partners c+16 .. c+23 become the
+// pair dwords 8h .. 8h+7 of their group.
+__global__ __launch_bounds__(256) void pair_order_kernel(const uint16_t *__restrict__ x,
+                                                         uint16_t *__restrict__ xp, int T, int K) {
+  const int units_per_row = K / 16;
+  const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (u >= (int64_t)T * units_per_row) return;
+  const int t = (int)(u / units_per_row);
+  const int ur = (int)(u % units_per_row);
+  const int c = (ur >> 1) * 32 + 8 * (ur & 1);
+  const uint16_t *src = x + (size_t)t * K + c;
+  const u32x4 lo = *reinterpret_cast<const u32x4 *>(src);
+  const u32x4 hi = *reinterpret_cast<const u32x4 *>(src + 16);
+  uint32_t d[8];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    d[2 * e] = pack_f16x2(__uint_as_float(lo[e] << 16), __uint_as_float(hi[e] << 16));
+    d[2 * e + 1] = pack_f16x2(__uint_as_float(lo[e] & 0xffff0000u), __uint_as_float(hi[e] & 0xffff0000u));
+  }
+  uint4 *dst = reinterpret_cast<uint4 *>(xp + (size_t)t * K + (c & ~31) + 2 * (c & 15));
+  dst[0] = make_uint4(d[0], d[1], d[2], d[3]);
+  dst[1] = make_uint4(d[4], d[5], d[6], d[7]);
+}
+
+// C = rowscale * (A_pairorder x (sign(W) * colscale)^T).  kOutBf16: C is
+// bf16 in natural column order (y); otherwise fp16 in pair order (Z).
+template <bool kOutBf16>
 __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     const uint16_t *__restrict__ A, int T, int K, const uint32_t *__restrict__ W, int N,
     const uint16_t *__restrict__ colscale, const uint16_t *__restrict__ rowscale,
     uint16_t *__restrict__ C) {
-  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * kATile + 2 * kCsBytes];
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -95,55 +124,58 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   const int t0 = (L / nN) * BM;
   const int n0 = (L % nN) * BN;
 
-  const int kw = K / 32;                // sign words per row
-  const int nk = (kw + 1) / 2;          // K steps (the last may hold one word)
-  const __amdgpu_buffer_rsrc_t ares = buffer_rsrc(A, (int64_t)T * K * 2);
-  const __amdgpu_buffer_rsrc_t wres = buffer_rsrc(W, (int64_t)N * kw * 4);
-  const __amdgpu_buffer_rsrc_t cres = buffer_rsrc(colscale, (int64_t)K * 2);
+  const int kw = K / 32;                       // sign words per row
+  const int nk = (kw + kWords - 1) / kWords;   // K steps (the last may be partial)
 
-  // Staging roles.  Activation units: (token, word wi, half h) -> columns
-  // 32wi+8h .. +7 and +16 .. +23; thread tid handles units tid and tid+256.
-  // Column scale: threads 0..7 each build 4 pair dwords.
-  int a_tok[2], a_col[2], a_dst[2];
+  // Staging roles (fixed per thread; a step only adds a scalar offset).
+  // Activations: 16-byte chunk q = tid + 256k of the tile -> token q / 16,
+  // byte 16 (q mod 16) of the token's K-step slice (already in pair order).
+  // Column scale: threads 0 .. 4*kWords-1 load columns c .. c+3 and c+16 ..
+  // c+19 of word tid/4 and build 4 pair dwords.  Sign words: thread tid
+  // stages row n0 + tid.
+  int a_off[kAChunks], a_dst[kAChunks];
 #pragma unroll
-  for (int k = 0; k < 2; ++k) {
-    const int u = tid + kThreads * k;
-    const int tok = u >> 2, wi = (u >> 1) & 1, h = u & 1;
-    a_tok[k] = t0 + tok;
-    a_col[k] = 32 * wi + 8 * h;
-    a_dst[k] = tok * kRowBytes + (16 * wi + 8 * h) * 4;
+  for (int k = 0; k < kAChunks; ++k) {
+    const int q = tid + kThreads * k;
+    const int tok = q / (BK * 2 / 16), part = q % (BK * 2 / 16);
+    a_off[k] = t0 + tok < T ? ((t0 + tok) * K) * 2 + 16 * part : kOob;
+    a_dst[k] = tok * kRowBytes + 16 * part;
   }
-  const int cs_wi = tid >> 2, cs_part = tid & 3;  // valid for tid < 8
+  const bool cs_thread = tid < 4 * kWords;
+  const int cs_off = cs_thread ? (32 * (tid >> 2) + 4 * (tid & 3)) * 2 : kOob;
+  const int w_off = n0 + tid < N ? (n0 + tid) * kw * 4 : kOob;
 
-  u32x4 a_raw[2][2];
+  u32x4 a_raw[kAChunks];
   u32x2 cs_raw[2];
+  uint32_t w_raw[kWords];
+  // All of a step's loads are consumed only by store_stage, after the MFMAs
+  // of the previous step, so the MFMAs never wait on global memory.  Every
+  // thread issues every load (out-of-range offsets where there is nothing
+  // to load), so the count of outstanding loads never depends on a branch.
+  //  The step offset moves the (scalar) resource base rather than being a
+  //  scalar offset: range checking covers the vector offset only, so every
+  //  access is checked against what remains of its buffer from the base.
   auto load_stage = [&](int step) {
-    const int k0 = step * BK;
+    const int ka = step * BK * 2;   // byte offset of the step in an A row / colscale
+    const int kwb = step * kWords * 4;
+    const __amdgpu_buffer_rsrc_t as = buffer_rsrc(A + step * BK, (int64_t)T * K * 2 - ka);
+    const __amdgpu_buffer_rsrc_t cs = buffer_rsrc(colscale + step * BK, (int64_t)K * 2 - ka);
+    const __amdgpu_buffer_rsrc_t ws = buffer_rsrc(W + step * kWords, (int64_t)N * kw * 4 - kwb);
 #pragma unroll
-    for (int k = 0; k < 2; ++k) {
-      const int col = k0 + a_col[k];
-      const bool ok = a_tok[k] < T && col < K;
-      const int off = ok ? (a_tok[k] * K + col) * 2 : kOob;
-      a_raw[k][0] = __builtin_amdgcn_raw_buffer_load_b128(ares, off, 0, 0);
-      a_raw[k][1] = __builtin_amdgcn_raw_buffer_load_b128(ares, ok ? off + 32 : kOob, 0, 0);
-    }
-    if (tid < 8) {
-      const int c = k0 + 32 * cs_wi + 4 * cs_part;
-      cs_raw[0] = __builtin_amdgcn_raw_buffer_load_b64(cres, c * 2, 0, 0);        // c..c+3
-      cs_raw[1] = __builtin_amdgcn_raw_buffer_load_b64(cres, (c + 16) * 2, 0, 0); // c+16..
-    }
+    for (int k = 0; k < kAChunks; ++k)
+      a_raw[k] = __builtin_amdgcn_raw_buffer_load_b128(as, a_off[k], 0, 0);
+    cs_raw[0] = __builtin_amdgcn_raw_buffer_load_b64(cs, cs_off, 0, 0);
+    cs_raw[1] = __builtin_amdgcn_raw_buffer_load_b64(cs, cs_off == kOob ? kOob : cs_off + 32, 0, 0);
+#pragma unroll
+    for (int i = 0; i < kWords; ++i)
+      w_raw[i] = __builtin_amdgcn_raw_buffer_load_b32(ws, w_off == kOob ? kOob : w_off + 4 * i, 0, 0);
   };
   auto store_stage = [&](int buf) {
     uint8_t *at = lds + buf * kATile;
 #pragma unroll
-    for (int k = 0; k < 2; ++k) {
-      uint32_t d[8];
-      make_pairs<kABf16>(a_raw[k][0], a_raw[k][1], d);
-      uint4 *dst = reinterpret_cast<uint4 *>(at + a_dst[k]);
-      dst[0] = make_uint4(d[0], d[1], d[2], d[3]);
-      dst[1] = make_uint4(d[4], d[5], d[6], d[7]);
-    }
-    if (tid < 8) {
+    for (int k = 0; k < kAChunks; ++k)
+      *reinterpret_cast<u32x4 *>(at + a_dst[k]) = a_raw[k];
+    if (cs_thread) {
       uint32_t d[4];
       d[0] = __builtin_amdgcn_perm(cs_raw[1].x, cs_raw[0].x, 0x05040100u);
       d[1] = __builtin_amdgcn_perm(cs_raw[1].x, cs_raw[0].x, 0x07060302u);
@@ -152,25 +184,15 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       reinterpret_cast<uint4 *>(lds + 2 * kATile + buf * kCsBytes)[tid] =
           make_uint4(d[0], d[1], d[2], d[3]);
     }
+    uint32_t *wdst =
+        reinterpret_cast<uint32_t *>(lds + 2 * kATile + 2 * kCsBytes + buf * kWBytes) + tid * kWords;
+#pragma unroll
+    for (int i = 0; i < kWords; ++i) wdst[i] = w_raw[i];
   };
 
-  // Sign words of this wave's rows: lane l, block j -> row n0 + 64*wave +
-  // 32*j + (l mod 32); both words of the K step.
-  const int wrow0 = n0 + 64 * wave + (lane & 31);
-  auto load_w = [&](int step, u32x2 (&wb)[2]) {
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int row = wrow0 + 32 * j;
-      const int w0 = 2 * step;
-      // Two 4-byte loads, each range-checked on its own: with an odd word
-      // count the second word of the last step lies past the row (and, for
-      // the last row, past the buffer); it reads as zero.
-      const int off = row < N ? (row * kw + w0) * 4 : kOob;
-      wb[j].x = __builtin_amdgcn_raw_buffer_load_b32(wres, off, 0, 0);
-      wb[j].y = __builtin_amdgcn_raw_buffer_load_b32(wres, (row < N && w0 + 1 < kw) ? off + 4 : kOob,
-                                                     0, 0);
-    }
-  };
+  // This lane's weight rows: block j -> tile row 64*wave + 32*j + (l mod 32).
+  const int wrow_l = 64 * wave + (lane & 31);
+  const int wrow0 = n0 + wrow_l;
 
   floatx16 acc[4][2];
 #pragma unroll
@@ -183,9 +205,7 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   uint32_t kSignMask;
   asm volatile("v_mov_b32 %0, 0x80008000" : "=v"(kSignMask));
 
-  u32x2 wcur[2], wnext[2];
   load_stage(0);
-  load_w(0, wcur);
   store_stage(0);
   __syncthreads();
 
@@ -193,14 +213,18 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   for (int step = 0; step < nk; ++step) {
     const int buf = step & 1;
     const bool more = step + 1 < nk;
-    if (more) {
-      load_stage(step + 1);
-      load_w(step + 1, wnext);
-    }
-    const uint8_t *at = lds + buf * kATile;
+    if (more) load_stage(step + 1);
+    const uint8_t *at = lds + buf * kATile + (lane & 31) * kRowBytes + 16 * g;
     const uint4 *cs = reinterpret_cast<const uint4 *>(lds + 2 * kATile + buf * kCsBytes);
+    const uint32_t *ws =
+        reinterpret_cast<const uint32_t *>(lds + 2 * kATile + 2 * kCsBytes + buf * kWBytes);
+    uint32_t wj[2][kWords];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int i = 0; i < kWords; ++i) wj[j][i] = ws[(wrow_l + 32 * j) * kWords + i];
+#pragma unroll
+    for (int ks = 0; ks < 2 * kWords; ++ks) {
       const int wi = ks >> 1, s = ks & 1;
       // column-scale pairs and activation fragments of this MFMA K step:
       // pair dwords 16wi + 8s + 4g .. +3
@@ -208,12 +232,11 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       half8 af[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        af[i] = *reinterpret_cast<const half8 *>(
-            at + (32 * i + (lane & 31)) * kRowBytes + (16 * wi + 8 * s + 4 * g) * 4);
+        af[i] = *reinterpret_cast<const half8 *>(at + 32 * i * kRowBytes + (16 * wi + 8 * s) * 4);
       const uint32_t cpair[4] = {c4.x, c4.y, c4.z, c4.w};
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        const uint32_t w = wi ? wcur[j].y : wcur[j].x;
+        const uint32_t w = wj[j][wi];
         uint32_t bd[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -226,11 +249,7 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bf, acc[i][j], 0, 0, 0);
       }
     }
-    if (more) {
-      store_stage(buf ^ 1);
-      wcur[0] = wnext[0];
-      wcur[1] = wnext[1];
-    }
+    if (more) store_stage(buf ^ 1);
     __syncthreads();
   }
 
@@ -241,6 +260,7 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     const int n = wrow0 + 32 * j;
     if (n >= N) continue;
     const float rs = rowscale ? f16_to_f32(rowscale[n]) : 1.0f;
+    const int cpos = kOutBf16 ? n : pair_pos(n);
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
 #pragma unroll
@@ -248,20 +268,21 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
         const int t = t0 + 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
         if (t < T) {
           const float v = acc[i][j][e] * rs;
-          C[(size_t)t * N + n] = kOutBf16 ? f32_to_bf16(v) : f32_to_f16(v);
+          C[(size_t)t * N + cpos] = kOutBf16 ? f32_to_bf16(v) : f32_to_f16(v);
         }
       }
     }
   }
 }
 
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
 }  // namespace
 
 size_t gemm_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
   (void)m;
-  (void)n;
-  const size_t z = (size_t)T * (size_t)r * sizeof(uint16_t);
-  return (z + 255) & ~(size_t)255;
+  // fp16 x in pair order, then the fp16 intermediate Z (pair order)
+  return align256((size_t)T * (size_t)n * 2) + align256((size_t)T * (size_t)r * 2);
 }
 
 hipError_t launch_gemm(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
@@ -269,20 +290,25 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
                        const uint16_t *s_mid, const uint16_t *s_in,
                        const uint16_t *x, int64_t T, uint16_t *y, void *ws,
                        hipStream_t s) {
-  // 32-bit element offsets inside the buffer resources
-  if (T * n > 0x3fffffff || T * r > 0x3fffffff || T * m > 0x7fffffff ||
-      m * (r / 32) > 0x1fffffff || r * (n / 32) > 0x1fffffff)
+  // byte offsets inside the buffer resources are 32-bit
+  if (T * n * 2 > 0x7fffffff || T * r * 2 > 0x7fffffff || m * (r / 32) * 4 > 0x7fffffff ||
+      r * (n / 32) * 4 > 0x7fffffff)
     return hipErrorInvalidValue;
-  uint16_t *Z = static_cast<uint16_t *>(ws);
-  const unsigned gy = (unsigned)((T + BM - 1) / BM);
-  dim3 g1((unsigned)((r + BN - 1) / BN), gy);
-  bingemm_kernel<true, false><<<g1, kThreads, 0, s>>>(x, (int)T, (int)n, Bv, (int)r, s_in,
-                                                      nullptr, Z);
+  uint16_t *xp = static_cast<uint16_t *>(ws);
+  uint16_t *Z = reinterpret_cast<uint16_t *>(static_cast<uint8_t *>(ws) + align256((size_t)T * n * 2));
+  const int64_t units = T * (n / 16);
+  pair_order_kernel<<<(unsigned)((units + 255) / 256), 256, 0, s>>>(x, xp, (int)T, (int)n);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  const unsigned gy = (unsigned)((T + BM - 1) / BM);
+  dim3 g1((unsigned)((r + BN - 1) / BN), gy);
+  bingemm_kernel<false><<<g1, kThreads, kLdsBytes, s>>>(xp, (int)T, (int)n, Bv, (int)r, s_in,
+                                                        nullptr, Z);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
   dim3 g2((unsigned)((m + BN - 1) / BN), gy);
-  bingemm_kernel<false, true><<<g2, kThreads, 0, s>>>(Z, (int)T, (int)r, Bu, (int)m, s_mid,
-                                                      s_out, y);
+  bingemm_kernel<true><<<g2, kThreads, kLdsBytes, s>>>(Z, (int)T, (int)r, Bu, (int)m, s_mid,
+                                                       s_out, y);
   return hipGetLastError();
 }
 
