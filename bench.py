@@ -28,6 +28,24 @@ HBM_PEAK_GBS = 8000.0
 MFMA_F16_PEAK_TFLOPS = 2500.0
 POOL_BYTES = 512 << 20          # > 2 x 256 MB MALL
 
+# HBM bytes per GEMV call from rocprofv3 FETCH_SIZE + WRITE_SIZE (scaled by a
+# 64 MiB copy calibration; see profiles/gemv_4096x4096_r2016_b1.md).  Valid
+# only for the kernel source it was measured on: reported as null as soon as
+# the source hash differs.
+GEMV_TRAFFIC = {"sources": ("paper_2609_06161_amd/csrc/af1_gemv.hip",
+                            "paper_2609_06161_amd/csrc/af1_device.h"),
+                "sha256": "80ed57a5f966d2af6c994ce2fe5a144e3613f8e6a4e0a38005b2c3c254b1b099",
+                "bytes_per_call": 2708887}
+
+
+def measured_gemv_traffic():
+    import hashlib
+    h = hashlib.sha256()
+    for rel in GEMV_TRAFFIC["sources"]:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return GEMV_TRAFFIC["bytes_per_call"] if h.hexdigest() == GEMV_TRAFFIC["sha256"] else None
+
 
 def gemv_algorithmic_bytes(m, n, r, b):
     """Packed signs + fp16 scales (storage bits / 8) + bf16 x and y."""
@@ -204,7 +222,7 @@ def main():
                    "us_per_layer_eager_launch": round(g["us_eager"], 3)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 5),
-                     "traffic": None,
+                     "traffic": measured_gemv_traffic(),
                      "alg_bytes_per_launch": g["alg_bytes"]},
     }
     if not args.no_gemm and args.only == "all":
