@@ -61,6 +61,7 @@ def parse():
     p.add_argument("--batch", type=int, default=1)
     p.add_argument("--gemm-steps", type=int, default=20)
     p.add_argument("--no-gemm", action="store_true")
+    p.add_argument("--no-decode-table", action="store_true")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--only", choices=("all", "gemv", "gemm"), default="all",
@@ -84,33 +85,49 @@ def time_events(fn, steps, stream):
     return s.elapsed_time(e)   # ms
 
 
-def bench_gemv(args, torch, stream):
-    from paper_2609_06161_amd import synth
-    from paper_2609_06161_amd.layer import DeviceLayer, to_device
-    m, n, r = synth.SHAPES["attn4096"]
-    b = args.batch
+class DevicePool:
+    """`count` distinct layers of one shape, generated on the device from a
+    seeded generator with the recipe's distributions (fair sign bits as
+    uniform 32-bit words, fp16 lognormal(0, 0.5) scales), so that a pool
+    larger than the 256 MB last-level cache is built in milliseconds."""
+
+    def __init__(self, torch, m, n, r, count, seed):
+        from paper_2609_06161_amd import af1
+        g = torch.Generator(device="cuda")
+        g.manual_seed(seed)
+        words = lambda k: torch.randint(-2 ** 31, 2 ** 31, (count, k), dtype=torch.int32,
+                                        device="cuda", generator=g)
+        scales = lambda k: (torch.empty((count, k), device="cuda").log_normal_(0.0, 0.5, generator=g)
+                            .to(torch.float16).view(torch.int16))
+        self.Bv, self.Bu = words(r * n // 32), words(m * r // 32)
+        self.s_in, self.s_mid, self.s_out = scales(n), scales(r), scales(m)
+        self.desc = [af1.make_layer(m, n, r, self.Bu[i], self.Bv[i], self.s_out[i],
+                                    self.s_mid[i], self.s_in[i]) for i in range(count)]
+        self.m, self.n, self.r, self.count = m, n, r, count
+
+
+def decode_time(args, torch, stream, m, n, r, b, seed, steps):
+    """µs per layer of the decode forward over a pool of distinct layers
+    (> 2x the last-level cache), eager and as a replayed HIP graph of one
+    pass over the pool."""
+    from paper_2609_06161_amd import af1, synth
+    from paper_2609_06161_amd.layer import to_device
     layer_bytes = r * (m + n) // 8
     pool = max(2, -(-POOL_BYTES // layer_bytes))
-    layers = []
-    for i in range(pool):
-        lin = synth.make_linear(1000 + i, m, n, r, b)
-        layers.append(DeviceLayer.from_host(lin))
-    x = to_device(synth.make_activations(7, b, n))
+    P = DevicePool(torch, m, n, r, pool, seed)
+    x = to_device(synth.make_activations(seed, b, n))
     y = torch.empty((b, m), dtype=torch.int16, device="cuda")
-    from paper_2609_06161_amd import af1
-    ws = torch.zeros(max(256, af1.af1_gemv_workspace_bytes(m, n, r, b)),
-                     dtype=torch.uint8, device="cuda")
+    ws = torch.zeros(max(256, af1.af1_gemv_workspace_bytes(m, n, r, b)), dtype=torch.uint8,
+                     device="cuda")
 
     def step(i):
         # stream=None: the binding uses torch's current stream (the capture
         # stream while a graph is being recorded)
-        layers[i % pool].gemv(x, y, ws, None)
+        af1.af1_linear_gemv(P.desc[i % pool], x, b, y, ws, ws.numel(), None)
 
-    # Eager: one Python -> C ABI call per layer.
-    time_events(step, args.warmup, stream)
-    ms_eager = time_events(step, args.steps, stream) / args.steps
-    # Graph: one pass over the pool recorded once, replayed; removes host
-    # launch overhead, the way a decode loop is run in serving.
+    time_events(step, min(args.warmup, pool), stream)
+    eager_steps = max(pool, steps // 4)
+    ms_eager = time_events(step, eager_steps, stream) / eager_steps
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
@@ -121,14 +138,31 @@ def bench_gemv(args, torch, stream):
     with torch.cuda.graph(graph):
         for i in range(pool):
             step(i)
-    replays = max(1, -(-args.steps // pool))
+    replays = max(1, -(-steps // pool))
     time_events(lambda i: graph.replay(), max(1, args.warmup // pool), stream)
     ms_graph = time_events(lambda i: graph.replay(), replays, stream) / (replays * pool)
-    ms_per_step = ms_graph
-    alg = gemv_algorithmic_bytes(m, n, r, b)
-    return dict(m=m, n=n, r=r, b=b, pool=pool, ms_per_step=ms_per_step, alg_bytes=alg,
-                pool_mb=pool * layer_bytes / 2**20, steps_timed=replays * pool,
-                us_eager=ms_eager * 1e3, us_graph=ms_graph * 1e3)
+    del graph, P
+    return dict(m=m, n=n, r=r, b=b, pool=pool, pool_mb=pool * layer_bytes / 2 ** 20,
+                steps_timed=replays * pool, us_graph=ms_graph * 1e3, us_eager=ms_eager * 1e3,
+                alg_bytes=gemv_algorithmic_bytes(m, n, r, b))
+
+
+DECODE_TABLE = [("sq1024", 1), ("attn4096", 8), ("kv1024x4096", 1), ("mlp_up14336x4096", 1),
+                ("mlp_up14336x4096", 4), ("mlp_up14336x4096", 16), ("mlp_down4096x14336", 1),
+                ("mlp_down4096x14336", 4), ("mlp_down4096x14336", 16)]
+
+
+def bench_decode_table(args, torch, stream):
+    from paper_2609_06161_amd import synth
+    out = {}
+    for name, b in DECODE_TABLE:
+        m, n, r = synth.SHAPES[name]
+        d = decode_time(args, torch, stream, m, n, r, b, 2000 + b, max(200, args.steps // 4))
+        out[f"{name}_b{b}"] = dict(us_per_layer=round(d["us_graph"], 3),
+                                   us_per_layer_eager=round(d["us_eager"], 3),
+                                   gbs=round(d["alg_bytes"] / (d["us_graph"] * 1e-6) / 1e9, 1),
+                                   alg_bytes=d["alg_bytes"])
+    return out
 
 
 def bench_gemm(args, torch, stream):
@@ -198,8 +232,11 @@ def main():
         print(json.dumps({"gemm": out}), flush=True)
         return
 
-    g = bench_gemv(args, torch, stream)
-    us = g["ms_per_step"] * 1e3
+    from paper_2609_06161_amd import synth
+    m, n, r = synth.SHAPES["attn4096"]
+    g = decode_time(args, torch, stream, m, n, r, args.batch, 1000, args.steps)
+    g["ms_per_step"] = g["us_graph"] * 1e-3
+    us = g["us_graph"]
     achieved = g["alg_bytes"] / (g["ms_per_step"] * 1e-3) / 1e9
     result = {
         "metric": METRIC,
@@ -225,6 +262,8 @@ def main():
                      "traffic": measured_gemv_traffic(),
                      "alg_bytes_per_launch": g["alg_bytes"]},
     }
+    if not args.no_decode_table and args.only == "all":
+        result["decode_table"] = bench_decode_table(args, torch, stream)
     if not args.no_gemm and args.only == "all":
         result["gemm"] = bench_gemm(args, torch, stream)
         result["gemm"]["peak_tflops"] = MFMA_F16_PEAK_TFLOPS

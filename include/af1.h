@@ -119,10 +119,12 @@ AF1_API af1_status af1_unpack(const uint32_t *words, int64_t rows, int64_t cols,
  *   x  : device, [b, n] bfloat16.       y : device, [b, m] bfloat16 (written).
  *   b  : 1 .. AF1_GEMV_MAX_BATCH.
  *   ws : device workspace of at least af1_gemv_workspace_bytes(m, n, r, b)
- *        bytes.  It must be zero-filled before its first use (it holds
- *        arrival counters); every call that completes leaves those counters
- *        at zero again, so one workspace serves any sequence of calls on one
- *        stream.  Calls that may overlap in time need distinct workspaces.
+ *        bytes.  Its first 512 KiB are a header of arrival counters at
+ *        fixed offsets; the header must be zero-filled before the
+ *        workspace's first use, and every call that
+ *        completes leaves the counters at zero again, so one workspace
+ *        serves any sequence of calls, of any shapes, on one stream.  Calls
+ *        that may overlap in time need distinct workspaces.
  * Arithmetic: s_in .* x in fp32 (exact), both sign products accumulated in
  * fp32, the rank-r intermediate kept in fp32, scales applied in fp32, y
  * rounded to bfloat16 (round to nearest even).  y must not overlap x, the

@@ -11,7 +11,7 @@
 
 namespace {
 
-constexpr const char *kVersion = "af1-mi355x 0.1.0 (gfx950)";
+constexpr const char *kVersion = "af1-mi355x 0.2.0 (gfx950)";
 
 bool dim_ok(int64_t d) { return d >= 32 && d <= AF1_MAX_DIM && d % 32 == 0; }
 

@@ -66,6 +66,18 @@ static_assert(kWaves * kMaxGroups * kGroupWords >= (kLdsBytes - kSlot) / kSlot, 
 constexpr int kStageIters = 4;
 constexpr int kOob = (int)0x80000000u;  // a buffer offset past any resource
 
+// The last-slab reduction hands partial sums between workgroups of one
+// launch with device-scope stores and loads (coherent across the XCDs' L2
+// caches) and relaxed atomics, ordered by waiting for this wave's memory
+// operations to complete.  A release/acquire fence at device scope would
+// write back and invalidate the whole L2 per workgroup, which costs tens of
+// microseconds at these grid sizes.
+__device__ __forceinline__ void wait_memory() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+__device__ __forceinline__ void store_device(float *p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Calls f(std::integral_constant<int, I>) for I = 0 .. N-1, fully unrolled,
 // so that register arrays indexed by I stay in registers.
 template <typename F, int... I>
@@ -170,61 +182,75 @@ constexpr int kModeLastSlab = 1;  // several slabs: the last one to finish adds 
 constexpr int kModePartial = 2;   // several slabs: each writes its scaled partial sum
                                   // (the next stage adds them while staging)
 
-// Arguments are scalars, most urgent first, so that they are preloaded into
-// SGPRs at wave launch instead of being fetched from the kernarg segment.
+// Where one workgroup's share of a stage lies: 16 rows starting at row0 and
+// the words [w_begin, w_begin + w_count) of those rows.  The wave's groups
+// are g = wave + kWaves * i, i < my_groups.
+struct Tile {
+  int tile, slab, row0, w_begin, w_count, my_groups;
+};
+
+__device__ __forceinline__ Tile make_tile(int tile, int slab, int wpr, int slab_words, int wave) {
+  Tile t;
+  t.tile = tile;
+  t.slab = slab;
+  t.row0 = tile * kTileRows;
+  t.w_begin = slab * slab_words;
+  t.w_count = min(slab_words, wpr - t.w_begin);
+  const int ngroups = (t.w_count + kGroupWords - 1) / kGroupWords;
+  t.my_groups = ngroups > wave ? (ngroups - wave + kWaves - 1) / kWaves : 0;
+  return t;
+}
+
+// Sign words of this wave's groups as unconditional buffer loads.  Lanes
+// past the last row or the slab's last word read data that never reaches a
+// stored output: a ragged group's tail meets the zero slot on the B side,
+// and rows past `rows` are not written.  Groups past my_groups use an
+// out-of-range offset: no branch, so the compiler has no join at which to
+// wait for them.
+__device__ __forceinline__ void load_signs(u32x2 (&wv)[kMaxGroups], const uint32_t *M, int rows,
+                                           int wpr, const Tile &t, int wave, int lane) {
+  const int rho = lane & 15;
+  const int q = lane >> 4;
+  const __amdgpu_buffer_rsrc_t mres = buffer_rsrc(
+      M + (size_t)t.row0 * wpr, (int64_t)(rows - t.row0) * wpr * 4);
+#pragma unroll
+  for (int i = 0; i < kMaxGroups; ++i) {
+    const int wl = (wave + kWaves * i) * kGroupWords + 2 * q;
+    // One 8-byte load per lane.  Buffer range checking applies per dword, so
+    // with an odd number of words per row a pair whose second word lies past
+    // the buffer still returns its first word (and zero for the second); a
+    // second word past the row but inside the buffer is an out-of-slab word
+    // and meets the zero slot.
+    const int off = i < t.my_groups ? (rho * wpr + t.w_begin + wl) * 4 : kOob;
+    wv[i] = __builtin_amdgcn_raw_buffer_load_b64(mres, off, 0, 0);
+  }
+}
+
+// One workgroup's tile of one stage, its sign words already loaded: stage
+// the input, run the products, add the waves' results, scale and store.
 //
 // kHiLoCols (b <= 8): the bf16 hi and lo parts of batch row beta occupy MFMA
 // columns 2*beta and 2*beta+1, so one MFMA per tile covers both; otherwise
 // (b up to 16) columns are batch rows and hi and lo take one MFMA each.
 template <bool kInX, bool kOutY, bool kHiLoCols>
-__global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
-    const uint32_t *__restrict__ M, const void *__restrict__ in,
-    const uint16_t *__restrict__ s_in, const uint16_t *__restrict__ row_scale, int rows,
-    int wpr, int slab_words, int b, int nslabs, int mode, int in_parts,
-    void *__restrict__ out, float *__restrict__ part, uint32_t *__restrict__ cnt) {
-  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // scalar: wave-uniform
-  const int tile = blockIdx.x;
-  const int slab = blockIdx.y;
-  const int row0 = tile * kTileRows;
-  const int w_begin = slab * slab_words;
-  const int w_count = min(slab_words, wpr - w_begin);
-  const int ngroups = (w_count + kGroupWords - 1) / kGroupWords;
-  // this wave's groups: g = wave + kWaves * i, i < my_groups
-  const int my_groups = ngroups > wave ? (ngroups - wave + kWaves - 1) / kWaves : 0;
+__device__ __forceinline__ void stage_tile(const u32x2 (&wv)[kMaxGroups], const Tile &T,
+                                           int wave, int lane, int tid, uint8_t *lds,
+                                           const void *in, const uint16_t *s_in,
+                                           const uint16_t *row_scale, int rows, int wpr, int b,
+                                           int nslabs, int mode, int in_parts, void *out,
+                                           float *part, uint32_t *cnt) {
   const size_t K = (size_t)wpr * 32;
+  const int w_begin = T.w_begin;
+  const int w_count = T.w_count;
+  const int my_groups = T.my_groups;
 
-  // A-operand lanes: row rho, word pair q.  B-operand lanes: column n, pair q.
-  const int rho = lane & 15;
+  // B-operand lanes: column n, pair q.
   const int q = lane >> 4;
   const int ncol = lane & 15;
   const int beta = kHiLoCols ? (ncol >> 1) : ncol;
   const int hl_col = kHiLoCols ? (ncol & 1) : 0;
 
-  // 1. Sign words of this wave's groups, issued before anything else as
-  //    unconditional buffer loads.  Lanes past the last row or the slab's
-  //    last word read data that never reaches a stored output: a ragged
-  //    group's tail meets the zero slot on the B side, and rows past `rows`
-  //    are not written.  Groups past my_groups use an out-of-range offset:
-  //    no branch, so the compiler has no join at which to wait for the loads.
-  const __amdgpu_buffer_rsrc_t mres =
-      buffer_rsrc(M + (size_t)row0 * wpr, (int64_t)(rows - row0) * wpr * 4);
-  u32x2 wv[kMaxGroups];
-#pragma unroll
-  for (int i = 0; i < kMaxGroups; ++i) {
-    const int wl = (wave + kWaves * i) * kGroupWords + 2 * q;
-    // Two 4-byte loads, each range-checked on its own: with an odd number of
-    // words per row the second word of the last pair lies past the row
-    // (and, for the last row, past the buffer).  Out-of-slab words are
-    // harmless (they meet the zero slot), but must not hide a valid word.
-    const int off = i < my_groups ? (rho * wpr + w_begin + wl) * 4 : kOob;
-    wv[i].x = __builtin_amdgcn_raw_buffer_load_b32(mres, off, 0, 0);
-    wv[i].y = __builtin_amdgcn_raw_buffer_load_b32(mres, off == kOob ? kOob : off + 4, 0, 0);
-  }
-
-  // 2. Stage this wave's columns of the input as bf16 hi/lo (p, p+16) pairs,
+  // 1. Stage this wave's columns of the input as bf16 hi/lo (p, p+16) pairs,
   //    one 144-byte slot per (batch row, word); slot 0 holds zeros for lanes
   //    with no batch row and for the tail of a ragged group.  A wave reads
   //    only slots it wrote itself, and a wave's LDS operations execute in
@@ -281,13 +307,13 @@ __global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
   // staging loads so that waiting for it waits for nothing else).
   const int orow_l = tid >> 4;
   const int obeta = tid & 15;
-  const int orow = row0 + orow_l;
+  const int orow = T.row0 + orow_l;
   const bool active = tid < kTileRows * 16 && obeta < b && orow < rows;
   const uint32_t rscale_bits = __builtin_amdgcn_raw_buffer_load_b16(
       buffer_rsrc(row_scale, (int64_t)rows * 2), orow * 2, 0, 0);
   __builtin_amdgcn_wave_barrier();
 
-  // 3. Products.  Step s = (group i = s / 2, word u = s % 2); independent
+  // 2. Products.  Step s = (group i = s / 2, word u = s % 2); independent
   //    accumulator chains per pair quad t (and per hi/lo when they are not
   //    in columns); the B operands of the next step are read from LDS while
   //    this step's MFMAs run.  Only lanes whose column carries a batch row
@@ -349,7 +375,7 @@ __global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
     for (int hl = 0; hl < kChains; ++hl)
       if (t | hl) tot += acc[t][hl];
 
-  // 4. Add the waves' 16x16 tiles through LDS (after every wave is done
+  // 3. Add the waves' 16x16 tiles through LDS (after every wave is done
   //    reading its staged operands).  Accumulator layout: lane l holds rows
   //    4*(l/16) + i (i = 0..3) of column l mod 16.
   __syncthreads();
@@ -371,31 +397,53 @@ __global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
   if (mode == kModeLastSlab) {
     // Publish this slab's partial sum; the last slab of the tile to arrive
     // adds all partials in slab order and resets the tile's counter.
-    if (active) part[((size_t)slab * b + obeta) * rows + orow] = sum;
-    __threadfence();
+    if (active) store_device(&part[((size_t)T.slab * b + obeta) * rows + orow], sum);
+    wait_memory();
     __syncthreads();
     __shared__ uint32_t s_last;
-    if (tid == 0) s_last = (atomicAdd(&cnt[tile], 1u) == (uint32_t)(nslabs - 1));
+    if (tid == 0)
+      s_last = __hip_atomic_fetch_add(&cnt[T.tile], 1u, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT) == (uint32_t)(nslabs - 1);
     __syncthreads();
     if (!s_last) return;
-    __threadfence();
     if (active) {
       sum = 0.f;
       for (int sl = 0; sl < nslabs; ++sl)
         sum += __hip_atomic_load(&part[((size_t)sl * b + obeta) * rows + orow], __ATOMIC_RELAXED,
                                  __HIP_MEMORY_SCOPE_AGENT);
     }
-    if (tid == 0) cnt[tile] = 0u;
+    if (tid == 0) __hip_atomic_store(&cnt[T.tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
   if (active) {
-    const float v = sum * f16_to_f32((uint16_t)rscale_bits);
+    float v = sum * f16_to_f32((uint16_t)rscale_bits);
     size_t o = (size_t)obeta * rows + orow;
-    if (mode == kModePartial) o += (size_t)slab * b * rows;
+    if (mode == kModePartial) o += (size_t)T.slab * b * rows;
     if constexpr (kOutY)
       static_cast<uint16_t *>(out)[o] = f32_to_bf16(v);
     else
       static_cast<float *>(out)[o] = v;
   }
+}
+
+// One stage as its own launch: workgroup (tile, slab) = (blockIdx.x,
+// blockIdx.y).  Arguments are scalars, most urgent first, so that they are
+// preloaded into SGPRs at wave launch instead of being fetched from the
+// kernarg segment.
+template <bool kInX, bool kOutY, bool kHiLoCols>
+__global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
+    const uint32_t *__restrict__ M, const void *__restrict__ in,
+    const uint16_t *__restrict__ s_in, const uint16_t *__restrict__ row_scale, int rows,
+    int wpr, int slab_words, int b, int nslabs, int mode, int in_parts,
+    void *__restrict__ out, float *__restrict__ part, uint32_t *__restrict__ cnt) {
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // scalar: wave-uniform
+  const Tile T = make_tile(blockIdx.x, blockIdx.y, wpr, slab_words, wave);
+  u32x2 wv[kMaxGroups];
+  load_signs(wv, M, rows, wpr, T, wave, lane);
+  stage_tile<kInX, kOutY, kHiLoCols>(wv, T, wave, lane, tid, lds, in, s_in, row_scale, rows, wpr,
+                                     b, nslabs, mode, in_parts, out, part, cnt);
 }
 
 // Largest slab (in words, a multiple of kGroupWords) whose staged input fits LDS.
@@ -445,22 +493,28 @@ struct WsLayout {
   size_t t, part1, cnt1, part2, cnt2, total;
 };
 
+// Workspace: a fixed header, then the shape-dependent arrays.  The header
+// holds the arrival counters (one per 16-row tile of each stage), which must
+// be zero at the start of a call, at offsets that do not depend on the
+// shape, so that calls of different shapes can share one workspace without
+// their arrays ever overlapping another shape's counters.
+constexpr size_t kMaxTiles = ((size_t)1 << 20) / kTileRows;  // rows <= 2^20
+constexpr size_t kHeaderBytes = 2 * kMaxTiles * 4;
+
 WsLayout ws_layout(int64_t m, int64_t n, int64_t r, int64_t b) {
   WsLayout L{};
   L.p1 = plan_stage(r, n / 32, b, true);
   L.p2 = plan_stage(m, r / 32, b, false);
+  L.cnt1 = 0;
+  L.cnt2 = kMaxTiles * 4;
   const int tparts = L.p1.mode == kModePartial ? L.p1.nslabs : 1;
-  size_t off = 0;
+  size_t off = kHeaderBytes;
   L.t = off;
   off += align256((size_t)tparts * b * r * 4);
   L.part1 = off;
   if (L.p1.mode == kModeLastSlab) off += align256((size_t)L.p1.nslabs * b * r * 4);
-  L.cnt1 = off;
-  if (L.p1.mode == kModeLastSlab) off += align256((size_t)((r + kTileRows - 1) / kTileRows) * 4);
   L.part2 = off;
   if (L.p2.mode == kModeLastSlab) off += align256((size_t)L.p2.nslabs * b * m * 4);
-  L.cnt2 = off;
-  if (L.p2.mode == kModeLastSlab) off += align256((size_t)((m + kTileRows - 1) / kTileRows) * 4);
   L.total = off;
   return L;
 }

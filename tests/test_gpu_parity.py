@@ -185,6 +185,32 @@ def test_gemv_column_slabs_reuse_workspace(oracle, m, n, r, b):
     assert max_row_rel_l2(bf16_bits_to_f64(ys), oracle_y(oracle, small)) <= TOL
 
 
+def test_gemv_workspace_shared_by_shapes_and_batches(oracle):
+    """One zero-filled workspace, 3 x 20 calls alternating shapes whose
+    stages use different column plans (a last-slab reduction at b=16, split
+    partial sums at b=1, single slabs at 14336x4096): the arrival counters
+    sit at fixed offsets and return to zero after every call, so every call
+    gives the same bits as on a fresh workspace."""
+    cases = []
+    for name, b in (("attn4096", 16), ("attn4096", 1), ("mlp_up14336x4096", 2)):
+        m, n, r = synth.SHAPES[name]
+        lin = synth.make_linear(500 + b, m, n, r, b)
+        L = DeviceLayer.from_host(lin)
+        x = to_device(lin.x)
+        ref = L.gemv(x)
+        torch.cuda.synchronize()
+        assert max_row_rel_l2(bf16_bits_to_f64(ref), oracle_y(oracle, lin)) <= TOL
+        cases.append((L, x, b, ref))
+    ws = torch.zeros(max(af1.af1_gemv_workspace_bytes(L.m, L.n, L.r, b) for L, _, b, _ in cases),
+                     dtype=torch.uint8, device="cuda")
+    for i in range(20):
+        for L, x, b, ref in cases:
+            y = torch.full((b, L.m), 0x7FC0, dtype=torch.int16, device="cuda")
+            L.gemv(x, y=y, ws=ws)
+            torch.cuda.synchronize()
+            assert torch.equal(y, ref), (i, L.m, L.n, L.r, b)
+
+
 def test_gemv_deterministic():
     lin = synth.make_linear(9, 4096, 4096, 2016, 4)
     assert np.array_equal(gpu_gemv(lin), gpu_gemv(lin))
