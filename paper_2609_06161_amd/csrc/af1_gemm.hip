@@ -16,8 +16,9 @@
 // bits).  The activations are kept in the same order: inside every group
 // of 32 columns, column p sits at position 2p and column p+16 at 2p+1.  A
 // pre-pass writes x in that order (converting bf16 to fp16 once, instead
-// of once per weight-row tile), and G1 writes Z in that order, so both GEMMs
-// stage their activation tiles with plain copies.
+// of once per weight-row tile) and the column scales as pair dwords, and G1
+// writes Z in that order, so the GEMMs stage their operands with plain
+// copies.
 //
 // Tiling.  A 256-thread workgroup computes a 128 (tokens) x 256 (weight
 // rows) tile of C over K steps of 128 columns.  The activation tile is the
@@ -27,14 +28,20 @@
 // sign bit is expanded exactly once, in registers, straight into an MFMA
 // operand.
 //
-// Pipeline.  LDS holds two sets of (activation tile, column-scale pairs,
-// sign words); each K step issues the global loads of the next step before
-// its own MFMAs, consumes them only after the MFMAs, and meets one barrier.
-// Per-step addresses move the scalar buffer base.  Columns past K
-// read a zero column scale, so they contribute nothing whatever the
-// activation or sign data they meet.  Tiles are assigned so that the
+// Staging.  Operands go from global memory straight into LDS (buffer loads
+// with the LDS destination), double-buffered: a K step issues the copies of
+// the next step, runs its MFMAs, waits for its copies and meets one
+// barrier.  No staging registers are needed, which leaves room to read the
+// next MFMA step's operands from LDS while the current one runs.  An LDS
+// copy instruction writes 64 consecutive 16-byte chunks, one per lane, but
+// each lane chooses its source: the chunk of token row t holding columns
+// 8c .. 8c+7 of the step is stored at chunk position c XOR (t mod 16) of the
+// row, so that the MFMA operand reads (16 bytes per lane, consecutive
+// tokens) fall in distinct LDS banks.  Tiles are assigned so that the
 // workgroups of one XCD (blockIdx mod 8) work on a contiguous range of
 // tiles and share activation rows in their L2.
+#include <utility>
+
 #include "af1_device.h"
 #include "af1_internal.h"
 
@@ -53,19 +60,60 @@ constexpr int BN = 256;          // weight rows per tile
 constexpr int kWords = 4;        // sign words per K step
 constexpr int BK = 32 * kWords;  // columns per K step
 constexpr int kThreads = 256;
-constexpr int kRowBytes = BK * 2 + 16;             // LDS bytes per token row (+16 pad)
-constexpr int kATile = BM * kRowBytes;
-constexpr int kCsBytes = kWords * 16 * 4;          // column-scale pairs of one K step
-constexpr int kWBytes = BN * kWords * 4;           // sign words of one K step
-constexpr int kAChunks = BM * BK * 2 / 16 / kThreads;  // 16-byte activation chunks per thread
-constexpr int kLdsBytes = 2 * (kATile + kCsBytes + kWBytes);
+constexpr int kARow = BK * 2;                // bytes of one token row of a K step
+constexpr int kATile = BM * kARow;           // 32 KiB
+constexpr int kWTile = BN * kWords * 4;      // 4 KiB
+constexpr int kCsTile = kWords * 16 * 4;     // column-scale pair dwords of one K step
+// LDS map: A0 | A1 | W0 | W1 | CS0 | CS1 (both activation buffers first, so
+// every operand read is a 16-bit immediate offset from one address).
+constexpr int kA0 = 0;
+constexpr int kW0 = 2 * kATile;
+constexpr int kCs0 = kW0 + 2 * kWTile;
+constexpr int kLdsBytes = kCs0 + 2 * kCsTile;
 constexpr int kOob = (int)0x80000000u;
-static_assert(kAChunks * kThreads * 16 == BM * BK * 2, "activation chunks");
-static_assert(4 * kWords <= kThreads, "column-scale staging");
+static_assert(BM * kARow == 32 * 1024 && kThreads == 256, "eight 1 KiB copies per wave");
+static_assert(kCsTile == 64 * 4, "one 4-byte copy per lane of wave 0");
+static_assert(kA0 + kATile + 3 * 32 * kARow + kARow < 65536, "immediate LDS offsets");
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, int64_t bytes) {
   const int n = bytes > 0x7fffffff ? 0x7fffffff : (bytes < 0 ? 0 : (int)bytes);
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, n, 0x00020000);
+}
+
+// The same raw buffer resource (stride 0, raw dword access) as four scalar
+// dwords, for the copy instructions below.
+__device__ __forceinline__ i32x4 copy_rsrc(const void *base, int64_t bytes) {
+  const int n = bytes > 0x7fffffff ? 0x7fffffff : (bytes < 0 ? 0 : (int)bytes);
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  return i32x4{(int)(uint32_t)a, (int)((a >> 32) & 0xffffu), n, 0x00020000};
+}
+
+// Global -> LDS copies: lane l of the wave writes `bytes` bytes at
+// dst + bytes * l (dst wave-uniform, passed in M0), read from voff of the
+// resource (zero when out of range).  Written as inline assembly so that the
+// compiler does not wait for them before every LDS read (it cannot tell
+// that they target the other buffer); wait_copies() is the only wait.
+__device__ __forceinline__ void copy16(i32x4 r, uint8_t *dst, int voff) {
+  const uint32_t m = (uint32_t)(size_t)(lds_void *)dst;
+  asm volatile("buffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voff), "s"(r), "{m0}"(m) : "memory");
+}
+__device__ __forceinline__ void copy4(i32x4 r, uint8_t *dst, int voff) {
+  const uint32_t m = (uint32_t)(size_t)(lds_void *)dst;
+  asm volatile("buffer_load_dword %0, %1, 0 offen lds" ::"v"(voff), "s"(r), "{m0}"(m) : "memory");
+}
+
+__device__ __forceinline__ void wait_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F &&f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
 // Two fp32 -> packed fp16 (round to nearest even).
@@ -104,12 +152,26 @@ __global__ __launch_bounds__(256) void pair_order_kernel(const uint16_t *__restr
   dst[1] = make_uint4(d[4], d[5], d[6], d[7]);
 }
 
+// Column scales (fp16, [K]) -> pair dwords: dword 16q + p holds columns
+// 32q + p (low half) and 32q + p + 16 (high half); columns from K up to
+// Kpad (a multiple of BK) are zero, so a partial last K step adds nothing.
+__global__ __launch_bounds__(256) void colscale_pairs_kernel(const uint16_t *__restrict__ s,
+                                                             uint32_t *__restrict__ out, int K,
+                                                             int Kpad) {
+  const int d = blockIdx.x * 256 + threadIdx.x;
+  if (d >= Kpad / 2) return;
+  const int c = (d >> 4) * 32 + (d & 15);
+  const uint32_t lo = c < K ? s[c] : 0u;
+  const uint32_t hi = c + 16 < K ? s[c + 16] : 0u;
+  out[d] = lo | (hi << 16);
+}
+
 // C = rowscale * (A_pairorder x (sign(W) * colscale)^T).  kOutBf16: C is
 // bf16 in natural column order (y); otherwise fp16 in pair order (Z).
 template <bool kOutBf16>
 __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     const uint16_t *__restrict__ A, int T, int K, const uint32_t *__restrict__ W, int N,
-    const uint16_t *__restrict__ colscale, const uint16_t *__restrict__ rowscale,
+    const uint32_t *__restrict__ cspairs, int Kpad, const uint16_t *__restrict__ rowscale,
     uint16_t *__restrict__ C) {
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   const int tid = threadIdx.x;
@@ -127,72 +189,65 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   const int kw = K / 32;                       // sign words per row
   const int nk = (kw + kWords - 1) / kWords;   // K steps (the last may be partial)
 
-  // Staging roles (fixed per thread; a step only adds a scalar offset).
-  // Activations: 16-byte chunk q = tid + 256k of the tile -> token q / 16,
-  // byte 16 (q mod 16) of the token's K-step slice (already in pair order).
-  // Column scale: threads 0 .. 4*kWords-1 load columns c .. c+3 and c+16 ..
-  // c+19 of word tid/4 and build 4 pair dwords.  Sign words: thread tid
-  // stages row n0 + tid.
-  int a_off[kAChunks], a_dst[kAChunks];
+  // Copy roles, fixed per lane (a step only moves the resources' bases).
+  //  Activations: wave w issues copies j = 8w + jj (jj < 8), each covering
+  //  token rows 4j .. 4j+3 of the tile; lane l fills chunk position l mod 16
+  //  of row 4j + l/16 with the chunk whose index is that position XOR the
+  //  row's low four bits.  Columns past K read the next row or zeros; they
+  //  meet zero column scales.
+  int a_off[8];
 #pragma unroll
-  for (int k = 0; k < kAChunks; ++k) {
-    const int q = tid + kThreads * k;
-    const int tok = q / (BK * 2 / 16), part = q % (BK * 2 / 16);
-    a_off[k] = t0 + tok < T ? ((t0 + tok) * K) * 2 + 16 * part : kOob;
-    a_dst[k] = tok * kRowBytes + 16 * part;
+  for (int jj = 0; jj < 8; ++jj) {
+    const int tok = 4 * (8 * wave + jj) + (lane >> 4);
+    const int part = (lane & 15) ^ (tok & 15);
+    a_off[jj] = t0 + tok < T ? (t0 + tok) * K * 2 + 16 * part : kOob;
   }
-  const bool cs_thread = tid < 4 * kWords;
-  const int cs_off = cs_thread ? (32 * (tid >> 2) + 4 * (tid & 3)) * 2 : kOob;
-  const int w_off = n0 + tid < N ? (n0 + tid) * kw * 4 : kOob;
+  //  Sign words: copy i of wave w covers tile rows 64w + 16i .. +15, four
+  //  words (16 bytes) per row.
+  int w_off[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = n0 + 64 * wave + 16 * i + (lane >> 2);
+    w_off[i] = row < N ? row * kw * 4 + 4 * (lane & 3) : kOob;
+  }
 
-  u32x4 a_raw[kAChunks];
-  u32x2 cs_raw[2];
-  uint32_t w_raw[kWords];
-  // All of a step's loads are consumed only by store_stage, after the MFMAs
-  // of the previous step, so the MFMAs never wait on global memory.  Every
-  // thread issues every load (out-of-range offsets where there is nothing
-  // to load), so the count of outstanding loads never depends on a branch.
-  //  The step offset moves the (scalar) resource base rather than being a
-  //  scalar offset: range checking covers the vector offset only, so every
-  //  access is checked against what remains of its buffer from the base.
-  auto load_stage = [&](int step) {
-    const int ka = step * BK * 2;   // byte offset of the step in an A row / colscale
-    const int kwb = step * kWords * 4;
-    const __amdgpu_buffer_rsrc_t as = buffer_rsrc(A + step * BK, (int64_t)T * K * 2 - ka);
-    const __amdgpu_buffer_rsrc_t cs = buffer_rsrc(colscale + step * BK, (int64_t)K * 2 - ka);
-    const __amdgpu_buffer_rsrc_t ws = buffer_rsrc(W + step * kWords, (int64_t)N * kw * 4 - kwb);
+  auto issue = [&](int step, int buf) {
+    const i32x4 as = copy_rsrc(A + step * BK, (int64_t)T * K * 2 - (int64_t)step * BK * 2);
+    const i32x4 ws = copy_rsrc(W + step * kWords, (int64_t)N * kw * 4 - (int64_t)step * kWords * 4);
 #pragma unroll
-    for (int k = 0; k < kAChunks; ++k)
-      a_raw[k] = __builtin_amdgcn_raw_buffer_load_b128(as, a_off[k], 0, 0);
-    cs_raw[0] = __builtin_amdgcn_raw_buffer_load_b64(cs, cs_off, 0, 0);
-    cs_raw[1] = __builtin_amdgcn_raw_buffer_load_b64(cs, cs_off == kOob ? kOob : cs_off + 32, 0, 0);
+    for (int jj = 0; jj < 8; ++jj)
+      copy16(as, lds + kA0 + buf * kATile + (8 * wave + jj) * 1024, a_off[jj]);
 #pragma unroll
-    for (int i = 0; i < kWords; ++i)
-      w_raw[i] = __builtin_amdgcn_raw_buffer_load_b32(ws, w_off == kOob ? kOob : w_off + 4 * i, 0, 0);
-  };
-  auto store_stage = [&](int buf) {
-    uint8_t *at = lds + buf * kATile;
-#pragma unroll
-    for (int k = 0; k < kAChunks; ++k)
-      *reinterpret_cast<u32x4 *>(at + a_dst[k]) = a_raw[k];
-    if (cs_thread) {
-      uint32_t d[4];
-      d[0] = __builtin_amdgcn_perm(cs_raw[1].x, cs_raw[0].x, 0x05040100u);
-      d[1] = __builtin_amdgcn_perm(cs_raw[1].x, cs_raw[0].x, 0x07060302u);
-      d[2] = __builtin_amdgcn_perm(cs_raw[1].y, cs_raw[0].y, 0x05040100u);
-      d[3] = __builtin_amdgcn_perm(cs_raw[1].y, cs_raw[0].y, 0x07060302u);
-      reinterpret_cast<uint4 *>(lds + 2 * kATile + buf * kCsBytes)[tid] =
-          make_uint4(d[0], d[1], d[2], d[3]);
+    for (int i = 0; i < 4; ++i) copy4(ws, lds + kW0 + buf * kWTile + (64 * wave + 16 * i) * 16, w_off[i]);
+    if (wave == 0) {
+      const i32x4 cs =
+          copy_rsrc(cspairs + step * (kCsTile / 4), (int64_t)Kpad * 2 - (int64_t)step * kCsTile);
+      copy4(cs, lds + kCs0 + buf * kCsTile, 4 * lane);
     }
-    uint32_t *wdst =
-        reinterpret_cast<uint32_t *>(lds + 2 * kATile + 2 * kCsBytes + buf * kWBytes) + tid * kWords;
-#pragma unroll
-    for (int i = 0; i < kWords; ++i) wdst[i] = w_raw[i];
   };
+
+  // No stale LDS pattern (possibly a NaN) may ever meet an MFMA, even in
+  // rows or columns that are never stored.
+  for (int o = tid * 16; o < kLdsBytes; o += kThreads * 16)
+    *reinterpret_cast<uint4 *>(lds + o) = make_uint4(0u, 0u, 0u, 0u);
+  __syncthreads();
+  issue(0, 0);
 
   // This lane's weight rows: block j -> tile row 64*wave + 32*j + (l mod 32).
   const int wrow_l = 64 * wave + (lane & 31);
   const int wrow0 = n0 + wrow_l;
+  const int g = lane >> 5;  // K half of an MFMA operand (slots 8g .. 8g+7)
+  // Activation operand of MFMA step ks (columns 16ks .. 16ks+15 of the K
+  // step): chunk 2ks + g of token row (l mod 32) + 32i, swizzled.
+  int a_rd[8];
+#pragma unroll
+  for (int ks = 0; ks < 8; ++ks) a_rd[ks] = (lane & 31) * kARow + (((2 * ks + g) ^ (lane & 15)) << 4);
+  // Shift that moves sign bit p = 8s + 4g + e of a word to bit 15.
+  int sh[2][4];
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sh[s][e] = 15 - (8 * s + 4 * g + e);
 
   floatx16 acc[4][2];
 #pragma unroll
@@ -205,52 +260,50 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   uint32_t kSignMask;
   asm volatile("v_mov_b32 %0, 0x80008000" : "=v"(kSignMask));
 
-  load_stage(0);
-  store_stage(0);
+  wait_copies();
   __syncthreads();
 
-  const int g = lane >> 5;  // K half of an MFMA operand (slots 8g .. 8g+7)
-  for (int step = 0; step < nk; ++step) {
-    const int buf = step & 1;
-    const bool more = step + 1 < nk;
-    if (more) load_stage(step + 1);
-    const uint8_t *at = lds + buf * kATile + (lane & 31) * kRowBytes + 16 * g;
-    const uint4 *cs = reinterpret_cast<const uint4 *>(lds + 2 * kATile + buf * kCsBytes);
-    const uint32_t *ws =
-        reinterpret_cast<const uint32_t *>(lds + 2 * kATile + 2 * kCsBytes + buf * kWBytes);
-    uint32_t wj[2][kWords];
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int i = 0; i < kWords; ++i) wj[j][i] = ws[(wrow_l + 32 * j) * kWords + i];
-#pragma unroll
-    for (int ks = 0; ks < 2 * kWords; ++ks) {
-      const int wi = ks >> 1, s = ks & 1;
-      // column-scale pairs and activation fragments of this MFMA K step:
-      // pair dwords 16wi + 8s + 4g .. +3
-      const uint4 c4 = cs[4 * wi + 2 * s + g];
-      half8 af[4];
+  auto run_step = [&](int step, auto BUF) {
+    constexpr int buf = decltype(BUF)::value;
+    if (step + 1 < nk) issue(step + 1, buf ^ 1);
+    const uint8_t *abase = lds + kA0 + buf * kATile;
+    const uint4 *wt = reinterpret_cast<const uint4 *>(lds + kW0 + buf * kWTile);
+    const uint4 *cs = reinterpret_cast<const uint4 *>(lds + kCs0 + buf * kCsTile);
+    const uint4 wq0 = wt[wrow_l], wq1 = wt[wrow_l + 32];
+    const uint32_t wj[2][kWords] = {{wq0.x, wq0.y, wq0.z, wq0.w}, {wq1.x, wq1.y, wq1.z, wq1.w}};
+    half8 af[2][4];
+    uint4 c4[2];
+    auto read_ops = [&](int ks, int slot) {
 #pragma unroll
       for (int i = 0; i < 4; ++i)
-        af[i] = *reinterpret_cast<const half8 *>(at + 32 * i * kRowBytes + (16 * wi + 8 * s) * 4);
-      const uint32_t cpair[4] = {c4.x, c4.y, c4.z, c4.w};
+        af[slot][i] = *reinterpret_cast<const half8 *>(abase + a_rd[ks] + 32 * i * kARow);
+      c4[slot] = cs[2 * ks + g];
+    };
+    read_ops(0, 0);
+    static_for<2 * kWords>([&](auto KS) {
+      constexpr int ks = decltype(KS)::value;
+      constexpr int cur = ks & 1;
+      if constexpr (ks + 1 < 2 * kWords) read_ops(ks + 1, cur ^ 1);
+      const uint32_t cpair[4] = {c4[cur].x, c4[cur].y, c4[cur].z, c4[cur].w};
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        const uint32_t w = wj[j][wi];
+        const uint32_t w = wj[j][ks >> 1];
         uint32_t bd[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int p = 8 * s + 4 * g + e;  // g is lane-dependent: variable shift
-          bd[e] = cpair[e] ^ ((w << (15 - p)) & kSignMask);
-        }
+        for (int e = 0; e < 4; ++e) bd[e] = cpair[e] ^ ((w << sh[ks & 1][e]) & kSignMask);
         const half8 bf = __builtin_bit_cast(half8, make_uint4(bd[0], bd[1], bd[2], bd[3]));
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[i], bf, acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[cur][i], bf, acc[i][j], 0, 0, 0);
       }
-    }
-    if (more) store_stage(buf ^ 1);
+    });
+    wait_copies();
     __syncthreads();
+  };
+
+  for (int step = 0; step < nk; step += 2) {
+    run_step(step, std::integral_constant<int, 0>{});
+    if (step + 1 < nk) run_step(step + 1, std::integral_constant<int, 1>{});
   }
 
   // Epilogue.  32x32 accumulator layout: lane l holds column (l mod 32) and
@@ -277,12 +330,17 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
+int64_t kpad(int64_t K) { return (K + BK - 1) / BK * BK; }
+
 }  // namespace
 
 size_t gemm_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
   (void)m;
-  // fp16 x in pair order, then the fp16 intermediate Z (pair order)
-  return align256((size_t)T * (size_t)n * 2) + align256((size_t)T * (size_t)r * 2);
+  // fp16 x in pair order, the fp16 intermediate Z (pair order), and the two
+  // column-scale pair arrays (s_in for G1, s_mid for G2), zero-padded to
+  // whole K steps
+  return align256((size_t)T * (size_t)n * 2) + align256((size_t)T * (size_t)r * 2) +
+         align256((size_t)kpad(n) * 2) + align256((size_t)kpad(r) * 2);
 }
 
 hipError_t launch_gemm(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
@@ -294,21 +352,31 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
   if (T * n * 2 > 0x7fffffff || T * r * 2 > 0x7fffffff || m * (r / 32) * 4 > 0x7fffffff ||
       r * (n / 32) * 4 > 0x7fffffff)
     return hipErrorInvalidValue;
-  uint16_t *xp = static_cast<uint16_t *>(ws);
-  uint16_t *Z = reinterpret_cast<uint16_t *>(static_cast<uint8_t *>(ws) + align256((size_t)T * n * 2));
+  uint8_t *base = static_cast<uint8_t *>(ws);
+  uint16_t *xp = reinterpret_cast<uint16_t *>(base);
+  base += align256((size_t)T * n * 2);
+  uint16_t *Z = reinterpret_cast<uint16_t *>(base);
+  base += align256((size_t)T * r * 2);
+  uint32_t *cs1 = reinterpret_cast<uint32_t *>(base);
+  base += align256((size_t)kpad(n) * 2);
+  uint32_t *cs2 = reinterpret_cast<uint32_t *>(base);
   const int64_t units = T * (n / 16);
   pair_order_kernel<<<(unsigned)((units + 255) / 256), 256, 0, s>>>(x, xp, (int)T, (int)n);
+  colscale_pairs_kernel<<<(unsigned)((kpad(n) / 2 + 255) / 256), 256, 0, s>>>(s_in, cs1, (int)n,
+                                                                                (int)kpad(n));
+  colscale_pairs_kernel<<<(unsigned)((kpad(r) / 2 + 255) / 256), 256, 0, s>>>(s_mid, cs2, (int)r,
+                                                                                (int)kpad(r));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const unsigned gy = (unsigned)((T + BM - 1) / BM);
   dim3 g1((unsigned)((r + BN - 1) / BN), gy);
-  bingemm_kernel<false><<<g1, kThreads, kLdsBytes, s>>>(xp, (int)T, (int)n, Bv, (int)r, s_in,
-                                                        nullptr, Z);
+  bingemm_kernel<false><<<g1, kThreads, kLdsBytes, s>>>(xp, (int)T, (int)n, Bv, (int)r, cs1,
+                                                        (int)kpad(n), nullptr, Z);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 g2((unsigned)((m + BN - 1) / BN), gy);
-  bingemm_kernel<true><<<g2, kThreads, kLdsBytes, s>>>(Z, (int)T, (int)r, Bu, (int)m, s_mid,
-                                                       s_out, y);
+  bingemm_kernel<true><<<g2, kThreads, kLdsBytes, s>>>(Z, (int)T, (int)r, Bu, (int)m, cs2,
+                                                       (int)kpad(r), s_out, y);
   return hipGetLastError();
 }
 
