@@ -284,6 +284,9 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       constexpr int ks = decltype(KS)::value;
       constexpr int cur = ks & 1;
       if constexpr (ks + 1 < 2 * kWords) read_ops(ks + 1, cur ^ 1);
+      // Keep the next step's LDS reads ahead of this step's MFMAs (the
+      // scheduler would otherwise sink them next to their use).
+      __builtin_amdgcn_sched_barrier(0);
       const uint32_t cpair[4] = {c4[cur].x, c4[cur].y, c4[cur].z, c4[cur].w};
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
