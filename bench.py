@@ -152,6 +152,54 @@ DECODE_TABLE = [("sq1024", 1), ("attn4096", 8), ("kv1024x4096", 1), ("mlp_up1433
                 ("mlp_down4096x14336", 4), ("mlp_down4096x14336", 16)]
 
 
+STACK_LINEARS = [("q", 4096, 4096, 2016), ("k", 1024, 4096, 800), ("v", 1024, 4096, 800),
+                 ("o", 4096, 4096, 2016), ("gate", 14336, 4096, 3136),
+                 ("up", 14336, 4096, 3136), ("down", 4096, 14336, 3136)]
+
+
+def bench_stack(args, torch, stream):
+    """An 8B-shaped decoder stack: 32 layers x 7 linears, per-linear ranks
+    drawn +-25% around the budget rank with the whole stack <= 1.0 BPW,
+    weights streamed from HBM in layer order, batch 1, each linear fed a
+    fixed synthetic x of its input width; one HIP graph of the whole pass."""
+    from paper_2609_06161_amd import af1, synth
+    from paper_2609_06161_amd.layer import to_device
+    entries = synth.draw_stack_ranks(77, 32, STACK_LINEARS, af1.af1_storage_bits)
+    bits = sum(af1.af1_storage_bits(m, n, r) for _, m, n, _, r in entries)
+    dense = sum(m * n for _, m, n, _, _ in entries)
+    pools, descs = [], []
+    for i, (name, m, n, r0, r) in enumerate(entries):
+        P = DevicePool(torch, m, n, r, 1, 5000 + i)
+        pools.append(P)
+        descs.append((P.desc[0], m, n, r))
+    xs = {w: to_device(synth.make_activations(60 + w % 97, 1, w)) for w in (4096, 14336)}
+    ys = {w: torch.empty((1, w), dtype=torch.int16, device="cuda") for w in (1024, 4096, 14336)}
+    ws = torch.zeros(max(af1.af1_gemv_workspace_bytes(m, n, r, 1) for _, m, n, r in descs),
+                     dtype=torch.uint8, device="cuda")
+
+    def run_all():
+        for d, m, n, r in descs:
+            af1.af1_linear_gemv(d, xs[n], 1, ys[m], ws, ws.numel(), None)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run_all()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        run_all()
+    time_events(lambda i: graph.replay(), 2, stream)
+    reps = 10
+    ms = time_events(lambda i: graph.replay(), reps, stream) / reps
+    alg = sum(gemv_algorithmic_bytes(m, n, r, 1) for _, m, n, r in descs)
+    del graph, pools
+    return dict(linears=len(descs), bpw=round(bits / dense, 5), weight_mb=round(bits / 8 / 1e6, 1),
+                us_per_pass=round(ms * 1e3, 2), us_per_decoder_layer=round(ms * 1e3 / 32, 3),
+                us_per_linear=round(ms * 1e3 / len(descs), 3),
+                gbs=round(alg / (ms * 1e-3) / 1e9, 1))
+
+
 def bench_decode_table(args, torch, stream):
     from paper_2609_06161_amd import synth
     out = {}
@@ -187,6 +235,17 @@ def bench_gemm(args, torch, stream):
         total_flops += flops
         total_ms += ms
         del L, x, y, ws
+        # Context: the dense bf16 layer this factorization replaces, as one
+        # torch.matmul (hipBLASLt), [T, n] x [n, m] with contiguous operands.
+        xd = torch.randn((T, n), device="cuda", dtype=torch.bfloat16)
+        wd = torch.randn((n, m), device="cuda", dtype=torch.bfloat16)
+        fd = lambda i: torch.matmul(xd, wd)
+        time_events(fd, 3, stream)
+        msd = time_events(fd, args.gemm_steps, stream) / args.gemm_steps
+        out[name]["dense_bf16_us"] = msd * 1e3
+        out[name]["dense_bf16_tflops"] = 2.0 * T * n * m / (msd * 1e-3) / 1e12
+        out[name]["speedup_vs_dense_bf16"] = msd / ms
+        del xd, wd
     out["all3_tflops"] = total_flops / (total_ms * 1e-3) / 1e12
     return out
 
@@ -264,6 +323,7 @@ def main():
     }
     if not args.no_decode_table and args.only == "all":
         result["decode_table"] = bench_decode_table(args, torch, stream)
+        result["decode_stack_8b"] = bench_stack(args, torch, stream)
     if not args.no_gemm and args.only == "all":
         result["gemm"] = bench_gemm(args, torch, stream)
         result["gemm"]["peak_tflops"] = MFMA_F16_PEAK_TFLOPS

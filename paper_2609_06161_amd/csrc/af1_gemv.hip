@@ -34,6 +34,7 @@
 // split over workgroups ("slabs"); each slab writes a partial sum and the
 // last slab of a row tile to finish (atomic counter) adds the partials in
 // slab order, so the result is deterministic.
+#include <atomic>
 #include <utility>
 
 #include "af1_device.h"
@@ -55,15 +56,16 @@ constexpr int kTileRows = 16;        // MFMA M
 constexpr int kGroupWords = 8;       // one 8-byte load per lane covers 16 rows x 8 words
 constexpr int kMaxGroups = 8;        // groups per wave (single pass)
 constexpr int kSlot = 144;           // LDS bytes per (batch row, word): 64 hi + 64 lo + 16 pad
-constexpr int kLdsBytes = 65536;
+constexpr int kLdsBudget = 160 * 1024;  // LDS of one gfx950 compute unit
 constexpr int kRedBytes = kWaves * 64 * 16;
-// The LDS budget caps a slab at (kLdsBytes - kSlot) / kSlot = 454 words,
-// which the waves cover in a single pass.
-static_assert(kWaves * kMaxGroups * kGroupWords >= (kLdsBytes - kSlot) / kSlot, "one pass");
-// Staging: a unit is 8 columns (+ their partners 16 on) of one batch row;
-// a wave stages my_groups * 16 * b units, two per lane per pass.  Within the
-// LDS budget that is at most 4 passes (b = 16, one group).
-constexpr int kStageIters = 4;
+constexpr int kMaxOutPerThread = 4;  // outputs (row, batch row) written per thread
+// Staging passes.  Shared staging: a slab holds at most (kLdsBudget - kSlot)
+// / kSlot words over all batch rows (2 units per word), taken two per thread
+// per pass.  Per-wave staging: 128 units per wave per pass; the plan keeps a
+// wave's units (groups x b x 16) within kStageIters passes.
+constexpr int kStageIters = 3;
+static_assert(kStageIters * 2 * kThreads >= 2 * ((kLdsBudget - kSlot) / kSlot), "staging passes");
+constexpr int kWaveStageUnits = kStageIters * 128;
 constexpr int kOob = (int)0x80000000u;  // a buffer offset past any resource
 
 // The last-slab reduction hands partial sums between workgroups of one
@@ -182,142 +184,209 @@ constexpr int kModeLastSlab = 1;  // several slabs: the last one to finish adds 
 constexpr int kModePartial = 2;   // several slabs: each writes its scaled partial sum
                                   // (the next stage adds them while staging)
 
-// Where one workgroup's share of a stage lies: 16 rows starting at row0 and
-// the words [w_begin, w_begin + w_count) of those rows.  The wave's groups
-// are g = wave + kWaves * i, i < my_groups.
-struct Tile {
-  int tile, slab, row0, w_begin, w_count, my_groups;
+// Output rows handled by one workgroup: rt_count tiles of 16 rows.  The 8
+// waves are split evenly over the tiles; the waves of one tile split its
+// columns into groups of 8 words (group g of the slab goes to wave g mod
+// waves_per_tile of that tile).
+struct Role {
+  int rt_log2;     // log2(tiles per workgroup)
+  int wpt;         // waves per tile
+  int rt;          // this wave's tile within the workgroup
+  int cw;          // this wave's column share within its tile
+  int tile;        // global 16-row tile of this wave
+  int row0;
+  int w_begin, w_count;
+  int my_groups;
 };
 
-__device__ __forceinline__ Tile make_tile(int tile, int slab, int wpr, int slab_words, int wave) {
-  Tile t;
-  t.tile = tile;
-  t.slab = slab;
-  t.row0 = tile * kTileRows;
-  t.w_begin = slab * slab_words;
-  t.w_count = min(slab_words, wpr - t.w_begin);
-  const int ngroups = (t.w_count + kGroupWords - 1) / kGroupWords;
-  t.my_groups = ngroups > wave ? (ngroups - wave + kWaves - 1) / kWaves : 0;
-  return t;
+__device__ __forceinline__ Role make_role(int wave, int rt_log2, int wpr, int slab_words) {
+  Role r;
+  r.rt_log2 = rt_log2;
+  r.wpt = kWaves >> rt_log2;
+  r.rt = wave >> (3 - rt_log2);
+  r.cw = wave & (r.wpt - 1);
+  r.tile = ((int)blockIdx.x << rt_log2) + r.rt;
+  r.row0 = r.tile * kTileRows;
+  r.w_begin = (int)blockIdx.y * slab_words;
+  r.w_count = min(slab_words, wpr - r.w_begin);
+  const int ngroups = (r.w_count + kGroupWords - 1) / kGroupWords;
+  r.my_groups = ngroups > r.cw ? (ngroups - r.cw + r.wpt - 1) >> (3 - rt_log2) : 0;
+  return r;
 }
 
-// Sign words of this wave's groups as unconditional buffer loads.  Lanes
-// past the last row or the slab's last word read data that never reaches a
-// stored output: a ragged group's tail meets the zero slot on the B side,
-// and rows past `rows` are not written.  Groups past my_groups use an
-// out-of-range offset: no branch, so the compiler has no join at which to
-// wait for them.
-__device__ __forceinline__ void load_signs(u32x2 (&wv)[kMaxGroups], const uint32_t *M, int rows,
-                                           int wpr, const Tile &t, int wave, int lane) {
-  const int rho = lane & 15;
-  const int q = lane >> 4;
-  const __amdgpu_buffer_rsrc_t mres = buffer_rsrc(
-      M + (size_t)t.row0 * wpr, (int64_t)(rows - t.row0) * wpr * 4);
-#pragma unroll
-  for (int i = 0; i < kMaxGroups; ++i) {
-    const int wl = (wave + kWaves * i) * kGroupWords + 2 * q;
-    // One 8-byte load per lane.  Buffer range checking applies per dword, so
-    // with an odd number of words per row a pair whose second word lies past
-    // the buffer still returns its first word (and zero for the second); a
-    // second word past the row but inside the buffer is an out-of-slab word
-    // and meets the zero slot.
-    const int off = i < t.my_groups ? (rho * wpr + t.w_begin + wl) * 4 : kOob;
-    wv[i] = __builtin_amdgcn_raw_buffer_load_b64(mres, off, 0, 0);
-  }
-}
-
-// One workgroup's tile of one stage, its sign words already loaded: stage
-// the input, run the products, add the waves' results, scale and store.
+// One stage: a +-1 product of 16 * 2^rt_log2 rows of M against the staged
+// input columns of one slab, then the per-row scale.
 //
 // kHiLoCols (b <= 8): the bf16 hi and lo parts of batch row beta occupy MFMA
 // columns 2*beta and 2*beta+1, so one MFMA per tile covers both; otherwise
 // (b up to 16) columns are batch rows and hi and lo take one MFMA each.
-template <bool kInX, bool kOutY, bool kHiLoCols>
-__device__ __forceinline__ void stage_tile(const u32x2 (&wv)[kMaxGroups], const Tile &T,
-                                           int wave, int lane, int tid, uint8_t *lds,
-                                           const void *in, const uint16_t *s_in,
-                                           const uint16_t *row_scale, int rows, int wpr, int b,
-                                           int nslabs, int mode, int in_parts, void *out,
-                                           float *part, uint32_t *cnt) {
+//
+// Arguments are scalars, most urgent first, so that they are preloaded into
+// SGPRs at wave launch instead of being fetched from the kernarg segment.
+//
+// kMulti: several row tiles per workgroup (rt_log2 > 0, staging shared by
+// the workgroup); otherwise one tile, and rt_log2 is ignored.
+template <bool kInX, bool kOutY, bool kHiLoCols, bool kMulti>
+__global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
+    const uint32_t *__restrict__ M, const void *__restrict__ in,
+    const uint16_t *__restrict__ s_in, const uint16_t *__restrict__ row_scale, int rows,
+    int wpr, int slab_words, int b, int rt_log2_arg, int nslabs, int mode, int in_parts,
+    void *__restrict__ out, float *__restrict__ part, uint32_t *__restrict__ cnt) {
+  const int rt_log2 = kMulti ? rt_log2_arg : 0;
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // scalar: wave-uniform
+  const Role R = make_role(wave, rt_log2, wpr, slab_words);
   const size_t K = (size_t)wpr * 32;
-  const int w_begin = T.w_begin;
-  const int w_count = T.w_count;
-  const int my_groups = T.my_groups;
+  const int w_begin = R.w_begin;
+  const int w_count = R.w_count;
 
-  // B-operand lanes: column n, pair q.
+  // 1. Sign words of this wave's groups, issued before anything else as
+  //    unconditional buffer loads.  Lanes past the last row or the slab's
+  //    last word read data that never reaches a stored output: a ragged
+  //    group's tail meets the zero slot on the B side, and rows past `rows`
+  //    are not written.  Groups past my_groups use an out-of-range offset:
+  //    no branch, so the compiler has no join at which to wait for them.
+  //    One 8-byte load per lane; buffer range checking applies per dword,
+  //    so a pair whose second word lies past the buffer still returns its
+  //    first word (a second word past the row but inside the buffer is an
+  //    out-of-slab word and meets the zero slot).
+  const int rho = lane & 15;
   const int q = lane >> 4;
-  const int ncol = lane & 15;
-  const int beta = kHiLoCols ? (ncol >> 1) : ncol;
-  const int hl_col = kHiLoCols ? (ncol & 1) : 0;
-
-  // 1. Stage this wave's columns of the input as bf16 hi/lo (p, p+16) pairs,
-  //    one 144-byte slot per (batch row, word); slot 0 holds zeros for lanes
-  //    with no batch row and for the tail of a ragged group.  A wave reads
-  //    only slots it wrote itself, and a wave's LDS operations execute in
-  //    order, so no workgroup barrier is needed before the products.
-  uint8_t *xs = lds + kSlot;
-  if (lane < kSlot / 16) reinterpret_cast<uint4 *>(lds)[lane] = make_uint4(0u, 0u, 0u, 0u);
+  u32x2 wv[kMaxGroups];
   {
-    const int units_per_group = b * kGroupWords * 2;
-    const int nunits = my_groups * units_per_group;
+    const int64_t left = (int64_t)(rows - R.row0) * wpr * 4;
+    const __amdgpu_buffer_rsrc_t mres = buffer_rsrc(M + (size_t)R.row0 * wpr, left);
+    // The group count lives in a vector register here so that the choice of
+    // offset is a select, not a branch around the load.
+    int my_groups_v = R.my_groups;
+    asm volatile("" : "+v"(my_groups_v));
+#pragma unroll
+    for (int i = 0; i < kMaxGroups; ++i) {
+      const int wl = (R.cw + R.wpt * i) * kGroupWords + 2 * q;
+      const int off = i < my_groups_v ? (rho * wpr + w_begin + wl) * 4 : kOob;
+      wv[i] = __builtin_amdgcn_raw_buffer_load_b64(mres, off, 0, 0);
+    }
+  }
+
+  // 2. Stage the input columns as bf16 hi/lo (p, p+16) pairs, one 144-byte
+  //    slot per (batch row, word); slot 0 holds zeros for lanes with no
+  //    batch row and for the tail of a ragged group.  A unit is 8 columns
+  //    (and their partners 16 on) of one batch row.  With one row tile per
+  //    workgroup every wave stages exactly the columns of its own groups
+  //    (and reads only what it wrote, so no barrier is needed); with
+  //    several, the waves of different tiles share columns and the
+  //    workgroup stages the slab once, then meets a barrier.  A wave with
+  //    no unit in a pass issues no load (out-of-range loads still occupy the
+  //    load path); lanes without a unit in a wave that has some store to a
+  //    scratch slot instead of branching, so that no load is moved behind
+  //    another unit's wait.
+  uint8_t *xs = lds + kSlot;
+  if (tid < kSlot / 16) reinterpret_cast<uint4 *>(lds)[tid] = make_uint4(0u, 0u, 0u, 0u);
+  {
+    constexpr bool shared = kMulti;
+    const int per_group = b * kGroupWords * 2;  // units of one group
+    const int nunits = shared ? b * 2 * w_count : R.my_groups * per_group;
+    const int span = shared ? 2 * w_count : per_group;
+    const float inv_span = 1.0f / (float)span;
     const int part_elems = b * (int)K;  // stride between partial input arrays
     const __amdgpu_buffer_rsrc_t xres =
         buffer_rsrc(in, (int64_t)b * K * (kInX ? 2 : 4) * (kInX ? 1 : in_parts));
     const __amdgpu_buffer_rsrc_t sres = buffer_rsrc(s_in, kInX ? (int64_t)K * 2 : 0);
     const bool two_parts = !kInX && in_parts > 1;
+    uint8_t *junk = xs + (size_t)b * w_count * kSlot + (tid & 15) * kSlot;
+    // pass stride and this thread's first unit
+    const int stride = shared ? 2 * kThreads : 128;
+    const int first = shared ? tid : lane;
+    const int wave_first = shared ? 64 * wave : 0;
 #pragma unroll
     for (int it = 0; it < kStageIters; ++it) {
-      const int c0 = it * 2 * 64;
-      if (c0 >= nunits) break;  // wave-uniform
+      const int base = it * stride;
+      if (base >= nunits) break;  // uniform
       int slot_off[2], half[2], off[2], col[2];
+      bool has[2];
 #pragma unroll
       for (int k = 0; k < 2; ++k) {
-        const int cu = c0 + 64 * k + lane;
-        const int i = cu / units_per_group;
-        const int rem = cu - i * units_per_group;
-        const int bb = rem / (kGroupWords * 2);
-        const int r2 = rem - bb * (kGroupWords * 2);
-        const int wl = (wave + kWaves * i) * kGroupWords + (r2 >> 1);
-        const bool ok = cu < nunits && wl < w_count;
-        half[k] = r2 & 1;
+        const int u = base + (stride >> 1) * k + first;
+        has[k] = base + (stride >> 1) * k + wave_first < nunits;  // wave-uniform
+        const bool ok = u < nunits;
+        // u / span for u < 2^12: a float estimate, corrected by one step
+        int q0 = (int)((float)u * inv_span);
+        q0 -= q0 * span > u;
+        q0 += (q0 + 1) * span <= u;
+        q0 = ok ? q0 : 0;
+        const int rem = u - q0 * span;
+        int bb, wl;
+        if (shared) {
+          bb = q0;
+          wl = rem >> 1;
+          half[k] = rem & 1;
+        } else {
+          // q0 = the wave's group index i, rem = (batch row, word, half)
+          bb = rem >> 4;
+          wl = (R.cw + R.wpt * q0) * kGroupWords + ((rem & 15) >> 1);
+          half[k] = rem & 1;
+        }
+        const bool valid = ok && wl < w_count;
         col[k] = (w_begin + wl) * 32 + 8 * half[k];
-        off[k] = ok ? (int)(bb * K) + col[k] : kOob;
-        slot_off[k] = ok ? (bb * w_count + wl) * kSlot : -1;
+        off[k] = valid ? (int)(bb * K) + col[k] : kOob;
+        slot_off[k] = valid ? (bb * w_count + wl) * kSlot : -1;
       }
-      const bool two = c0 + 64 < nunits;  // wave-uniform
-      const UnitRaw raw0 = load_unit<kInX>(xres, sres, off[0], col[0]);
-      UnitRaw raw1, raw0b, raw1b;
-      if (two) raw1 = load_unit<kInX>(xres, sres, off[1], col[1]);
-      if (two_parts) {
-        raw0b = load_unit<kInX>(xres, sres, off[0], col[0], part_elems);
-        if (two) raw1b = load_unit<kInX>(xres, sres, off[1], col[1], part_elems);
+      UnitRaw raw[2], rawb[2];
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        if (has[k]) {
+          raw[k] = load_unit<kInX>(xres, sres, off[k], col[k]);
+          if (two_parts) rawb[k] = load_unit<kInX>(xres, sres, off[k], col[k], part_elems);
+        }
       }
-      float v[16];
-      if (slot_off[0] >= 0) {
-        unit_values<kInX>(raw0, v, two_parts ? &raw0b : nullptr);
-        store_unit(xs + slot_off[0], half[0], v);
-      }
-      if (two && slot_off[1] >= 0) {
-        unit_values<kInX>(raw1, v, two_parts ? &raw1b : nullptr);
-        store_unit(xs + slot_off[1], half[1], v);
+#pragma unroll
+      for (int k = 0; k < 2; ++k) {
+        if (has[k]) {
+          float v[16];
+          unit_values<kInX>(raw[k], v, two_parts ? &rawb[k] : nullptr);
+          store_unit(slot_off[k] >= 0 ? xs + slot_off[k] : junk, half[k], v);
+        }
       }
     }
   }
-  // Row scale of the output this thread writes at the end (loaded after the
-  // staging loads so that waiting for it waits for nothing else).
-  const int orow_l = tid >> 4;
-  const int obeta = tid & 15;
-  const int orow = T.row0 + orow_l;
-  const bool active = tid < kTileRows * 16 && obeta < b && orow < rows;
-  const uint32_t rscale_bits = __builtin_amdgcn_raw_buffer_load_b16(
-      buffer_rsrc(row_scale, (int64_t)rows * 2), orow * 2, 0, 0);
-  __builtin_amdgcn_wave_barrier();
+  // Row scales of the outputs this thread writes at the end (loaded after
+  // the staging loads so that waiting for them waits for nothing else).
+  // Outputs o = tid + kThreads * k: row (o mod rows_per_wg) of the
+  // workgroup's rows, batch row o / rows_per_wg.
+  const int rows_log2 = 4 + rt_log2;
+  const int rows_wg = 1 << rows_log2;
+  const int row_wg0 = (int)blockIdx.x * rows_wg;
+  const int nout = rows_wg * b;
+  // uniform, <= kMaxOutPerThread (one tile: 16 b <= 256 outputs)
+  const int nk_out = kMulti ? (nout + kThreads - 1) / kThreads : 1;
+  uint32_t rscale_bits[kMaxOutPerThread];
+  {
+    const __amdgpu_buffer_rsrc_t rres = buffer_rsrc(row_scale, (int64_t)rows * 2);
+#pragma unroll
+    for (int k = 0; k < kMaxOutPerThread; ++k) {
+      // the first load is unconditional (and so is its use below): a load
+      // whose only use sits in a branch is moved there, behind every wait
+      if (k > 0 && k >= nk_out) break;
+      const int o = tid + kThreads * k;
+      const int orow = row_wg0 + (o & (rows_wg - 1));
+      rscale_bits[k] = __builtin_amdgcn_raw_buffer_load_b16(rres, o < nout ? orow * 2 : kOob, 0, 0);
+    }
+  }
+  if constexpr (kMulti)
+    __syncthreads();  // the staged slab is complete
+  else
+    __builtin_amdgcn_wave_barrier();
 
-  // 2. Products.  Step s = (group i = s / 2, word u = s % 2); independent
+  // 3. Products.  Step s = (group i = s / 2, word u = s % 2); independent
   //    accumulator chains per pair quad t (and per hi/lo when they are not
   //    in columns); the B operands of the next step are read from LDS while
   //    this step's MFMAs run.  Only lanes whose column carries a batch row
   //    read LDS; the others keep zero operands.
+  const int ncol = lane & 15;
+  const int beta = kHiLoCols ? (ncol >> 1) : ncol;
+  const int hl_col = kHiLoCols ? (ncol & 1) : 0;
   uint32_t kSignMask, kOne;
   asm volatile("v_mov_b32 %0, 0x80008000" : "=v"(kSignMask));
   asm volatile("v_mov_b32 %0, 0x3f803f80" : "=v"(kOne));
@@ -328,10 +397,10 @@ __device__ __forceinline__ void stage_tile(const u32x2 (&wv)[kMaxGroups], const 
   for (int t = 0; t < 4; ++t)
 #pragma unroll
     for (int hl = 0; hl < kChains; ++hl) acc[t][hl] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const int nsteps = my_groups * 2;
+  const int nsteps = R.my_groups * 2;
   const bool b_lane = beta < b;
   auto b_ptr = [&](int st) -> const uint8_t * {
-    const int wl = (wave + kWaves * (st >> 1)) * kGroupWords + 2 * q + (st & 1);
+    const int wl = (R.cw + R.wpt * (st >> 1)) * kGroupWords + 2 * q + (st & 1);
     return wl < w_count ? xs + ((size_t)beta * w_count + wl) * kSlot + 64 * hl_col : lds;
   };
   uint4 bop[2][kReads];
@@ -375,112 +444,162 @@ __device__ __forceinline__ void stage_tile(const u32x2 (&wv)[kMaxGroups], const 
     for (int hl = 0; hl < kChains; ++hl)
       if (t | hl) tot += acc[t][hl];
 
-  // 3. Add the waves' 16x16 tiles through LDS (after every wave is done
-  //    reading its staged operands).  Accumulator layout: lane l holds rows
-  //    4*(l/16) + i (i = 0..3) of column l mod 16.
+  // 4. Add the 16x16 tiles of the waves that share a row tile, through LDS
+  //    (after every wave is done reading the staged input).  Accumulator
+  //    layout: lane l holds rows 4*(l/16) + i (i = 0..3) of column l mod 16.
   __syncthreads();
-  float4 *red = reinterpret_cast<float4 *>(lds);
-  red[wave * 64 + lane] = make_float4(tot[0], tot[1], tot[2], tot[3]);
+  reinterpret_cast<float4 *>(lds)[wave * 64 + lane] = make_float4(tot[0], tot[1], tot[2], tot[3]);
   __syncthreads();
-  float sum = 0.f;
-  if (tid < kTileRows * 16) {
-    const float *redf = reinterpret_cast<const float *>(lds);
-    const int c0 = kHiLoCols ? 2 * obeta : obeta;
-    const int l0 = 16 * (orow_l >> 2) + (c0 & 15);
+  const float *redf = reinterpret_cast<const float *>(lds);
+  float sum[kMaxOutPerThread];
 #pragma unroll
-    for (int wv2 = 0; wv2 < kWaves; ++wv2) {
-      sum += redf[(wv2 * 64 + l0) * 4 + (orow_l & 3)];
-      if constexpr (kHiLoCols) sum += redf[(wv2 * 64 + l0 + 1) * 4 + (orow_l & 3)];
+  for (int k = 0; k < kMaxOutPerThread; ++k) {
+    sum[k] = 0.f;
+    if (k >= nk_out) break;
+    const int o = tid + kThreads * k;
+    if (o < nout) {
+      const int r_wg = o & (rows_wg - 1);
+      const int obeta = o >> rows_log2;
+      const int rt = r_wg >> 4, orow_l = r_wg & 15;
+      const int c0 = kHiLoCols ? 2 * obeta : obeta;
+      const int l0 = 16 * (orow_l >> 2) + (c0 & 15);
+#pragma unroll
+      for (int c = 0; c < kWaves; ++c) {
+        if (c >= R.wpt) break;
+        const int wv2 = rt * R.wpt + c;
+        sum[k] += redf[(wv2 * 64 + l0) * 4 + (orow_l & 3)];
+        if constexpr (kHiLoCols) sum[k] += redf[(wv2 * 64 + l0 + 1) * 4 + (orow_l & 3)];
+      }
     }
   }
 
   if (mode == kModeLastSlab) {
-    // Publish this slab's partial sum; the last slab of the tile to arrive
-    // adds all partials in slab order and resets the tile's counter.
-    if (active) store_device(&part[((size_t)T.slab * b + obeta) * rows + orow], sum);
+    // Publish this slab's partial sums; the last slab of the workgroup's
+    // rows to arrive adds all partials in slab order and resets the counter.
+#pragma unroll
+    for (int k = 0; k < kMaxOutPerThread; ++k) {
+      if (k >= nk_out) break;
+      const int o = tid + kThreads * k;
+      const int orow = row_wg0 + (o & (rows_wg - 1));
+      if (o < nout && orow < rows)
+        store_device(&part[((size_t)blockIdx.y * b + (o >> rows_log2)) * rows + orow], sum[k]);
+    }
     wait_memory();
     __syncthreads();
     __shared__ uint32_t s_last;
     if (tid == 0)
-      s_last = __hip_atomic_fetch_add(&cnt[T.tile], 1u, __ATOMIC_RELAXED,
+      s_last = __hip_atomic_fetch_add(&cnt[blockIdx.x], 1u, __ATOMIC_RELAXED,
                                       __HIP_MEMORY_SCOPE_AGENT) == (uint32_t)(nslabs - 1);
     __syncthreads();
     if (!s_last) return;
-    if (active) {
-      sum = 0.f;
-      for (int sl = 0; sl < nslabs; ++sl)
-        sum += __hip_atomic_load(&part[((size_t)sl * b + obeta) * rows + orow], __ATOMIC_RELAXED,
-                                 __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+    for (int k = 0; k < kMaxOutPerThread; ++k) {
+      if (k >= nk_out) break;
+      const int o = tid + kThreads * k;
+      const int orow = row_wg0 + (o & (rows_wg - 1));
+      if (o < nout && orow < rows) {
+        sum[k] = 0.f;
+        for (int sl = 0; sl < nslabs; ++sl)
+          sum[k] += __hip_atomic_load(&part[((size_t)sl * b + (o >> rows_log2)) * rows + orow],
+                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
     }
-    if (tid == 0) __hip_atomic_store(&cnt[T.tile], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (tid == 0) __hip_atomic_store(&cnt[blockIdx.x], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  if (active) {
-    float v = sum * f16_to_f32((uint16_t)rscale_bits);
-    size_t o = (size_t)obeta * rows + orow;
-    if (mode == kModePartial) o += (size_t)T.slab * b * rows;
-    if constexpr (kOutY)
-      static_cast<uint16_t *>(out)[o] = f32_to_bf16(v);
-    else
-      static_cast<float *>(out)[o] = v;
+#pragma unroll
+  for (int k = 0; k < kMaxOutPerThread; ++k) {
+    if (k > 0 && k >= nk_out) break;
+    const int o = tid + kThreads * k;
+    const int orow = row_wg0 + (o & (rows_wg - 1));
+    const float v = sum[k] * f16_to_f32((uint16_t)rscale_bits[k]);
+    if (o < nout && orow < rows) {
+      size_t oi = (size_t)(o >> rows_log2) * rows + orow;
+      if (mode == kModePartial) oi += (size_t)blockIdx.y * b * rows;
+      if constexpr (kOutY)
+        static_cast<uint16_t *>(out)[oi] = f32_to_bf16(v);
+      else
+        static_cast<float *>(out)[oi] = v;
+    }
   }
 }
 
-// One stage as its own launch: workgroup (tile, slab) = (blockIdx.x,
-// blockIdx.y).  Arguments are scalars, most urgent first, so that they are
-// preloaded into SGPRs at wave launch instead of being fetched from the
-// kernarg segment.
-template <bool kInX, bool kOutY, bool kHiLoCols>
-__global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
-    const uint32_t *__restrict__ M, const void *__restrict__ in,
-    const uint16_t *__restrict__ s_in, const uint16_t *__restrict__ row_scale, int rows,
-    int wpr, int slab_words, int b, int nslabs, int mode, int in_parts,
-    void *__restrict__ out, float *__restrict__ part, uint32_t *__restrict__ cnt) {
-  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // scalar: wave-uniform
-  const Tile T = make_tile(blockIdx.x, blockIdx.y, wpr, slab_words, wave);
-  u32x2 wv[kMaxGroups];
-  load_signs(wv, M, rows, wpr, T, wave, lane);
-  stage_tile<kInX, kOutY, kHiLoCols>(wv, T, wave, lane, tid, lds, in, s_in, row_scale, rows, wpr,
-                                     b, nslabs, mode, in_parts, out, part, cnt);
-}
-
-// Largest slab (in words, a multiple of kGroupWords) whose staged input fits LDS.
-int slab_words_for(int64_t b, int64_t wpr) {
-  int64_t w = (kLdsBytes - kSlot) / (kSlot * b);
-  w -= w % kGroupWords;
-  if (w < kGroupWords) w = kGroupWords;
-  return (int)(w < wpr ? w : ((wpr + kGroupWords - 1) / kGroupWords) * kGroupWords);
-}
-
-size_t lds_bytes_for(int64_t b, int slab_words, int64_t wpr) {
-  const int64_t w = slab_words < wpr ? slab_words : wpr;
-  size_t stage = (size_t)kSlot * (1 + (size_t)b * w);
+size_t lds_bytes_for(int64_t b, int slab_words) {
+  // zero slot, staged slots, 16 scratch slots for lanes without a unit
+  const size_t stage = (size_t)kSlot * (1 + (size_t)b * slab_words + 16);
   return stage > (size_t)kRedBytes ? stage : (size_t)kRedBytes;
 }
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
-// How one stage splits its columns.  Slabs are forced when b * K does not
-// fit the LDS budget (the last slab of each tile adds the partials).  When a
-// single slab fits but the row tiles alone would leave most compute units
-// idle, the columns are split in two and the next stage adds the two
-// partial results while staging its input.
+// Compute units of the current device, queried once per device.
+int device_cus() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
+  if (dev < 64) {
+    const int c = cache[dev].load(std::memory_order_relaxed);
+    if (c > 0) return c;
+  }
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    return 256;
+  if (dev < 64) cache[dev].store(cus, std::memory_order_relaxed);
+  return cus;
+}
+
+// How one stage is split over workgroups.
+//  rt_log2: rows per workgroup = 16 << rt_log2.  More rows per workgroup
+//    share one staged copy of the input (its conversion and its reads are
+//    paid once per workgroup), which matters as the batch grows; fewer rows
+//    per workgroup spread a small stage over more compute units.
+//  slab_words: columns (in words) per workgroup; at most what one wave's
+//    groups and the LDS budget allow.  Several slabs are added by the last
+//    one to finish, or (stage 1, few row tiles, small batch) each writes a
+//    partial result that the next stage adds while staging.
 struct StagePlan {
-  int slab_words, nslabs, mode;
+  int rt_log2, slab_words, nslabs, mode;
 };
 
-StagePlan plan_stage(int64_t rows, int64_t wpr, int64_t b, bool allow_partial) {
-  StagePlan p{slab_words_for(b, wpr), 0, kModeFinal};
+int max_slab_words(int64_t b, int rt_log2) {
+  int64_t w = (kLdsBudget - 17 * kSlot) / (kSlot * b);
+  const int64_t per_waves = (int64_t)kMaxGroups * kGroupWords * (kWaves >> rt_log2);
+  if (w > per_waves) w = per_waves;
+  return (int)(w - w % kGroupWords);
+}
+
+StagePlan plan_stage(int64_t rows, int64_t wpr, int64_t b, bool allow_partial, int cus) {
+  const int64_t tiles = (rows + kTileRows - 1) / kTileRows;
+  // Preferred tiles per workgroup for this batch (input shared over more
+  // rows as b grows), then: no more workgroups than two per compute unit,
+  // no fewer than half a workgroup per compute unit, at most
+  // kMaxOutPerThread outputs per thread.
+  int want = b >= 8 ? 3 : (b >= 4 ? 2 : (b >= 2 ? 1 : 0));
+  int rt = 0;
+  auto wgs = [&](int r) {
+    const int sw = max_slab_words(b, r);
+    const int64_t ns = (wpr + sw - 1) / sw;
+    return ((tiles + (1 << r) - 1) >> r) * ns;
+  };
+  while (rt < 3 && (((tiles + (1 << rt) - 1) >> rt) > 2 * cus)) ++rt;
+  while (rt < want && wgs(rt + 1) >= cus / 2) ++rt;
+  while (((int64_t)kTileRows << rt) * b > (int64_t)kThreads * kMaxOutPerThread) --rt;
+  StagePlan p{rt, 0, 0, kModeFinal};
+  int sw = max_slab_words(b, rt);
+  if (rt == 0) {
+    // per-wave staging: at most kWaveStageUnits units (groups x b x 16) per wave
+    const int groups_per_wave = kWaveStageUnits / (int)(b * kGroupWords * 2);
+    const int cap = groups_per_wave * kGroupWords * kWaves;
+    if (sw > cap) sw = cap;
+  }
+  p.slab_words = (int)(sw < wpr ? sw : ((wpr + kGroupWords - 1) / kGroupWords) * kGroupWords);
   p.nslabs = (int)((wpr + p.slab_words - 1) / p.slab_words);
   if (p.nslabs > 1) {
     p.mode = kModeLastSlab;
     return p;
   }
-  const int64_t tiles = (rows + kTileRows - 1) / kTileRows;
   const int64_t groups = (wpr + kGroupWords - 1) / kGroupWords;
-  if (allow_partial && tiles < 192 && groups >= 2 && b <= 8) {
+  if (allow_partial && rt == 0 && tiles < 192 && groups >= 2 && b <= 8) {
     p.slab_words = (int)(((groups + 1) / 2) * kGroupWords);
     p.nslabs = (int)((wpr + p.slab_words - 1) / p.slab_words);
     p.mode = p.nslabs > 1 ? kModePartial : kModeFinal;
@@ -494,17 +613,17 @@ struct WsLayout {
 };
 
 // Workspace: a fixed header, then the shape-dependent arrays.  The header
-// holds the arrival counters (one per 16-row tile of each stage), which must
-// be zero at the start of a call, at offsets that do not depend on the
-// shape, so that calls of different shapes can share one workspace without
-// their arrays ever overlapping another shape's counters.
+// holds the arrival counters (one per workgroup row group of each stage),
+// which must be zero at the start of a call, at offsets that do not depend
+// on the shape, so that calls of different shapes can share one workspace
+// without their arrays ever overlapping another shape's counters.
 constexpr size_t kMaxTiles = ((size_t)1 << 20) / kTileRows;  // rows <= 2^20
 constexpr size_t kHeaderBytes = 2 * kMaxTiles * 4;
 
-WsLayout ws_layout(int64_t m, int64_t n, int64_t r, int64_t b) {
+WsLayout ws_layout(int64_t m, int64_t n, int64_t r, int64_t b, int cus) {
   WsLayout L{};
-  L.p1 = plan_stage(r, n / 32, b, true);
-  L.p2 = plan_stage(m, r / 32, b, false);
+  L.p1 = plan_stage(r, n / 32, b, true, cus);
+  L.p2 = plan_stage(m, r / 32, b, false, cus);
   L.cnt1 = 0;
   L.cnt2 = kMaxTiles * 4;
   const int tparts = L.p1.mode == kModePartial ? L.p1.nslabs : 1;
@@ -532,27 +651,34 @@ struct StageArgs {
 
 template <bool kInX, bool kOutY>
 hipError_t launch_stage(const StageArgs &a, const StagePlan &p, hipStream_t s) {
-  // The kernel stages at most kStageIters * 128 units per wave.
-  const int groups = (p.slab_words + kGroupWords - 1) / kGroupWords;
-  if ((int64_t)((groups + kWaves - 1) / kWaves) * a.b * kGroupWords * 2 > kStageIters * 128)
-    return hipErrorInvalidValue;
-  dim3 grid((unsigned)((a.rows + kTileRows - 1) / kTileRows), (unsigned)p.nslabs);
-  const size_t lds = lds_bytes_for(a.b, p.slab_words, a.wpr);
-  if (a.b <= 8)
-    gemv_stage_kernel<kInX, kOutY, true><<<grid, kThreads, lds, s>>>(
-        a.M, a.in, a.s_in, a.row_scale, a.rows, a.wpr, p.slab_words, a.b, p.nslabs, p.mode,
-        a.in_parts, a.out, a.part, a.cnt);
-  else
-    gemv_stage_kernel<kInX, kOutY, false><<<grid, kThreads, lds, s>>>(
-        a.M, a.in, a.s_in, a.row_scale, a.rows, a.wpr, p.slab_words, a.b, p.nslabs, p.mode,
-        a.in_parts, a.out, a.part, a.cnt);
+  const int rows_wg = kTileRows << p.rt_log2;
+  if ((int64_t)rows_wg * a.b > (int64_t)kThreads * kMaxOutPerThread) return hipErrorInvalidValue;
+  dim3 grid((unsigned)((a.rows + rows_wg - 1) / rows_wg), (unsigned)p.nslabs);
+  const size_t lds = lds_bytes_for(a.b, p.slab_words < a.wpr ? p.slab_words : a.wpr);
+  auto go = [&](auto kernel) {
+    kernel<<<grid, kThreads, lds, s>>>(a.M, a.in, a.s_in, a.row_scale, a.rows, a.wpr,
+                                       p.slab_words, a.b, p.rt_log2, p.nslabs, p.mode,
+                                       a.in_parts, a.out, a.part, a.cnt);
+  };
+  const bool multi = p.rt_log2 > 0;
+  if (a.b <= 8) {
+    if (multi)
+      go(gemv_stage_kernel<kInX, kOutY, true, true>);
+    else
+      go(gemv_stage_kernel<kInX, kOutY, true, false>);
+  } else {
+    if (multi)
+      go(gemv_stage_kernel<kInX, kOutY, false, true>);
+    else
+      go(gemv_stage_kernel<kInX, kOutY, false, false>);
+  }
   return hipGetLastError();
 }
 
 }  // namespace
 
 size_t gemv_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t b) {
-  return ws_layout(m, n, r, b).total;
+  return ws_layout(m, n, r, b, device_cus()).total;
 }
 
 hipError_t launch_gemv(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
@@ -560,7 +686,7 @@ hipError_t launch_gemv(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
                        const uint16_t *s_mid, const uint16_t *s_in,
                        const uint16_t *x, int64_t b, uint16_t *y, void *ws,
                        hipStream_t s) {
-  const WsLayout L = ws_layout(m, n, r, b);
+  const WsLayout L = ws_layout(m, n, r, b, device_cus());
   uint8_t *base = static_cast<uint8_t *>(ws);
   float *t = reinterpret_cast<float *>(base + L.t);
   const StageArgs s1{Bv, x, s_in, s_mid, (int)r, (int)(n / 32), (int)b, 1, t,
