@@ -34,8 +34,8 @@ POOL_BYTES = 512 << 20          # > 2 x 256 MB MALL
 # the source hash differs.
 GEMV_TRAFFIC = {"sources": ("paper_2609_06161_amd/csrc/af1_gemv.hip",
                             "paper_2609_06161_amd/csrc/af1_device.h"),
-                "sha256": "80ed57a5f966d2af6c994ce2fe5a144e3613f8e6a4e0a38005b2c3c254b1b099",
-                "bytes_per_call": 2708887}
+                "sha256": "eadb73eb7c8230e057b0356718548d95d983e3e7f9ad33900d4733cc485d00f9",
+                "bytes_per_call": 2686479}
 
 
 def measured_gemv_traffic():
