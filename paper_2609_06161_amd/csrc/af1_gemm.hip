@@ -15,8 +15,9 @@
 // operation produce two fp16 operands (column-scale pair XOR the two sign
 // bits).  The activations are kept in the same order: inside every group
 // of 32 columns, column p sits at position 2p and column p+16 at 2p+1.  A
-// pre-pass writes x in that order (converting bf16 to fp16 once, instead
-// of once per weight-row tile) and the column scales as pair dwords, and G1
+// preparation pass writes x in that order (converting bf16 to fp16 once,
+// instead of once per weight-row tile) and the column scales as pair dwords
+// (one launch for all three), and G1
 // writes Z in that order, so the GEMMs stage their operands with plain
 // copies.
 //
@@ -130,11 +131,9 @@ __device__ __forceinline__ int pair_pos(int c) {
 // x (bf16, [T][K]) -> xp (fp16, [T][K], pair order).  One thread per 16
 // columns: 8 columns c .. c+7 and their partners c+16 .. c+23 become the
 // pair dwords 8h .. 8h+7 of their group.
-__global__ __launch_bounds__(256) void pair_order_kernel(const uint16_t *__restrict__ x,
-                                                         uint16_t *__restrict__ xp, int T, int K) {
+__device__ __forceinline__ void pair_order_unit(const uint16_t *__restrict__ x,
+                                                uint16_t *__restrict__ xp, int K, int64_t u) {
   const int units_per_row = K / 16;
-  const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (u >= (int64_t)T * units_per_row) return;
   const int t = (int)(u / units_per_row);
   const int ur = (int)(u % units_per_row);
   const int c = (ur >> 1) * 32 + 8 * (ur & 1);
@@ -155,15 +154,35 @@ __global__ __launch_bounds__(256) void pair_order_kernel(const uint16_t *__restr
 // Column scales (fp16, [K]) -> pair dwords: dword 16q + p holds columns
 // 32q + p (low half) and 32q + p + 16 (high half); columns from K up to
 // Kpad (a multiple of BK) are zero, so a partial last K step adds nothing.
-__global__ __launch_bounds__(256) void colscale_pairs_kernel(const uint16_t *__restrict__ s,
-                                                             uint32_t *__restrict__ out, int K,
-                                                             int Kpad) {
-  const int d = blockIdx.x * 256 + threadIdx.x;
-  if (d >= Kpad / 2) return;
+__device__ __forceinline__ void colscale_pair(const uint16_t *__restrict__ s,
+                                              uint32_t *__restrict__ out, int K, int d) {
   const int c = (d >> 4) * 32 + (d & 15);
   const uint32_t lo = c < K ? s[c] : 0u;
   const uint32_t hi = c + 16 < K ? s[c + 16] : 0u;
   out[d] = lo | (hi << 16);
+}
+
+// The three operand preparations of one call in one launch: blocks
+// [0, nbx) convert x, the next nb1 build the G1 column-scale pairs (s_in),
+// the last ones the G2 pairs (s_mid).
+__global__ __launch_bounds__(256) void prep_kernel(const uint16_t *__restrict__ x,
+                                                   uint16_t *__restrict__ xp, int T, int n,
+                                                   const uint16_t *__restrict__ s_in,
+                                                   uint32_t *__restrict__ cs1, int npad,
+                                                   const uint16_t *__restrict__ s_mid,
+                                                   uint32_t *__restrict__ cs2, int r, int rpad,
+                                                   int nbx, int nb1) {
+  const int blk = blockIdx.x;
+  if (blk < nbx) {
+    const int64_t u = (int64_t)blk * 256 + threadIdx.x;
+    if (u < (int64_t)T * (n / 16)) pair_order_unit(x, xp, n, u);
+  } else if (blk < nbx + nb1) {
+    const int d = (blk - nbx) * 256 + threadIdx.x;
+    if (d < npad / 2) colscale_pair(s_in, cs1, n, d);
+  } else {
+    const int d = (blk - nbx - nb1) * 256 + threadIdx.x;
+    if (d < rpad / 2) colscale_pair(s_mid, cs2, r, d);
+  }
 }
 
 // C = rowscale * (A_pairorder x (sign(W) * colscale)^T).  kOutBf16: C is
@@ -364,11 +383,12 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
   base += align256((size_t)kpad(n) * 2);
   uint32_t *cs2 = reinterpret_cast<uint32_t *>(base);
   const int64_t units = T * (n / 16);
-  pair_order_kernel<<<(unsigned)((units + 255) / 256), 256, 0, s>>>(x, xp, (int)T, (int)n);
-  colscale_pairs_kernel<<<(unsigned)((kpad(n) / 2 + 255) / 256), 256, 0, s>>>(s_in, cs1, (int)n,
-                                                                                (int)kpad(n));
-  colscale_pairs_kernel<<<(unsigned)((kpad(r) / 2 + 255) / 256), 256, 0, s>>>(s_mid, cs2, (int)r,
-                                                                                (int)kpad(r));
+  const int nbx = (int)((units + 255) / 256);
+  const int nb1 = (int)((kpad(n) / 2 + 255) / 256);
+  const int nb2 = (int)((kpad(r) / 2 + 255) / 256);
+  prep_kernel<<<(unsigned)(nbx + nb1 + nb2), 256, 0, s>>>(x, xp, (int)T, (int)n, s_in, cs1,
+                                                           (int)kpad(n), s_mid, cs2, (int)r,
+                                                           (int)kpad(r), nbx, nb1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const unsigned gy = (unsigned)((T + BM - 1) / BM);
