@@ -211,6 +211,37 @@ def test_gemv_workspace_shared_by_shapes_and_batches(oracle):
             assert torch.equal(y, ref), (i, L.m, L.n, L.r, b)
 
 
+@pytest.mark.parametrize("m,n,r,b", [(14368, 4096, 3136, 4), (4128, 14336, 3136, 8),
+                                     (1056, 2080, 4064, 16), (14368, 4096, 3136, 16)])
+def test_gemv_multi_tile_workgroups_ragged(oracle, m, n, r, b):
+    """Batches whose plans give workgroups several 16-row tiles (2 to 8)
+    sharing one staged input, with row counts that leave the last workgroup
+    partly empty (m/16 = 898 and 258 tiles), every element checked, y
+    prefilled with NaN."""
+    lin = synth.make_linear(900 + b, m, n, r, b)
+    print(f"multi-tile m={m} n={n} r={r} b={b}", flush=True)
+    L = DeviceLayer.from_host(lin)
+    y = torch.full((b, m), 0x7FC0, dtype=torch.int16, device="cuda")
+    L.gemv(to_device(lin.x), y=y)
+    torch.cuda.synchronize()
+    ok, where = elementwise_ok(bf16_bits_to_f64(y), oracle_y(oracle, lin))
+    assert ok, where
+
+
+@pytest.mark.parametrize("m,n,r,b", [(1024, 1024, 1280, 1), (4096, 4096, 5120, 1),
+                                     (4096, 4096, 5120, 8)])
+def test_gemv_rank_above_dimensions(oracle, m, n, r, b):
+    """The paper's 2.5-bit setting has r > min(m, n) (Table 1): the same
+    kernels, with the second product the wider one."""
+    lin = synth.make_linear(40 + b, m, n, r, b)
+    assert max_row_rel_l2(gpu_gemv(lin), oracle_y(oracle, lin)) <= TOL
+
+
+def test_gemm_rank_above_dimensions(oracle):
+    lin = synth.make_linear(41, 4096, 4096, 5120, 96)
+    assert max_row_rel_l2(gpu_gemm(lin), oracle_y(oracle, lin)) <= TOL
+
+
 def test_gemv_deterministic():
     lin = synth.make_linear(9, 4096, 4096, 2016, 4)
     assert np.array_equal(gpu_gemv(lin), gpu_gemv(lin))
