@@ -56,9 +56,19 @@ constexpr int kTileRows = 16;        // MFMA M
 constexpr int kGroupWords = 8;       // one 8-byte load per lane covers 16 rows x 8 words
 constexpr int kMaxGroups = 8;        // groups per wave (single pass)
 constexpr int kSlot = 144;           // LDS bytes per (batch row, word): 64 hi + 64 lo + 16 pad
+
+// LDS bytes between the staged slots of consecutive batch rows: the words
+// of one row, plus 16 bytes when needed to make the stride an odd multiple
+// of 16 bytes, so that the lanes of an MFMA operand read (different batch
+// rows, same word) fall in distinct 16-byte bank groups.
+__host__ __device__ constexpr int row_stride(int w_count) {
+  return w_count * kSlot + ((w_count & 1) ? 0 : 16);
+}
 constexpr int kLdsBudget = 160 * 1024;  // LDS of one gfx950 compute unit
 constexpr int kRedBytes = kWaves * 64 * 16;
 constexpr int kMaxOutPerThread = 4;  // outputs (row, batch row) written per thread
+constexpr int kMaxSlabsLoaded = 8;   // partial sums loaded at once by the last slab
+constexpr int kDeviceScope = 16;     // buffer cache policy sc1: coherent across XCDs
 // Staging passes.  Shared staging: a slab holds at most (kLdsBudget - kSlot)
 // / kSlot words over all batch rows (2 units per word), taken two per thread
 // per pass.  Per-wave staging: 128 units per wave per pass; the plan keeps a
@@ -295,7 +305,8 @@ __global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
         buffer_rsrc(in, (int64_t)b * K * (kInX ? 2 : 4) * (kInX ? 1 : in_parts));
     const __amdgpu_buffer_rsrc_t sres = buffer_rsrc(s_in, kInX ? (int64_t)K * 2 : 0);
     const bool two_parts = !kInX && in_parts > 1;
-    uint8_t *junk = xs + (size_t)b * w_count * kSlot + (tid & 15) * kSlot;
+    const int bstride = row_stride(w_count);
+    uint8_t *junk = xs + (size_t)b * bstride + (tid & 15) * kSlot;
     // pass stride and this thread's first unit
     const int stride = shared ? 2 * kThreads : 128;
     const int first = shared ? tid : lane;
@@ -331,7 +342,7 @@ __global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
         const bool valid = ok && wl < w_count;
         col[k] = (w_begin + wl) * 32 + 8 * half[k];
         off[k] = valid ? (int)(bb * K) + col[k] : kOob;
-        slot_off[k] = valid ? (bb * w_count + wl) * kSlot : -1;
+        slot_off[k] = valid ? bb * bstride + wl * kSlot : -1;
       }
       UnitRaw raw[2], rawb[2];
 #pragma unroll
@@ -401,7 +412,7 @@ __global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
   const bool b_lane = beta < b;
   auto b_ptr = [&](int st) -> const uint8_t * {
     const int wl = (R.cw + R.wpt * (st >> 1)) * kGroupWords + 2 * q + (st & 1);
-    return wl < w_count ? xs + ((size_t)beta * w_count + wl) * kSlot + 64 * hl_col : lds;
+    return wl < w_count ? xs + (size_t)beta * row_stride(w_count) + wl * kSlot + 64 * hl_col : lds;
   };
   uint4 bop[2][kReads];
 #pragma unroll
@@ -492,17 +503,30 @@ __global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
                                       __HIP_MEMORY_SCOPE_AGENT) == (uint32_t)(nslabs - 1);
     __syncthreads();
     if (!s_last) return;
+    // Device-scope loads of every slab's partial, issued before any is
+    // added (the slab count is small: at most kMaxSlabsLoaded per pass).
+    const __amdgpu_buffer_rsrc_t pres = buffer_rsrc(part, (int64_t)nslabs * b * rows * 4);
 #pragma unroll
     for (int k = 0; k < kMaxOutPerThread; ++k) {
       if (k >= nk_out) break;
       const int o = tid + kThreads * k;
       const int orow = row_wg0 + (o & (rows_wg - 1));
-      if (o < nout && orow < rows) {
-        sum[k] = 0.f;
-        for (int sl = 0; sl < nslabs; ++sl)
-          sum[k] += __hip_atomic_load(&part[((size_t)sl * b + (o >> rows_log2)) * rows + orow],
-                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const bool mine = o < nout && orow < rows;
+      const int off0 = mine ? ((o >> rows_log2) * rows + orow) * 4 : kOob;
+      float acc_s = 0.f;
+      for (int sl0 = 0; sl0 < nslabs; sl0 += kMaxSlabsLoaded) {
+        float pv[kMaxSlabsLoaded];
+#pragma unroll
+        for (int q = 0; q < kMaxSlabsLoaded; ++q) {
+          const int sl = sl0 + q;
+          const int off = (sl < nslabs && off0 != kOob) ? off0 + sl * b * rows * 4 : kOob;
+          pv[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(pres, off, 0,
+                                                                                 kDeviceScope));
+        }
+#pragma unroll
+        for (int q = 0; q < kMaxSlabsLoaded; ++q) acc_s += pv[q];
       }
+      sum[k] = acc_s;
     }
     if (tid == 0) __hip_atomic_store(&cnt[blockIdx.x], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
@@ -525,7 +549,7 @@ __global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
 
 size_t lds_bytes_for(int64_t b, int slab_words) {
   // zero slot, staged slots, 16 scratch slots for lanes without a unit
-  const size_t stage = (size_t)kSlot * (1 + (size_t)b * slab_words + 16);
+  const size_t stage = (size_t)kSlot * 17 + (size_t)b * row_stride(slab_words);
   return stage > (size_t)kRedBytes ? stage : (size_t)kRedBytes;
 }
 
@@ -562,7 +586,7 @@ struct StagePlan {
 };
 
 int max_slab_words(int64_t b, int rt_log2) {
-  int64_t w = (kLdsBudget - 17 * kSlot) / (kSlot * b);
+  int64_t w = ((kLdsBudget - 17 * kSlot) / b - 16) / kSlot;
   const int64_t per_waves = (int64_t)kMaxGroups * kGroupWords * (kWaves >> rt_log2);
   if (w > per_waves) w = per_waves;
   return (int)(w - w % kGroupWords);
