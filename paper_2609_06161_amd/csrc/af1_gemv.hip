@@ -623,7 +623,11 @@ StagePlan plan_stage(int64_t rows, int64_t wpr, int64_t b, bool allow_partial, i
     return p;
   }
   const int64_t groups = (wpr + kGroupWords - 1) / kGroupWords;
-  if (allow_partial && rt == 0 && tiles < 192 && groups >= 2 && b <= 8) {
+  // Few row tiles: split the columns in two (more workgroups share the
+  // latency-bound work).  Long rows split even when the tiles nearly fill
+  // the device (per-workgroup sign expansion then dominates).
+  if (allow_partial && rt == 0 && (tiles < 192 || (tiles < cus && wpr >= 256)) && groups >= 2 &&
+      b <= 8) {
     p.slab_words = (int)(((groups + 1) / 2) * kGroupWords);
     p.nslabs = (int)((wpr + p.slab_words - 1) / p.slab_words);
     p.mode = p.nslabs > 1 ? kModePartial : kModeFinal;
