@@ -247,6 +247,13 @@ def bench_gemm(args, torch, stream):
         out[name]["speedup_vs_dense_bf16"] = msd / ms
         del xd, wd
     out["all3_tflops"] = total_flops / (total_ms * 1e-3) / 1e12
+    # MFMA roofline of the prefill leg: algorithmic flops 2*T*r*(m+n) of the
+    # three calls over their summed time, against the dense fp16 peak (the
+    # contractions run on fp16 operands).
+    out["roofline"] = {"bound": "mfma", "achieved": round(out["all3_tflops"], 1),
+                       "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                       "frac": round(out["all3_tflops"] / MFMA_F16_PEAK_TFLOPS, 4),
+                       "traffic": None}
     return out
 
 
