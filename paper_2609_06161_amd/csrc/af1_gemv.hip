@@ -22,18 +22,23 @@
 // as the A (signs) and B (inputs) operands agree, so the LDS copy of the
 // input is stored in the same (p, p+16) pairs.
 //
+// Workgroups.  A 512-thread workgroup owns 16 * 2^k output rows (k = 0..3,
+// chosen per stage from the batch and the row count: more rows per
+// workgroup share one staged copy of the input as the batch grows).  Its 8
+// waves are split over the 16-row tiles, and the waves of a tile split its
+// columns into groups of 8 words.
+//
 // Latency.  A decode-size call is bound by launch and memory latency, not
-// bandwidth.  Each workgroup owns a 16-row tile; its 8 waves split the
-// columns into groups of 8 words.  Every wave first issues the loads of its
-// sign words (buffer loads: out-of-range lanes read zeros, no branches, so
-// no early waits), then the loads of its own slice of the input, converts
-// that slice to bf16 hi/lo pairs in LDS (waves read only what they wrote,
-// so no workgroup barrier is needed), and runs its MFMAs with the LDS
-// operand reads double-buffered.  The waves' 16x16 results are added
-// through LDS.  When b * K is too large for one LDS slab the columns are
-// split over workgroups ("slabs"); each slab writes a partial sum and the
-// last slab of a row tile to finish (atomic counter) adds the partials in
-// slab order, so the result is deterministic.
+// bandwidth.  Every wave first issues the loads of its sign words (buffer
+// loads: out-of-range lanes read zeros, no branches, so no early waits),
+// then the input is loaded and converted to bf16 hi/lo pairs in LDS (with
+// one tile per workgroup each wave stages only the columns it uses and no
+// barrier is needed), and the MFMAs run with the LDS operand reads
+// double-buffered.  The 16x16 results of a tile's waves are added through
+// LDS.  When b * K is too large for one LDS slab the columns are split over
+// workgroups ("slabs"); each slab writes a partial sum and the last slab of
+// a row group to finish (atomic counter) adds the partials in slab order,
+// so the result is deterministic.
 #include <atomic>
 #include <utility>
 
