@@ -66,15 +66,21 @@ constexpr int kATile = BM * kARow;           // 32 KiB
 constexpr int kWTile = BN * kWords * 4;      // 4 KiB
 constexpr int kCsTile = kWords * 16 * 4;     // column-scale pair dwords of one K step
 // LDS map: A0 | A1 | W0 | W1 | CS0 | CS1 (both activation buffers first, so
-// every operand read is a 16-bit immediate offset from one address).
-constexpr int kA0 = 0;
-constexpr int kW0 = 2 * kATile;
-constexpr int kCs0 = kW0 + 2 * kWTile;
-constexpr int kLdsBytes = kCs0 + 2 * kCsTile;
+// every operand read is a 16-bit immediate offset from one address), for a
+// token tile of kBM rows (128, or 64 for grids that would give each compute
+// unit at most one workgroup).
+template <int kBM>
+struct Lds {
+  static constexpr int kATileT = kBM * kARow;
+  static constexpr int kA0 = 0;
+  static constexpr int kW0 = 2 * kATileT;
+  static constexpr int kCs0 = kW0 + 2 * kWTile;
+  static constexpr int kBytes = kCs0 + 2 * kCsTile;
+};
 constexpr int kOob = (int)0x80000000u;
-static_assert(BM * kARow == 32 * 1024 && kThreads == 256, "eight 1 KiB copies per wave");
+static_assert(BM * kARow == 32 * 1024 && kThreads == 256, "eight 1 KiB copies per wave at BM");
 static_assert(kCsTile == 64 * 4, "one 4-byte copy per lane of wave 0");
-static_assert(kA0 + kATile + 3 * 32 * kARow + kARow < 65536, "immediate LDS offsets");
+static_assert(kATile + 3 * 32 * kARow + kARow < 65536, "immediate LDS offsets");
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef int i32x4 __attribute__((ext_vector_type(4)));
@@ -187,7 +193,7 @@ __global__ __launch_bounds__(256) void prep_kernel(const uint16_t *__restrict__ 
 
 // C = rowscale * (A_pairorder x (sign(W) * colscale)^T).  kOutBf16: C is
 // bf16 in natural column order (y); otherwise fp16 in pair order (Z).
-template <bool kOutBf16>
+template <bool kOutBf16, int kBM>
 __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     const uint16_t *__restrict__ A, int T, int K, const uint32_t *__restrict__ W, int N,
     const uint32_t *__restrict__ cspairs, int Kpad, const uint16_t *__restrict__ rowscale,
@@ -196,28 +202,33 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  using LM = Lds<kBM>;
+  constexpr int kA0 = LM::kA0, kW0 = LM::kW0, kCs0 = LM::kCs0, kATile = LM::kATileT;
+  constexpr int kLdsBytes = LM::kBytes;
+  constexpr int kTokBlocks = kBM / 32;          // 32-token MFMA blocks per wave
+  constexpr int kACopies = kBM * kARow / 1024 / 4;  // 1 KiB copies per wave per step
 
   // Tile assignment: consecutive workgroups land on consecutive XCDs; give
   // each XCD a contiguous range of tiles (weight-row tiles fastest).
   const int nN = gridDim.x, nT = gridDim.y, total = nN * nT;
   int L = blockIdx.y * nN + blockIdx.x;
   if ((total & 7) == 0) L = (L & 7) * (total >> 3) + (L >> 3);
-  const int t0 = (L / nN) * BM;
+  const int t0 = (L / nN) * kBM;
   const int n0 = (L % nN) * BN;
 
   const int kw = K / 32;                       // sign words per row
   const int nk = (kw + kWords - 1) / kWords;   // K steps (the last may be partial)
 
   // Copy roles, fixed per lane (a step only moves the resources' bases).
-  //  Activations: wave w issues copies j = 8w + jj (jj < 8), each covering
+  //  Activations: wave w issues copies j = kACopies*w + jj, each covering
   //  token rows 4j .. 4j+3 of the tile; lane l fills chunk position l mod 16
   //  of row 4j + l/16 with the chunk whose index is that position XOR the
   //  row's low four bits.  Columns past K read the next row or zeros; they
   //  meet zero column scales.
-  int a_off[8];
+  int a_off[kACopies];
 #pragma unroll
-  for (int jj = 0; jj < 8; ++jj) {
-    const int tok = 4 * (8 * wave + jj) + (lane >> 4);
+  for (int jj = 0; jj < kACopies; ++jj) {
+    const int tok = 4 * (kACopies * wave + jj) + (lane >> 4);
     const int part = (lane & 15) ^ (tok & 15);
     a_off[jj] = t0 + tok < T ? (t0 + tok) * K * 2 + 16 * part : kOob;
   }
@@ -234,8 +245,8 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     const i32x4 as = copy_rsrc(A + step * BK, (int64_t)T * K * 2 - (int64_t)step * BK * 2);
     const i32x4 ws = copy_rsrc(W + step * kWords, (int64_t)N * kw * 4 - (int64_t)step * kWords * 4);
 #pragma unroll
-    for (int jj = 0; jj < 8; ++jj)
-      copy16(as, lds + kA0 + buf * kATile + (8 * wave + jj) * 1024, a_off[jj]);
+    for (int jj = 0; jj < kACopies; ++jj)
+      copy16(as, lds + kA0 + buf * kATile + (kACopies * wave + jj) * 1024, a_off[jj]);
 #pragma unroll
     for (int i = 0; i < 4; ++i) copy4(ws, lds + kW0 + buf * kWTile + (64 * wave + 16 * i) * 16, w_off[i]);
     if (wave == 0) {
@@ -268,9 +279,9 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
 #pragma unroll
     for (int e = 0; e < 4; ++e) sh[s][e] = 15 - (8 * s + 4 * g + e);
 
-  floatx16 acc[4][2];
+  floatx16 acc[kTokBlocks][2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < kTokBlocks; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
@@ -290,11 +301,11 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     const uint4 *cs = reinterpret_cast<const uint4 *>(lds + kCs0 + buf * kCsTile);
     const uint4 wq0 = wt[wrow_l], wq1 = wt[wrow_l + 32];
     const uint32_t wj[2][kWords] = {{wq0.x, wq0.y, wq0.z, wq0.w}, {wq1.x, wq1.y, wq1.z, wq1.w}};
-    half8 af[2][4];
+    half8 af[2][kTokBlocks];
     uint4 c4[2];
     auto read_ops = [&](int ks, int slot) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < kTokBlocks; ++i)
         af[slot][i] = *reinterpret_cast<const half8 *>(abase + a_rd[ks] + 32 * i * kARow);
       c4[slot] = cs[2 * ks + g];
     };
@@ -315,7 +326,7 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
         for (int e = 0; e < 4; ++e) bd[e] = cpair[e] ^ ((w << sh[ks & 1][e]) & kSignMask);
         const half8 bf = __builtin_bit_cast(half8, make_uint4(bd[0], bd[1], bd[2], bd[3]));
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < kTokBlocks; ++i)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[cur][i], bf, acc[i][j], 0, 0, 0);
       }
     });
@@ -337,7 +348,7 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     const float rs = rowscale ? f16_to_f32(rowscale[n]) : 1.0f;
     const int cpos = kOutBf16 ? n : pair_pos(n);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < kTokBlocks; ++i) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int t = t0 + 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
@@ -391,16 +402,31 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
                                                            (int)kpad(r), nbx, nb1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const unsigned gy = (unsigned)((T + BM - 1) / BM);
-  dim3 g1((unsigned)((r + BN - 1) / BN), gy);
-  bingemm_kernel<false><<<g1, kThreads, kLdsBytes, s>>>(xp, (int)T, (int)n, Bv, (int)r, cs1,
-                                                        (int)kpad(n), nullptr, Z);
-  e = hipGetLastError();
+  // A grid of 128-token tiles that gives each compute unit at most one
+  // workgroup (one wave per SIMD) uses 64-token tiles instead: twice the
+  // workgroups, each expanding its signs for half as many tokens.  Measured
+  // on 8192x8192 G1 (+2%); grids between one and two workgroups per unit
+  // were slower with it.
+  const int cus = device_cus();
+  auto launch = [&](auto kOut, const uint16_t *A, int64_t K, const uint32_t *W, int64_t N,
+                    const uint32_t *cs, const uint16_t *rs, uint16_t *C) {
+    constexpr bool kOutBf16 = decltype(kOut)::value;
+    const unsigned gx = (unsigned)((N + BN - 1) / BN);
+    const int64_t tiles128 = (int64_t)gx * ((T + BM - 1) / BM);
+    if (tiles128 <= (int64_t)cus && T > 64) {
+      dim3 g(gx, (unsigned)((T + 63) / 64));
+      bingemm_kernel<kOutBf16, 64><<<g, kThreads, Lds<64>::kBytes, s>>>(
+          A, (int)T, (int)K, W, (int)N, cs, (int)kpad(K), rs, C);
+    } else {
+      dim3 g(gx, (unsigned)((T + BM - 1) / BM));
+      bingemm_kernel<kOutBf16, BM><<<g, kThreads, Lds<BM>::kBytes, s>>>(
+          A, (int)T, (int)K, W, (int)N, cs, (int)kpad(K), rs, C);
+    }
+    return hipGetLastError();
+  };
+  e = launch(std::false_type{}, xp, n, Bv, r, cs1, nullptr, Z);
   if (e != hipSuccess) return e;
-  dim3 g2((unsigned)((m + BN - 1) / BN), gy);
-  bingemm_kernel<true><<<g2, kThreads, kLdsBytes, s>>>(Z, (int)T, (int)r, Bu, (int)m, cs2,
-                                                       (int)kpad(r), s_out, y);
-  return hipGetLastError();
+  return launch(std::true_type{}, Z, r, Bu, m, cs2, s_out, y);
 }
 
 }  // namespace af1

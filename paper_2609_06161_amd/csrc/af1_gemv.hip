@@ -560,23 +560,6 @@ size_t lds_bytes_for(int64_t b, int slab_words) {
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
-// Compute units of the current device, queried once per device.
-int device_cus() {
-  static std::atomic<int> cache[64];
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
-  if (dev < 64) {
-    const int c = cache[dev].load(std::memory_order_relaxed);
-    if (c > 0) return c;
-  }
-  int cus = 0;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      cus <= 0)
-    return 256;
-  if (dev < 64) cache[dev].store(cus, std::memory_order_relaxed);
-  return cus;
-}
-
 // How one stage is split over workgroups.
 //  rt_log2: rows per workgroup = 16 << rt_log2.  More rows per workgroup
 //    share one staged copy of the input (its conversion and its reads are
@@ -709,6 +692,23 @@ hipError_t launch_stage(const StageArgs &a, const StagePlan &p, hipStream_t s) {
 }
 
 }  // namespace
+
+// Compute units of the current device, queried once per device.
+int device_cus() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 256;
+  if (dev < 64) {
+    const int c = cache[dev].load(std::memory_order_relaxed);
+    if (c > 0) return c;
+  }
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    return 256;
+  if (dev < 64) cache[dev].store(cus, std::memory_order_relaxed);
+  return cus;
+}
 
 size_t gemv_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t b) {
   return ws_layout(m, n, r, b, device_cus()).total;

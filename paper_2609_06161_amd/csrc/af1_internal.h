@@ -8,6 +8,10 @@
 
 namespace af1 {
 
+// Compute units of the current device (queried once per device; 256 if the
+// query fails).
+int device_cus();
+
 hipError_t launch_pack(const void *src, int dtype, int64_t rows, int64_t cols,
                        uint32_t *dst, hipStream_t s);
 hipError_t launch_unpack(const uint32_t *words, int64_t rows, int64_t cols,
