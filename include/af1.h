@@ -138,15 +138,19 @@ AF1_API af1_status af1_linear_gemv(const af1_factorized_linear *L, const uint16_
 /*
  * af1_linear_gemm -- prefill-regime forward for T tokens on the matrix cores.
  *   x  : device, [T, n] bfloat16.       y : device, [T, m] bfloat16 (written).
- *   T  : 1 .. AF1_GEMM_MAX_TOKENS.
+ *   T  : 1 .. AF1_GEMM_MAX_TOKENS, and T * max(n, r) * 2 < 2^31 (the
+ *        kernels address operands with 32-bit byte offsets); otherwise
+ *        AF1_ERR_BATCH.  A sign matrix of 2 GiB or more is AF1_ERR_SHAPE.
  *   ws : device workspace of at least af1_gemm_workspace_bytes(m, n, r, T)
- *        bytes; holds the [T, r] intermediate.
+ *        bytes; holds the fp16 copy of x, the [T, r] intermediate and the
+ *        column-scale pairs.
  * Arithmetic: both products run on fp16 MFMA with fp32 accumulation.  The
  * sign of each factor entry is applied to the fp16 column scale (s_in for
  * the first product, s_mid for the second), so every operand is exact:
  * x enters as fp16 (exact for |x| < 65504), the intermediate is rounded
- * once to fp16 before the second product (|values| must stay below 65504),
- * s_out is applied in fp32 and y is rounded to bfloat16.
+ * once to fp16 before the second product (|values| must stay below 65504;
+ * values below 2^-14 keep fewer significant bits), s_out is applied in fp32
+ * and y is rounded to bfloat16.
  */
 AF1_API size_t af1_gemm_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T);
 AF1_API af1_status af1_linear_gemm(const af1_factorized_linear *L, const uint16_t *x,

@@ -116,11 +116,22 @@ size_t af1_gemm_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
 
 af1_status af1_linear_gemm(const af1_factorized_linear *L, const uint16_t *x, int64_t T,
                            uint16_t *y, void *ws, size_t ws_bytes, void *stream) {
+  // The kernels address each operand with 32-bit byte offsets: a sign
+  // matrix must stay below 2 GiB (else a shape error), and so must the
+  // [T, n] and [T, r] activations, which bounds T (else a batch error).
+  int64_t max_tokens = AF1_GEMM_MAX_TOKENS;
+  if (L && dim_ok(L->m) && dim_ok(L->n) && dim_ok(L->r)) {
+    if (L->m * (L->r / 32) * 4 > INT32_MAX || L->r * (L->n / 32) * 4 > INT32_MAX)
+      return AF1_ERR_SHAPE;
+    const int64_t widest = L->n > L->r ? L->n : L->r;
+    const int64_t limit = INT32_MAX / (2 * widest);
+    if (limit < max_tokens) max_tokens = limit;
+  }
   const size_t need = (L && dim_ok(L->m) && dim_ok(L->n) && dim_ok(L->r) && T >= 1 &&
-                       T <= AF1_GEMM_MAX_TOKENS)
+                       T <= max_tokens)
                           ? af1::gemm_workspace_bytes(L->m, L->n, L->r, T)
                           : 0;
-  const af1_status st = check_forward(L, x, T, AF1_GEMM_MAX_TOKENS, y, ws, ws_bytes, need);
+  const af1_status st = check_forward(L, x, T, max_tokens, y, ws, ws_bytes, need);
   if (st != AF1_OK) return st;
   return hip_status(af1::launch_gemm(L->m, L->n, L->r, L->Bu, L->Bv, L->s_out, L->s_mid,
                                      L->s_in, x, T, y, ws, as_stream(stream)));

@@ -130,6 +130,19 @@ def test_gemm_token_and_workspace_validation():
     assert gemm(L, T=2048, ws_bytes=need - 1) == af1.AF1_ERR_WORKSPACE
 
 
+def test_gemm_rejects_operands_beyond_32bit_offsets():
+    """The GEMM kernels address operands with 32-bit byte offsets: T * max(n,
+    r) * 2 must stay below 2^31 (a batch error), a sign matrix below 2 GiB (a
+    shape error); both are reported before anything is launched."""
+    L = fake_layer(4096, 32768, 2016)            # widest operand row: 64 KiB
+    assert gemm(L, T=32768, ws_bytes=1 << 40) == af1.AF1_ERR_BATCH
+    L = fake_layer(4096, 2048, 32768)            # Z rows are the widest here
+    assert gemm(L, T=32768, ws_bytes=1 << 40) == af1.AF1_ERR_BATCH
+    big = 1 << 20
+    assert gemm(fake_layer(big, 4096, big), T=1) == af1.AF1_ERR_SHAPE
+    assert gemm(fake_layer(4096, big, big), T=1) == af1.AF1_ERR_SHAPE
+
+
 def test_pack_validation():
     P = af1.af1_pack
     assert P(None, 0, 4, 64, Y, stream=0, check=False) == af1.AF1_ERR_NULL

@@ -242,6 +242,48 @@ def test_gemm_rank_above_dimensions(oracle):
     assert max_row_rel_l2(gpu_gemm(lin), oracle_y(oracle, lin)) <= TOL
 
 
+@pytest.mark.parametrize("layer", [0, 31])
+def test_gemv_stack_linears_heterogeneous_ranks(oracle, layer):
+    """The decoder-stack workload's ranks (drawn +-25% around the budget rank
+    with the stack at <= 1.0 BPW): every linear of one layer at b=1, each
+    checked element-wise."""
+    linears = [("q", 4096, 4096, 2016), ("k", 1024, 4096, 800), ("v", 1024, 4096, 800),
+               ("o", 4096, 4096, 2016), ("gate", 14336, 4096, 3136),
+               ("up", 14336, 4096, 3136), ("down", 4096, 14336, 3136)]
+    entries = synth.draw_stack_ranks(77, 32, linears, af1.af1_storage_bits)
+    for i, (name, m, n, r0, r) in enumerate(entries[7 * layer: 7 * layer + 7]):
+        lin = synth.make_linear(7000 + 7 * layer + i, m, n, r, 1)
+        print(f"stack layer {layer} {name}: {m}x{n} r={r}", flush=True)
+        ok, where = elementwise_ok(gpu_gemv(lin), oracle_y(oracle, lin))
+        assert ok, (name, r, where)
+
+
+def test_gemv_subnormal_scales(oracle):
+    """fp16 subnormal scales (no flush to zero anywhere on the decode path):
+    s_in, s_mid, s_out drawn from the subnormal range, x large enough that
+    y stays normal in bf16."""
+    m, n, r, b = 1024, 2048, 512, 3
+    lin = synth.make_linear(13, m, n, r, b)
+    rng = np.random.default_rng(5)
+    for name, k in (("s_in", n), ("s_mid", r), ("s_out", m)):
+        setattr(lin, name, rng.integers(1, 0x0400, size=k, dtype=np.uint16))
+    lin.x = synth.f32_to_bf16_bits(rng.standard_normal((b, n)).astype(np.float32) * 1e4)
+    ref = oracle_y(oracle, lin)
+    assert np.all(np.abs(ref[np.abs(ref) > 0]) > 1e-30)
+    assert max_row_rel_l2(gpu_gemv(lin), ref) <= TOL
+
+
+def test_gemm_max_tokens(oracle):
+    """The largest token count the entry point accepts (2^20) on a small
+    layer: sampled tokens, the last one included, against the oracle."""
+    m, n, r, T = 64, 96, 64, 1 << 20
+    lin = synth.make_linear(17, m, n, r, T)
+    y = gpu_gemm(lin)
+    idx = np.sort(np.random.default_rng(1).choice(T, 64, replace=False))
+    idx[-1] = T - 1
+    assert max_row_rel_l2(y[idx], oracle_y(oracle, lin, lin.x[idx])) <= TOL
+
+
 def test_gemv_deterministic():
     lin = synth.make_linear(9, 4096, 4096, 2016, 4)
     assert np.array_equal(gpu_gemv(lin), gpu_gemv(lin))
