@@ -257,6 +257,39 @@ def bench_gemm(args, torch, stream):
     return out
 
 
+def bench_pack(args, torch, stream):
+    """Sign -> bit packing of a 16384 x 16384 matrix from each source type:
+    HBM-bound, algorithmic bytes = source bytes + packed bytes."""
+    from paper_2609_06161_amd import af1
+    rows = cols = 16384
+    out = {}
+    dst = torch.empty(rows * cols // 32, dtype=torch.int32, device="cuda")
+    for name, dtype, code in (("f32", torch.float32, af1.AF1_SRC_F32),
+                              ("bf16", torch.bfloat16, af1.AF1_SRC_BF16),
+                              ("i8", torch.int8, af1.AF1_SRC_I8)):
+        g = torch.Generator(device="cuda")
+        g.manual_seed(3)
+        src = (torch.randint(-100, 100, (rows, cols), device="cuda", generator=g)
+               .to(dtype))
+        fn = lambda i: af1.af1_pack(src, code, rows, cols, dst, None)
+        time_events(fn, 3, stream)
+        ms = time_events(fn, 20, stream) / 20
+        nbytes = rows * cols * src.element_size() + rows * cols // 8
+        out[name] = dict(us=round(ms * 1e3, 1), gbs=round(nbytes / (ms * 1e-3) / 1e9, 1),
+                         frac=round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 3))
+        del src
+    # Context: a plain device copy of 1 GiB (read + write), the practical
+    # HBM rate of this GPU.
+    a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    c = torch.empty_like(a)
+    fn = lambda i: c.copy_(a)
+    time_events(fn, 3, stream)
+    ms = time_events(fn, 10, stream) / 10
+    out["copy_1GiB_gbs"] = round(2 * (1 << 30) / (ms * 1e-3) / 1e9, 1)
+    del a, c
+    return out
+
+
 def bench_cpu_oracle(args):
     import oracle
     from paper_2609_06161_amd import synth
@@ -331,6 +364,8 @@ def main():
     if not args.no_decode_table and args.only == "all":
         result["decode_table"] = bench_decode_table(args, torch, stream)
         result["decode_stack_8b"] = bench_stack(args, torch, stream)
+    if args.only == "all":
+        result["pack_16384x16384"] = bench_pack(args, torch, stream)
     if not args.no_gemm and args.only == "all":
         result["gemm"] = bench_gemm(args, torch, stream)
         result["gemm"]["peak_tflops"] = MFMA_F16_PEAK_TFLOPS
