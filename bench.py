@@ -161,7 +161,11 @@ def bench_stack(args, torch, stream):
     """An 8B-shaped decoder stack: 32 layers x 7 linears, per-linear ranks
     drawn +-25% around the budget rank with the whole stack <= 1.0 BPW,
     weights streamed from HBM in layer order, batch 1, each linear fed a
-    fixed synthetic x of its input width; one HIP graph of the whole pass."""
+    fixed synthetic x of its input width; one HIP graph of the whole pass.
+
+    Two schedules: the 224 linears one call each, and the projections that
+    read the same input fused into one call (q, k, v; gate, up), which is
+    how a decoder issues them: 4 calls per layer instead of 7."""
     from paper_2609_06161_amd import af1, synth
     from paper_2609_06161_amd.layer import to_device
     entries = synth.draw_stack_ranks(77, 32, STACK_LINEARS, af1.af1_storage_bits)
@@ -171,33 +175,51 @@ def bench_stack(args, torch, stream):
     for i, (name, m, n, r0, r) in enumerate(entries):
         P = DevicePool(torch, m, n, r, 1, 5000 + i)
         pools.append(P)
-        descs.append((P.desc[0], m, n, r))
+        descs.append((name, P.desc[0], m, n, r))
     xs = {w: to_device(synth.make_activations(60 + w % 97, 1, w)) for w in (4096, 14336)}
-    ys = {w: torch.empty((1, w), dtype=torch.int16, device="cuda") for w in (1024, 4096, 14336)}
-    ws = torch.zeros(max(af1.af1_gemv_workspace_bytes(m, n, r, 1) for _, m, n, r in descs),
-                     dtype=torch.uint8, device="cuda")
+    ys = {name: torch.empty((1, m), dtype=torch.int16, device="cuda")
+          for name, m, _, _ in STACK_LINEARS}
+    groups = []   # per layer: [q,k,v], [o], [gate,up], [down]
+    for layer in range(32):
+        q, k, v, o, gate, up, down = descs[7 * layer: 7 * layer + 7]
+        groups += [[q, k, v], [o], [gate, up], [down]]
+    ws_bytes = max(af1.af1_gemv_multi_workspace_bytes([e[1] for e in g], 1) for g in groups)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
 
-    def run_all():
-        for d, m, n, r in descs:
-            af1.af1_linear_gemv(d, xs[n], 1, ys[m], ws, ws.numel(), None)
+    def run_serial():
+        for name, d, m, n, r in descs:
+            af1.af1_linear_gemv(d, xs[n], 1, ys[name], ws, ws.numel(), None)
 
-    side = torch.cuda.Stream()
-    side.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(side):
-        run_all()
-    torch.cuda.current_stream().wait_stream(side)
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        run_all()
-    time_events(lambda i: graph.replay(), 2, stream)
-    reps = 10
-    ms = time_events(lambda i: graph.replay(), reps, stream) / reps
-    alg = sum(gemv_algorithmic_bytes(m, n, r, 1) for _, m, n, r in descs)
-    del graph, pools
-    return dict(linears=len(descs), bpw=round(bits / dense, 5), weight_mb=round(bits / 8 / 1e6, 1),
-                us_per_pass=round(ms * 1e3, 2), us_per_decoder_layer=round(ms * 1e3 / 32, 3),
-                us_per_linear=round(ms * 1e3 / len(descs), 3),
-                gbs=round(alg / (ms * 1e-3) / 1e9, 1))
+    def run_fused():
+        for g in groups:
+            n = g[0][3]
+            if len(g) == 1:
+                name, d, m, n, r = g[0]
+                af1.af1_linear_gemv(d, xs[n], 1, ys[name], ws, ws.numel(), None)
+            else:
+                af1.af1_linear_gemv_multi([e[1] for e in g], xs[n], 1, [ys[e[0]] for e in g],
+                                          ws, ws.numel(), None)
+
+    out = dict(linears=len(descs), bpw=round(bits / dense, 5), weight_mb=round(bits / 8 / 1e6, 1))
+    alg = sum(gemv_algorithmic_bytes(m, n, r, 1) for _, _, m, n, r in descs)
+    for label, fn in (("", run_serial), ("_fused_projections", run_fused)):
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            fn()
+        time_events(lambda i: graph.replay(), 2, stream)
+        reps = 10
+        ms = time_events(lambda i: graph.replay(), reps, stream) / reps
+        out[f"us_per_decoder_layer{label}"] = round(ms * 1e3 / 32, 3)
+        out[f"gbs{label}"] = round(alg / (ms * 1e-3) / 1e9, 1)
+        del graph
+    out["us_per_linear"] = round(out["us_per_decoder_layer"] / 7, 3)
+    del pools
+    return out
 
 
 def bench_decode_table(args, torch, stream):

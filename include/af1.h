@@ -136,6 +136,35 @@ AF1_API af1_status af1_linear_gemv(const af1_factorized_linear *L, const uint16_
                            void *stream);
 
 /*
+ * af1_linear_gemv_multi -- decode forward of several layers that read the
+ * same input x (all with the same n): the q, k and v projections of an
+ * attention block, or the gate and up projections of an MLP.  Each output
+ * is what af1_linear_gemv computes for its layer (same arithmetic; the
+ * grouping of an output's partial sums may differ).  All layers run in two
+ * launches when no layer needs a last-slab reduction at this batch (every
+ * configuration up to b = 8 at n, r <= 4096 does); otherwise the layers
+ * run one after the other on the same workspace.  A decode step at batch 1
+ * is bound by launch and memory latency, so fewer launches are the gain.
+ *   Ls    : host array of count layers, 1 <= count <= AF1_GEMV_MULTI_MAX.
+ *   x     : device, [b, n] bfloat16.
+ *   ys    : host array of count device pointers; ys[i] is [b, Ls[i].m]
+ *           bfloat16 (written).
+ *   ws    : device workspace of at least
+ *           af1_gemv_multi_workspace_bytes(Ls, count, b) bytes, header
+ *           zero-filled before first use as for af1_linear_gemv.
+ * Errors: as af1_linear_gemv for every layer; AF1_ERR_NULL for a NULL Ls,
+ * ys or ys[i]; AF1_ERR_SHAPE for a count outside 1..AF1_GEMV_MULTI_MAX or
+ * layers whose n differ; AF1_ERR_ALIAS when an output overlaps another
+ * output, x, any layer's arrays or ws.
+ */
+#define AF1_GEMV_MULTI_MAX 4
+AF1_API size_t af1_gemv_multi_workspace_bytes(const af1_factorized_linear *Ls, int32_t count,
+                                              int64_t b);
+AF1_API af1_status af1_linear_gemv_multi(const af1_factorized_linear *Ls, int32_t count,
+                                         const uint16_t *x, int64_t b, uint16_t *const *ys,
+                                         void *ws, size_t ws_bytes, void *stream);
+
+/*
  * af1_linear_gemm -- prefill-regime forward for T tokens on the matrix cores.
  *   x  : device, [T, n] bfloat16.       y : device, [T, m] bfloat16 (written).
  *   T  : 1 .. AF1_GEMM_MAX_TOKENS, and T * max(n, r) * 2 < 2^31 (the

@@ -23,6 +23,7 @@ AF1_ERR_DTYPE = 8
 
 AF1_SRC_F32, AF1_SRC_BF16, AF1_SRC_F16, AF1_SRC_I8 = 0, 1, 2, 3
 AF1_GEMV_MAX_BATCH = 16
+AF1_GEMV_MULTI_MAX = 4
 AF1_MAX_DIM = 1 << 20
 
 _lib = None
@@ -56,6 +57,10 @@ def lib():
     L.af1_gemv_workspace_bytes.argtypes = [I64, I64, I64, I64]
     L.af1_gemv_workspace_bytes.restype = SZ
     L.af1_linear_gemv.argtypes = [ctypes.POINTER(af1_factorized_linear), P, I64, P, P, SZ, P]
+    L.af1_gemv_multi_workspace_bytes.argtypes = [ctypes.POINTER(af1_factorized_linear), I32, I64]
+    L.af1_gemv_multi_workspace_bytes.restype = SZ
+    L.af1_linear_gemv_multi.argtypes = [ctypes.POINTER(af1_factorized_linear), I32, P, I64,
+                                        ctypes.POINTER(P), P, SZ, P]
     L.af1_gemm_workspace_bytes.argtypes = [I64, I64, I64, I64]
     L.af1_gemm_workspace_bytes.restype = SZ
     L.af1_linear_gemm.argtypes = [ctypes.POINTER(af1_factorized_linear), P, I64, P, P, SZ, P]
@@ -66,7 +71,8 @@ def lib():
     L.af1_status_string.argtypes = [I32]
     L.af1_status_string.restype = ctypes.c_char_p
     L.af1_version.restype = ctypes.c_char_p
-    for fn in ("af1_pack", "af1_unpack", "af1_linear_gemv", "af1_linear_gemm"):
+    for fn in ("af1_pack", "af1_unpack", "af1_linear_gemv", "af1_linear_gemv_multi",
+               "af1_linear_gemm"):
         getattr(L, fn).restype = I32
     _lib = L
     return L
@@ -132,6 +138,30 @@ def af1_linear_gemv(layer, x, b: int, y, ws, ws_bytes: int, stream=None, check=T
     st = lib().af1_linear_gemv(ref, _addr(x), b, _addr(y), _addr(ws), ws_bytes, _stream(stream))
     if check:
         _check(st, "af1_linear_gemv")
+    return st
+
+
+def _layer_array(layers):
+    arr = (af1_factorized_linear * len(layers))()
+    for i, L in enumerate(layers):
+        arr[i] = L
+    return arr
+
+
+def af1_gemv_multi_workspace_bytes(layers, b) -> int:
+    return int(lib().af1_gemv_multi_workspace_bytes(_layer_array(layers), len(layers), b))
+
+
+def af1_linear_gemv_multi(layers, x, b: int, ys, ws, ws_bytes: int, stream=None,
+                          check=True) -> int:
+    """layers: list of af1_factorized_linear; ys: list of outputs (tensors or
+    addresses), one per layer.  The count passed is len(layers)."""
+    arr = _layer_array(layers) if layers is not None else None
+    yarr = (ctypes.c_void_p * len(ys))(*[_addr(y) for y in ys]) if ys is not None else None
+    st = lib().af1_linear_gemv_multi(arr, len(layers) if layers is not None else 0, _addr(x), b,
+                                     yarr, _addr(ws), ws_bytes, _stream(stream))
+    if check:
+        _check(st, "af1_linear_gemv_multi")
     return st
 
 

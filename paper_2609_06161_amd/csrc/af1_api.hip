@@ -109,6 +109,61 @@ af1_status af1_linear_gemv(const af1_factorized_linear *L, const uint16_t *x, in
                                      L->s_in, x, b, y, ws, as_stream(stream)));
 }
 
+size_t af1_gemv_multi_workspace_bytes(const af1_factorized_linear *Ls, int32_t count,
+                                      int64_t b) {
+  if (!Ls || count < 1 || count > AF1_GEMV_MULTI_MAX || b < 1 || b > AF1_GEMV_MAX_BATCH) return 0;
+  int64_t m[AF1_GEMV_MULTI_MAX], r[AF1_GEMV_MULTI_MAX];
+  for (int i = 0; i < count; ++i) {
+    if (!dim_ok(Ls[i].m) || !dim_ok(Ls[i].n) || !dim_ok(Ls[i].r) || Ls[i].n != Ls[0].n) return 0;
+    m[i] = Ls[i].m;
+    r[i] = Ls[i].r;
+  }
+  return af1::gemv_multi_workspace_bytes(m, r, count, Ls[0].n, b);
+}
+
+af1_status af1_linear_gemv_multi(const af1_factorized_linear *Ls, int32_t count,
+                                 const uint16_t *x, int64_t b, uint16_t *const *ys, void *ws,
+                                 size_t ws_bytes, void *stream) {
+  if (!Ls || !ys) return AF1_ERR_NULL;
+  if (count < 1 || count > AF1_GEMV_MULTI_MAX) return AF1_ERR_SHAPE;
+  for (int i = 0; i < count; ++i)
+    if (dim_ok(Ls[i].n) && dim_ok(Ls[0].n) && Ls[i].n != Ls[0].n) return AF1_ERR_SHAPE;
+  const size_t need = af1_gemv_multi_workspace_bytes(Ls, count, b);
+  for (int i = 0; i < count; ++i) {
+    if (!ys[i]) return AF1_ERR_NULL;
+    const af1_status st = check_forward(&Ls[i], x, b, AF1_GEMV_MAX_BATCH, ys[i], ws, ws_bytes, need);
+    if (st != AF1_OK) return st;
+  }
+  // outputs against every other layer's arrays and against each other
+  for (int i = 0; i < count; ++i) {
+    const Span yi = span(ys[i], (uint64_t)b * Ls[i].m * 2);
+    for (int j = 0; j < count; ++j) {
+      const af1_factorized_linear &Lj = Ls[j];
+      const Span arrays[] = {span(Lj.Bu, (uint64_t)Lj.m * Lj.r / 8),
+                             span(Lj.Bv, (uint64_t)Lj.r * Lj.n / 8),
+                             span(Lj.s_out, (uint64_t)Lj.m * 2), span(Lj.s_mid, (uint64_t)Lj.r * 2),
+                             span(Lj.s_in, (uint64_t)Lj.n * 2)};
+      for (const Span &a : arrays)
+        if (overlap(yi, a)) return AF1_ERR_ALIAS;
+      if (j != i && overlap(yi, span(ys[j], (uint64_t)b * Lj.m * 2))) return AF1_ERR_ALIAS;
+    }
+  }
+  int64_t m[AF1_GEMV_MULTI_MAX], r[AF1_GEMV_MULTI_MAX];
+  const uint32_t *Bu[AF1_GEMV_MULTI_MAX], *Bv[AF1_GEMV_MULTI_MAX];
+  const uint16_t *so[AF1_GEMV_MULTI_MAX], *sm[AF1_GEMV_MULTI_MAX], *si[AF1_GEMV_MULTI_MAX];
+  for (int i = 0; i < count; ++i) {
+    m[i] = Ls[i].m;
+    r[i] = Ls[i].r;
+    Bu[i] = Ls[i].Bu;
+    Bv[i] = Ls[i].Bv;
+    so[i] = Ls[i].s_out;
+    sm[i] = Ls[i].s_mid;
+    si[i] = Ls[i].s_in;
+  }
+  return hip_status(af1::launch_gemv_multi(count, m, r, Ls[0].n, Bu, Bv, so, sm, si, x, b, ys, ws,
+                                           as_stream(stream)));
+}
+
 size_t af1_gemm_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
   if (!dim_ok(m) || !dim_ok(n) || !dim_ok(r) || T < 1 || T > AF1_GEMM_MAX_TOKENS) return 0;
   return af1::gemm_workspace_bytes(m, n, r, T);

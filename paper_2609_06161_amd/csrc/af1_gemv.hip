@@ -214,13 +214,14 @@ struct Role {
   int my_groups;
 };
 
-__device__ __forceinline__ Role make_role(int wave, int rt_log2, int wpr, int slab_words) {
+__device__ __forceinline__ Role make_role(int wave, int group, int rt_log2, int wpr,
+                                         int slab_words) {
   Role r;
   r.rt_log2 = rt_log2;
   r.wpt = kWaves >> rt_log2;
   r.rt = wave >> (3 - rt_log2);
   r.cw = wave & (r.wpt - 1);
-  r.tile = ((int)blockIdx.x << rt_log2) + r.rt;
+  r.tile = (group << rt_log2) + r.rt;
   r.row0 = r.tile * kTileRows;
   r.w_begin = (int)blockIdx.y * slab_words;
   r.w_count = min(slab_words, wpr - r.w_begin);
@@ -242,17 +243,17 @@ __device__ __forceinline__ Role make_role(int wave, int rt_log2, int wpr, int sl
 // kMulti: several row tiles per workgroup (rt_log2 > 0, staging shared by
 // the workgroup); otherwise one tile, and rt_log2 is ignored.
 template <bool kInX, bool kOutY, bool kHiLoCols, bool kMulti>
-__global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
+__device__ __forceinline__ void stage_body(
     const uint32_t *__restrict__ M, const void *__restrict__ in,
     const uint16_t *__restrict__ s_in, const uint16_t *__restrict__ row_scale, int rows,
     int wpr, int slab_words, int b, int rt_log2_arg, int nslabs, int mode, int in_parts,
-    void *__restrict__ out, float *__restrict__ part, uint32_t *__restrict__ cnt) {
+    void *__restrict__ out, float *__restrict__ part, uint32_t *__restrict__ cnt, int group) {
   const int rt_log2 = kMulti ? rt_log2_arg : 0;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // scalar: wave-uniform
-  const Role R = make_role(wave, rt_log2, wpr, slab_words);
+  const Role R = make_role(wave, group, rt_log2, wpr, slab_words);
   const size_t K = (size_t)wpr * 32;
   const int w_begin = R.w_begin;
   const int w_count = R.w_count;
@@ -373,7 +374,7 @@ __global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
   // workgroup's rows, batch row o / rows_per_wg.
   const int rows_log2 = 4 + rt_log2;
   const int rows_wg = 1 << rows_log2;
-  const int row_wg0 = (int)blockIdx.x * rows_wg;
+  const int row_wg0 = group * rows_wg;
   const int nout = rows_wg * b;
   // uniform, <= kMaxOutPerThread (one tile: 16 b <= 256 outputs)
   const int nk_out = kMulti ? (nout + kThreads - 1) / kThreads : 1;
@@ -504,7 +505,7 @@ __global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
     __syncthreads();
     __shared__ uint32_t s_last;
     if (tid == 0)
-      s_last = __hip_atomic_fetch_add(&cnt[blockIdx.x], 1u, __ATOMIC_RELAXED,
+      s_last = __hip_atomic_fetch_add(&cnt[group], 1u, __ATOMIC_RELAXED,
                                       __HIP_MEMORY_SCOPE_AGENT) == (uint32_t)(nslabs - 1);
     __syncthreads();
     if (!s_last) return;
@@ -533,7 +534,7 @@ __global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
       }
       sum[k] = acc_s;
     }
-    if (tid == 0) __hip_atomic_store(&cnt[blockIdx.x], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (tid == 0) __hip_atomic_store(&cnt[group], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 #pragma unroll
   for (int k = 0; k < kMaxOutPerThread; ++k) {
@@ -550,6 +551,53 @@ __global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
         static_cast<float *>(out)[oi] = v;
     }
   }
+}
+
+// One stage of one layer: row group (blockIdx.x), slab (blockIdx.y).
+// Arguments are scalars, most urgent first, so that they are preloaded into
+// SGPRs at wave launch instead of being fetched from the kernarg segment.
+template <bool kInX, bool kOutY, bool kHiLoCols, bool kMulti>
+__global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
+    const uint32_t *__restrict__ M, const void *__restrict__ in,
+    const uint16_t *__restrict__ s_in, const uint16_t *__restrict__ row_scale, int rows,
+    int wpr, int slab_words, int b, int rt_log2, int nslabs, int mode, int in_parts,
+    void *__restrict__ out, float *__restrict__ part, uint32_t *__restrict__ cnt) {
+  stage_body<kInX, kOutY, kHiLoCols, kMulti>(M, in, s_in, row_scale, rows, wpr, slab_words, b,
+                                             rt_log2, nslabs, mode, in_parts, out, part, cnt,
+                                             (int)blockIdx.x);
+}
+
+// One stage of several layers that share the input width (the segments):
+// the row groups of segment s are blockIdx.x in [group_end[s-1],
+// group_end[s]).  Each layer keeps its own sign matrix, scales, input and
+// output; the plan (rows per workgroup, slab, mode) is common, with one
+// slab (no last-slab reduction).
+constexpr int kMaxSegs = 4;
+struct Segs {
+  int count;
+  int group_end[kMaxSegs];
+  int rows[kMaxSegs];
+  int wpr[kMaxSegs];
+  const uint32_t *M[kMaxSegs];
+  const void *in[kMaxSegs];
+  const uint16_t *s_in[kMaxSegs];
+  const uint16_t *row_scale[kMaxSegs];
+  void *out[kMaxSegs];
+};
+
+template <bool kInX, bool kOutY, bool kHiLoCols, bool kMulti>
+__global__ __launch_bounds__(kThreads) void gemv_segs_kernel(const Segs segs, int slab_words,
+                                                             int b, int rt_log2, int mode,
+                                                             int in_parts) {
+  const int g = (int)blockIdx.x;
+  int sg = 0;
+#pragma unroll
+  for (int i = 0; i + 1 < kMaxSegs; ++i)
+    if (i + 1 < segs.count && g >= segs.group_end[i]) sg = i + 1;
+  const int g0 = sg > 0 ? segs.group_end[sg - 1] : 0;
+  stage_body<kInX, kOutY, kHiLoCols, kMulti>(
+      segs.M[sg], segs.in[sg], segs.s_in[sg], segs.row_scale[sg], segs.rows[sg], segs.wpr[sg],
+      slab_words, b, rt_log2, 1, mode, in_parts, segs.out[sg], nullptr, nullptr, g - g0);
 }
 
 size_t lds_bytes_for(int64_t b, int slab_words) {
@@ -691,6 +739,66 @@ hipError_t launch_stage(const StageArgs &a, const StagePlan &p, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <bool kInX, bool kOutY>
+hipError_t launch_segs(const Segs &sg, const StagePlan &p, int b, int max_wpr, int in_parts,
+                       hipStream_t s) {
+  const size_t lds = lds_bytes_for(b, p.slab_words < max_wpr ? p.slab_words : max_wpr);
+  dim3 grid((unsigned)sg.group_end[sg.count - 1], (unsigned)p.nslabs);
+  auto go = [&](auto kernel) {
+    kernel<<<grid, kThreads, lds, s>>>(sg, p.slab_words, b, p.rt_log2, p.mode, in_parts);
+  };
+  const bool multi = p.rt_log2 > 0;
+  if (b <= 8) {
+    if (multi)
+      go(gemv_segs_kernel<kInX, kOutY, true, true>);
+    else
+      go(gemv_segs_kernel<kInX, kOutY, true, false>);
+  } else {
+    if (multi)
+      go(gemv_segs_kernel<kInX, kOutY, false, true>);
+    else
+      go(gemv_segs_kernel<kInX, kOutY, false, false>);
+  }
+  return hipGetLastError();
+}
+
+// Several layers sharing n in two launches: the stage plans are made for
+// the summed rows (stage 2 for the widest rank), and apply when neither
+// stage needs a last-slab reduction.
+struct MultiLayout {
+  StagePlan p1, p2;
+  bool fused;
+  size_t t[kMaxSegs];
+  size_t total;
+};
+
+MultiLayout multi_layout(const int64_t *m, const int64_t *r, int count, int64_t n, int64_t b,
+                         int cus) {
+  MultiLayout L{};
+  int64_t rows1 = 0, rows2 = 0, wpr2 = 0;
+  for (int i = 0; i < count; ++i) {
+    rows1 += r[i];
+    rows2 += m[i];
+    if (r[i] / 32 > wpr2) wpr2 = r[i] / 32;
+  }
+  L.p1 = plan_stage(rows1, n / 32, b, true, cus);
+  L.p2 = plan_stage(rows2, wpr2, b, false, cus);
+  L.fused = L.p1.mode != kModeLastSlab && L.p2.mode == kModeFinal;
+  const int tparts = L.p1.mode == kModePartial ? L.p1.nslabs : 1;
+  size_t off = kHeaderBytes;
+  for (int i = 0; i < count; ++i) {
+    L.t[i] = off;
+    off += align256((size_t)tparts * b * r[i] * 4);
+  }
+  L.total = off;
+  // the per-layer fallback reuses the workspace one layer at a time
+  for (int i = 0; i < count; ++i) {
+    const size_t one = ws_layout(m[i], n, r[i], b, cus).total;
+    if (one > L.total) L.total = one;
+  }
+  return L;
+}
+
 }  // namespace
 
 // Compute units of the current device, queried once per device.
@@ -712,6 +820,59 @@ int device_cus() {
 
 size_t gemv_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t b) {
   return ws_layout(m, n, r, b, device_cus()).total;
+}
+
+size_t gemv_multi_workspace_bytes(const int64_t *m, const int64_t *r, int count, int64_t n,
+                                  int64_t b) {
+  return multi_layout(m, r, count, n, b, device_cus()).total;
+}
+
+hipError_t launch_gemv_multi(int count, const int64_t *m, const int64_t *r, int64_t n,
+                             const uint32_t *const *Bu, const uint32_t *const *Bv,
+                             const uint16_t *const *s_out, const uint16_t *const *s_mid,
+                             const uint16_t *const *s_in, const uint16_t *x, int64_t b,
+                             uint16_t *const *y, void *ws, hipStream_t s) {
+  if (count < 1 || count > kMaxSegs) return hipErrorInvalidValue;
+  const MultiLayout L = multi_layout(m, r, count, n, b, device_cus());
+  if (!L.fused) {
+    for (int i = 0; i < count; ++i) {
+      const hipError_t e =
+          launch_gemv(m[i], n, r[i], Bu[i], Bv[i], s_out[i], s_mid[i], s_in[i], x, b, y[i], ws, s);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
+  uint8_t *base = static_cast<uint8_t *>(ws);
+  const int tparts = L.p1.mode == kModePartial ? L.p1.nslabs : 1;
+  Segs s1{}, s2{};
+  s1.count = s2.count = count;
+  const int rw1 = kTileRows << L.p1.rt_log2, rw2 = kTileRows << L.p2.rt_log2;
+  int g1 = 0, g2 = 0, wpr2 = 0;
+  for (int i = 0; i < count; ++i) {
+    float *t = reinterpret_cast<float *>(base + L.t[i]);
+    g1 += (int)((r[i] + rw1 - 1) / rw1);
+    g2 += (int)((m[i] + rw2 - 1) / rw2);
+    s1.group_end[i] = g1;
+    s2.group_end[i] = g2;
+    s1.rows[i] = (int)r[i];
+    s1.wpr[i] = (int)(n / 32);
+    s1.M[i] = Bv[i];
+    s1.in[i] = x;
+    s1.s_in[i] = s_in[i];
+    s1.row_scale[i] = s_mid[i];
+    s1.out[i] = t;
+    s2.rows[i] = (int)m[i];
+    s2.wpr[i] = (int)(r[i] / 32);
+    s2.M[i] = Bu[i];
+    s2.in[i] = t;
+    s2.s_in[i] = nullptr;
+    s2.row_scale[i] = s_out[i];
+    s2.out[i] = y[i];
+    if (s2.wpr[i] > wpr2) wpr2 = s2.wpr[i];
+  }
+  hipError_t e = launch_segs<true, false>(s1, L.p1, (int)b, (int)(n / 32), 1, s);
+  if (e != hipSuccess) return e;
+  return launch_segs<false, true>(s2, L.p2, (int)b, wpr2, tparts, s);
 }
 
 hipError_t launch_gemv(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,

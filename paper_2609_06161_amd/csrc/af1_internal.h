@@ -24,6 +24,16 @@ hipError_t launch_gemv(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
                        const uint16_t *x, int64_t b, uint16_t *y, void *ws,
                        hipStream_t s);
 
+// Several layers that share n (count <= 4): two launches for all of them
+// when the plan allows, else one call per layer on the same workspace.
+size_t gemv_multi_workspace_bytes(const int64_t *m, const int64_t *r, int count, int64_t n,
+                                  int64_t b);
+hipError_t launch_gemv_multi(int count, const int64_t *m, const int64_t *r, int64_t n,
+                             const uint32_t *const *Bu, const uint32_t *const *Bv,
+                             const uint16_t *const *s_out, const uint16_t *const *s_mid,
+                             const uint16_t *const *s_in, const uint16_t *x, int64_t b,
+                             uint16_t *const *y, void *ws, hipStream_t s);
+
 size_t gemm_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T);
 hipError_t launch_gemm(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
                        const uint32_t *Bv, const uint16_t *s_out,

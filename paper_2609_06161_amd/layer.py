@@ -62,3 +62,16 @@ class DeviceLayer:
             ws = torch.empty(max(need, 256), dtype=torch.uint8, device=x.device)
         af1.af1_linear_gemm(self.desc, x, T, y, ws, ws.numel(), stream)
         return y
+
+
+def gemv_multi(layers, x: torch.Tensor, ys=None, ws: torch.Tensor = None, stream=None):
+    """One decode step of several layers that read the same x (same n)."""
+    b = x.shape[0]
+    if ys is None:
+        ys = [torch.empty((b, L.m), dtype=torch.int16, device=x.device) for L in layers]
+    descs = [L.desc for L in layers]
+    need = af1.af1_gemv_multi_workspace_bytes(descs, b)
+    if ws is None:
+        ws = torch.zeros(max(need, 256), dtype=torch.uint8, device=x.device)
+    af1.af1_linear_gemv_multi(descs, x, b, ys, ws, ws.numel(), stream)
+    return ys

@@ -143,6 +143,29 @@ def test_gemm_rejects_operands_beyond_32bit_offsets():
     assert gemm(fake_layer(4096, big, big), T=1) == af1.AF1_ERR_SHAPE
 
 
+def test_gemv_multi_validation():
+    M = af1.af1_linear_gemv_multi
+    q = fake_layer(4096, 4096, 2016)
+    k = fake_layer(1024, 4096, 800, base=BASE + 512 * MB)
+    v = fake_layer(1024, 4096, 800, base=BASE + 1024 * MB)
+    ys = [Y, Y + 16 * MB, Y + 32 * MB]
+    call = lambda layers, ys, **kw: M(layers, kw.get("x", X), kw.get("b", 1), ys, WS,
+                                      kw.get("ws_bytes", 1 << 30), stream=0, check=False)
+    assert call([q, k, v], None) == af1.AF1_ERR_NULL
+    assert call([q, k, v], [Y, None, Y + 32 * MB]) == af1.AF1_ERR_NULL
+    assert call([q, k, fake_layer(1024, 2048, 800, base=BASE + 1024 * MB)], ys) == af1.AF1_ERR_SHAPE
+    assert call([q, k, v, q, k], ys + [Y + 48 * MB, Y + 64 * MB]) == af1.AF1_ERR_SHAPE
+    assert call([q, k, v], ys, b=17) == af1.AF1_ERR_BATCH
+    assert call([q, k, v], ys, ws_bytes=1024) == af1.AF1_ERR_WORKSPACE
+    # two outputs overlapping each other, and an output over another layer's signs
+    assert call([q, k, v], [Y, Y + 4096, Y + 32 * MB]) == af1.AF1_ERR_ALIAS
+    assert call([q, k, v], [Y, Y + 16 * MB, BASE + 512 * MB]) == af1.AF1_ERR_ALIAS
+    need = af1.af1_gemv_multi_workspace_bytes([q, k, v], 1)
+    assert need >= af1.af1_gemv_workspace_bytes(4096, 4096, 2016, 1)
+    assert af1.af1_gemv_multi_workspace_bytes([q, k, v], 0) == 0
+    assert af1.af1_gemv_multi_workspace_bytes([], 1) == 0
+
+
 def test_pack_validation():
     P = af1.af1_pack
     assert P(None, 0, 4, 64, Y, stream=0, check=False) == af1.AF1_ERR_NULL

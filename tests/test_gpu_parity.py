@@ -9,7 +9,7 @@ import pytest
 import torch
 
 from paper_2609_06161_amd import af1, synth
-from paper_2609_06161_amd.layer import DeviceLayer, bf16_bits_to_f64, to_device
+from paper_2609_06161_amd.layer import DeviceLayer, bf16_bits_to_f64, gemv_multi, to_device
 
 pytestmark = pytest.mark.gpu
 
@@ -282,6 +282,55 @@ def test_gemm_max_tokens(oracle):
     idx = np.sort(np.random.default_rng(1).choice(T, 64, replace=False))
     idx[-1] = T - 1
     assert max_row_rel_l2(y[idx], oracle_y(oracle, lin, lin.x[idx])) <= TOL
+
+
+QKV = [(4096, 4096, 2016), (1024, 4096, 800), (1024, 4096, 800)]
+GATE_UP = [(14336, 4096, 3136), (14336, 4096, 3136)]
+
+
+@pytest.mark.parametrize("shapes,b", [(QKV, 1), (QKV, 4), (QKV, 8), (GATE_UP, 1),
+                                      (GATE_UP, 16), (QKV[:1], 1),
+                                      ([(96, 2080, 160), (544, 2080, 96), (1056, 2080, 4064),
+                                        (32, 2080, 32)], 3)])
+def test_gemv_multi_matches_oracle(oracle, shapes, b):
+    """Several layers reading one x in one call (two launches for q/k/v and
+    gate/up; at b=16 gate/up need last-slab reductions and run one after
+    the other): every output element against the oracle, outputs prefilled
+    with NaN."""
+    x = synth.make_activations(33 + b, b, shapes[0][1])
+    lins = [synth.make_linear(600 + i, m, n, r, b) for i, (m, n, r) in enumerate(shapes)]
+    for lin in lins:
+        lin.x = x
+    print(f"multi {[s[:3] for s in shapes]} b={b}", flush=True)
+    layers = [DeviceLayer.from_host(lin) for lin in lins]
+    ys = [torch.full((b, L.m), 0x7FC0, dtype=torch.int16, device="cuda") for L in layers]
+    gemv_multi(layers, to_device(x), ys=ys)
+    torch.cuda.synchronize()
+    for lin, y in zip(lins, ys):
+        ok, where = elementwise_ok(bf16_bits_to_f64(y), oracle_y(oracle, lin))
+        assert ok, (lin.m, lin.n, lin.r, where)
+
+
+def test_gemv_multi_workspace_reuse_with_single_calls(oracle):
+    """One workspace serving multi calls and single-layer calls in turn."""
+    b = 2
+    x = synth.make_activations(70, b, 4096)
+    lins = [synth.make_linear(700 + i, m, n, r, b) for i, (m, n, r) in enumerate(QKV)]
+    for lin in lins:
+        lin.x = x
+    layers = [DeviceLayer.from_host(lin) for lin in lins]
+    xd = to_device(x)
+    descs = [L.desc for L in layers]
+    ws = torch.zeros(af1.af1_gemv_multi_workspace_bytes(descs, b), dtype=torch.uint8,
+                     device="cuda")
+    refs = [oracle_y(oracle, lin) for lin in lins]
+    for _ in range(3):
+        ys = gemv_multi(layers, xd, ws=ws)
+        single = layers[1].gemv(xd, ws=ws)
+        torch.cuda.synchronize()
+        for y, ref in zip(ys, refs):
+            assert max_row_rel_l2(bf16_bits_to_f64(y), ref) <= TOL
+        assert max_row_rel_l2(bf16_bits_to_f64(single), refs[1]) <= TOL
 
 
 def test_gemv_deterministic():
