@@ -14,6 +14,9 @@ source, the passage of the paper it follows:
 - ``storage_bits`` / ``bpw``: the deployable-storage count of App. A.3.
 - ``budget_rank``: the largest rank (multiple of 32) within 1.0 BPW.
 - ``paper_rank``: the budget-to-rank rounding rule of App. A.1.3.
+- ``transpose_packed``: the packed storage of a sign matrix's transpose.
+- ``backward``: the gradients of the scale-only reconstruction of Sec. 4.1
+  (sign matrices frozen) with respect to s_out, s_mid, s_in and x.
 """
 import ctypes
 import os
@@ -46,6 +49,9 @@ def _load():
     lib.oracle_pack.argtypes = [P, ctypes.c_int, I64, I64, P]
     lib.oracle_unpack.argtypes = [P, I64, I64, P]
     lib.oracle_forward.argtypes = [I64, I64, I64, P, P, P, P, P, P, I64, P]
+    lib.oracle_transpose_packed.argtypes = [P, I64, I64, P]
+    lib.oracle_backward.argtypes = [I64, I64, I64, P, P, P, P, P, P, P, I64,
+                                    P, P, P, P]
     lib.oracle_what_dense.argtypes = [I64, I64, I64, P, P, P, P, P, P]
     lib.oracle_what_packed.argtypes = [I64, I64, I64, P, P, P, P, P, P]
     lib.oracle_storage_bits.argtypes = [I64, I64, I64]
@@ -122,6 +128,37 @@ def forward(m, n, r, Bu, Bv, s_out, s_mid, s_in, x) -> np.ndarray:
                                   _ptr(s_mid), _ptr(s_in), _ptr(x), b, _ptr(y)),
            "forward")
     return y
+
+
+def transpose_packed(words: np.ndarray, cols: int) -> np.ndarray:
+    """Packed cols x rows storage of the transpose of a packed rows x cols
+    sign matrix."""
+    words = _c(words, np.uint32)
+    rows = words.shape[0]
+    out = np.empty((cols, rows // 32), dtype=np.uint32)
+    _check(_load().oracle_transpose_packed(_ptr(words), rows, cols, _ptr(out)),
+           "transpose_packed")
+    return out
+
+
+def backward(m, n, r, Bu, Bv, s_out, s_mid, s_in, x, dy):
+    """fp64 (dx[b, n], ds_out[m], ds_mid[r], ds_in[n]) for the upstream
+    gradient dy[b, m] (bfloat16 patterns), sign matrices frozen."""
+    Bu = _c(Bu, np.uint32); Bv = _c(Bv, np.uint32)
+    s_out = _c(s_out, np.uint16); s_mid = _c(s_mid, np.uint16)
+    s_in = _c(s_in, np.uint16); x = _c(x, np.uint16); dy = _c(dy, np.uint16)
+    b = x.shape[0]
+    if dy.shape != (b, m) or x.shape != (b, n):
+        raise ValueError("x must be b x n and dy b x m")
+    dx = np.empty((b, n), dtype=np.float64)
+    ds_out = np.empty(m, dtype=np.float64)
+    ds_mid = np.empty(r, dtype=np.float64)
+    ds_in = np.empty(n, dtype=np.float64)
+    _check(_load().oracle_backward(m, n, r, _ptr(Bu), _ptr(Bv), _ptr(s_out),
+                                   _ptr(s_mid), _ptr(s_in), _ptr(x), _ptr(dy), b,
+                                   _ptr(dx), _ptr(ds_out), _ptr(ds_mid), _ptr(ds_in)),
+           "backward")
+    return dx, ds_out, ds_mid, ds_in
 
 
 def what_dense(A, B, a, lam, bvec) -> np.ndarray:

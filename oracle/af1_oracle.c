@@ -28,6 +28,12 @@
  *   - cols must be a multiple of 32 (no padding bits exist);
  *   - scales are IEEE binary16 bit patterns, activations bfloat16 patterns.
  *
+ * It also computes the gradients of the scale-only reconstruction (Sec. 4.1,
+ * labels eq:final_reconstruction and eq:scale_only_kl): with the two sign
+ * matrices frozen, the vector-Jacobian product of the layer with respect to
+ * s_out, s_mid, s_in and x, and the bit transpose of the packed storage that
+ * the transposed products use.
+ *
  * Arithmetic: every value is widened exactly to double and every product and
  * sum is taken in double, in the factorised order written above.  The entry
  * -wise path sum of App. A.2.1 (label eq:binary_paths) is provided as an
@@ -39,7 +45,13 @@
  * layer, the Sylvester-Hadamard identity H*H = n*I, one-hot probes against
  * the brute-force matrix, single-bit-flip deltas, sign-gauge invariance,
  * linearity, the storage-bit count of App. A.3 against hand-computed
- * integers, and the half-precision widenings against numpy's own.
+ * integers, and the half-precision widenings against numpy's own.  The
+ * gradients are pinned by one-hot probes of the brute-force path sum (the
+ * layer is linear in each scale vector and in x, so a one-hot scale vector
+ * gives one gradient entry exactly), by dx against dy times the brute-force
+ * matrix, by the four homogeneity identities sum(s .* ds) = sum(dy .* y),
+ * and by dx against the forward of the transposed layer.  The transpose is
+ * pinned against numpy's unpackbits/packbits and a single-bit probe.
  */
 #include <math.h>
 #include <stddef.h>
@@ -217,6 +229,150 @@ int oracle_forward(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
         }
     }
     free(U); free(V); free(u); free(t);
+    return OR_OK;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Transposed sign storage (for the products with B_u^T and B_v^T).        */
+/* ---------------------------------------------------------------------- */
+
+/*
+ * dst is the cols x rows sign matrix whose entry (j, i) is the sign of
+ * src(i, j), in the same packed format.  Both dimensions must be multiples
+ * of 32 so that source and destination rows are whole words.  Written bit
+ * by bit from the format definition above.
+ */
+int oracle_transpose_packed(const uint32_t *src, int64_t rows, int64_t cols,
+                            uint32_t *dst)
+{
+    if (!src || !dst || rows < 0 || cols < 0 || rows % 32 || cols % 32)
+        return OR_ERR_ARG;
+    int64_t swords = cols / 32, dwords = rows / 32;
+    for (int64_t j = 0; j < cols; ++j)
+        for (int64_t w = 0; w < dwords; ++w) {
+            uint32_t word = 0;
+            for (int bit = 0; bit < 32; ++bit) {
+                int64_t i = 32 * w + bit;
+                uint32_t s = (src[i * swords + j / 32] >> (j % 32)) & 1u;
+                word |= s << bit;
+            }
+            dst[j * dwords + w] = word;
+        }
+    return OR_OK;
+}
+
+/* ---------------------------------------------------------------------- */
+/* Scale-only reconstruction: gradients with the sign matrices frozen      */
+/* (Sec. 4.1, paragraph on scale-only global reconstruction, labels        */
+/* eq:final_reconstruction and eq:scale_only_kl).                          */
+/* ---------------------------------------------------------------------- */
+
+/*
+ * The paper trains only the three scale vectors (a, m, b here s_out, s_mid,
+ * s_in) after freezing A_pm1 and B_pm1, through the unchanged factorised
+ * graph.  For an upstream gradient dy of one linear's output this is the
+ * chain rule through the four steps of the forward, per token beta:
+ *
+ *   forward   u = s_in .* x,  v = Bv u,  t = s_mid .* v,  z = Bu t,
+ *             y = s_out .* z
+ *   backward  dz = s_out .* dy          ds_out += dy .* z
+ *             dt = Bu^T dz              ds_mid += dt .* v
+ *             dv = s_mid .* dt
+ *             du = Bv^T dv              ds_in  += du .* x
+ *             dx = s_in .* du
+ *
+ * The scale gradients are summed over the b tokens.  Bu: m x r packed,
+ * Bv: r x n packed (the forward factors themselves; the transposed products
+ * read them column-wise), s_*: binary16 patterns, x: b x n and dy: b x m
+ * bfloat16 patterns.  Outputs (caller-allocated doubles, overwritten):
+ * dx b x n, ds_out m, ds_mid r, ds_in n.
+ */
+int oracle_backward(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
+                    const uint32_t *Bv, const uint16_t *s_out,
+                    const uint16_t *s_mid, const uint16_t *s_in,
+                    const uint16_t *x, const uint16_t *dy, int64_t b,
+                    double *dx, double *ds_out, double *ds_mid, double *ds_in)
+{
+    if (m <= 0 || n <= 0 || r <= 0 || b < 0 || m % 32 || n % 32 || r % 32 ||
+        !Bu || !Bv || !s_out || !s_mid || !s_in || !ds_out || !ds_mid ||
+        !ds_in || (b > 0 && (!x || !dy || !dx)))
+        return OR_ERR_ARG;
+    for (int64_t i = 0; i < m; ++i) ds_out[i] = 0.0;
+    for (int64_t k = 0; k < r; ++k) ds_mid[k] = 0.0;
+    for (int64_t j = 0; j < n; ++j) ds_in[j] = 0.0;
+    if (b == 0)
+        return OR_OK;
+
+    int8_t *U = (int8_t *)malloc((size_t)(m * r));
+    int8_t *V = (int8_t *)malloc((size_t)(r * n));
+    double *u = (double *)malloc(sizeof(double) * (size_t)n);
+    double *v = (double *)malloc(sizeof(double) * (size_t)r);
+    double *t = (double *)malloc(sizeof(double) * (size_t)r);
+    double *z = (double *)malloc(sizeof(double) * (size_t)m);
+    double *dz = (double *)malloc(sizeof(double) * (size_t)m);
+    double *dt = (double *)malloc(sizeof(double) * (size_t)r);
+    double *dv = (double *)malloc(sizeof(double) * (size_t)r);
+    if (!U || !V || !u || !v || !t || !z || !dz || !dt || !dv) {
+        free(U); free(V); free(u); free(v); free(t); free(z); free(dz);
+        free(dt); free(dv);
+        return OR_ERR_NOMEM;
+    }
+    oracle_unpack(Bu, m, r, U);
+    oracle_unpack(Bv, r, n, V);
+
+    for (int64_t beta = 0; beta < b; ++beta) {
+        const uint16_t *xb = x + beta * n;
+        const uint16_t *dyb = dy + beta * m;
+        double *dxb = dx + beta * n;
+        /* forward intermediates of this token */
+        for (int64_t j = 0; j < n; ++j)
+            u[j] = oracle_f16_to_f64(s_in[j]) * oracle_bf16_to_f64(xb[j]);
+#pragma omp parallel for schedule(static)
+        for (int64_t k = 0; k < r; ++k) {
+            double acc = 0.0;
+            for (int64_t j = 0; j < n; ++j)
+                acc += (double)V[k * n + j] * u[j];
+            v[k] = acc;
+            t[k] = oracle_f16_to_f64(s_mid[k]) * acc;
+        }
+#pragma omp parallel for schedule(static)
+        for (int64_t i = 0; i < m; ++i) {
+            double acc = 0.0;
+            for (int64_t k = 0; k < r; ++k)
+                acc += (double)U[i * r + k] * t[k];
+            z[i] = acc;
+        }
+        /* output scale: its gradient and the gradient entering Bu */
+        for (int64_t i = 0; i < m; ++i) {
+            double g = oracle_bf16_to_f64(dyb[i]);
+            ds_out[i] += g * z[i];
+            dz[i] = oracle_f16_to_f64(s_out[i]) * g;
+        }
+        /* dt = Bu^T dz: column k of Bu against dz */
+#pragma omp parallel for schedule(static)
+        for (int64_t k = 0; k < r; ++k) {
+            double acc = 0.0;
+            for (int64_t i = 0; i < m; ++i)
+                acc += (double)U[i * r + k] * dz[i];
+            dt[k] = acc;
+        }
+        /* middle scale */
+        for (int64_t k = 0; k < r; ++k) {
+            ds_mid[k] += dt[k] * v[k];
+            dv[k] = oracle_f16_to_f64(s_mid[k]) * dt[k];
+        }
+        /* du = Bv^T dv: column j of Bv against dv; then the input scale */
+#pragma omp parallel for schedule(static)
+        for (int64_t j = 0; j < n; ++j) {
+            double acc = 0.0;
+            for (int64_t k = 0; k < r; ++k)
+                acc += (double)V[k * n + j] * dv[k];
+            dxb[j] = oracle_f16_to_f64(s_in[j]) * acc;
+            ds_in[j] += acc * oracle_bf16_to_f64(xb[j]);
+        }
+    }
+    free(U); free(V); free(u); free(v); free(t); free(z); free(dz);
+    free(dt); free(dv);
     return OR_OK;
 }
 

@@ -16,6 +16,9 @@ trained weights and calibration data are not available):
      outliers are off).
   4. x: float32 N(0, 1) of shape [batch, n]; outlier channels scaled by 20 in
      float32; the whole tensor rounded once, RNE, to bfloat16.
+  5. For the scale-only reconstruction (gradients with the signs frozen):
+     the upstream gradient dy, float32 N(0, 1) times 2^-10 of shape
+     [batch, m] (from its own seed), rounded once, RNE, to bfloat16.
 """
 from dataclasses import dataclass
 
@@ -108,6 +111,15 @@ def make_activations(seed: int, batch: int, n: int, outliers: bool = True) -> np
     k = int(round(0.01 * n)) if outliers else 0
     idx = np.sort(rng.choice(n, size=k, replace=False)) if k else None
     return activations_bf16(rng, batch, n, idx)
+
+
+def make_output_grad(seed: int, batch: int, m: int, scale: float = 2.0 ** -10) -> np.ndarray:
+    """Upstream gradient of one linear's output for the scale-only
+    reconstruction: float32 N(0, 1) times `scale` (a power of two, so the
+    scaling is exact), shape [batch, m], rounded once, RNE, to bfloat16."""
+    rng = np.random.default_rng(seed)
+    g = rng.standard_normal(size=(batch, m), dtype=np.float32) * np.float32(scale)
+    return f32_to_bf16_bits(g)
 
 
 def random_sign_source(seed: int, rows: int, cols: int, dtype: str) -> np.ndarray:
