@@ -186,6 +186,90 @@ AF1_API af1_status af1_linear_gemm(const af1_factorized_linear *L, const uint16_
                            int64_t T, uint16_t *y, void *ws, size_t ws_bytes,
                            void *stream);
 
+/*
+ * af1_pack_transpose -- the packed storage of the transpose of a packed sign
+ * matrix: dst (cols x rows signs, cols * (rows/32) words) gets at row j,
+ * column i the sign of src row i, column j.  The scale-only reconstruction
+ * (Sec. 4.1) freezes the sign matrices, so the products with Bu^T and Bv^T
+ * that its gradients need read factors transposed once with this call.
+ *   src  : device, rows * (cols/32) uint32 words.
+ *   dst  : device, cols * (rows/32) uint32 words (written).
+ * rows and cols are multiples of 32 in [0, AF1_TRANSPOSE_MAX_DIM] with
+ * rows * cols < 2^40 (AF1_ERR_SHAPE otherwise); a zero dimension enqueues
+ * nothing.  Bit-exact.  dst must not overlap src (AF1_ERR_ALIAS).
+ */
+#define AF1_TRANSPOSE_MAX_DIM ((int64_t)1 << 24)
+AF1_API af1_status af1_pack_transpose(const uint32_t *src, int64_t rows, int64_t cols,
+                                      uint32_t *dst, void *stream);
+
+/*
+ * Scale-only reconstruction (Sec. 4.1, paragraph on scale-only global
+ * reconstruction, labels eq:final_reconstruction and eq:scale_only_kl):
+ * after factorisation the paper freezes Bu and Bv and trains only s_out,
+ * s_mid and s_in through the unchanged factorised graph.  These two calls
+ * are that graph's forward and backward for T tokens of one layer; the
+ * loss (a KL divergence to a full-precision teacher in the paper) and the
+ * optimiser stay with the caller.
+ *
+ * af1_linear_forward_train -- y as af1_linear_gemm computes it (same
+ * kernels and rounding, bit-identical y), and in `saved` the two pre-scale
+ * intermediates the gradients need: v = Bv (s_in .* x) ([T, r], fp16, in a
+ * layout private to the library) and z = Bu (s_mid .* v) ([T, m], fp32).
+ *   saved : device, at least af1_train_saved_bytes(m, n, r, T) bytes,
+ *           written; hand it unchanged to af1_linear_backward with the same
+ *           layer, x and T.
+ *   ws    : device, at least af1_train_workspace_bytes(m, n, r, T) bytes
+ *           (scratch; one buffer serves both calls).
+ *   T     : 1 .. AF1_GEMM_MAX_TOKENS and T * max(m, n, r) * 2 < 2^31, else
+ *           AF1_ERR_BATCH.
+ * Errors: as af1_linear_gemm; AF1_ERR_NULL / AF1_ERR_ALIGN for saved;
+ * AF1_ERR_WORKSPACE when saved_bytes or ws_bytes is too small;
+ * AF1_ERR_ALIAS when saved overlaps x, y, ws or the layer's arrays.
+ *
+ * af1_linear_backward -- for the upstream gradient dy of y:
+ *     dz = s_out .* dy,   dt = Bu^T dz,   du = Bv^T (s_mid .* dt)
+ *     dx = s_in .* du                                 ([T, n] bfloat16)
+ *     ds_out = sum_t dy .* z,  ds_mid = sum_t dt .* v,  ds_in = sum_t du .* x
+ * (sums over the T tokens, fp32).
+ *   L     : the layer (dims and scales; L->Bu and L->Bv are not read and
+ *           may be NULL).
+ *   BuT   : device, Bu^T (r x m signs, r * (m/32) words), from
+ *           af1_pack_transpose(L->Bu, m, r, BuT).
+ *   BvT   : device, Bv^T (n x r signs, n * (r/32) words), from
+ *           af1_pack_transpose(L->Bv, r, n, BvT).
+ *   x     : device, [T, n] bfloat16, the forward input.
+ *   dy    : device, [T, m] bfloat16.
+ *   saved : what af1_linear_forward_train wrote for this layer, x and T.
+ *   dx    : device, [T, n] bfloat16 (written), or NULL to skip it.
+ *   ds_out, ds_mid, ds_in : device fp32 arrays of m, r and n entries.
+ *           accumulate = 0 overwrites them; accumulate != 0 adds this
+ *           call's sums to their contents (gradient accumulation over
+ *           micro-batches).
+ *   ws    : device, at least af1_train_workspace_bytes(m, n, r, T) bytes.
+ * Arithmetic: both products run on bf16 MFMA with fp32 accumulation (bf16
+ * keeps the range of fp32, so small gradients do not underflow): s_out .* dy
+ * and s_mid .* dt are rounded once to bf16 and multiplied by exact +-1
+ * operands; the token sums are taken in fp32 from the fp32 accumulators,
+ * per tile and then over tiles in a fixed order, so results are
+ * deterministic (bit-identical from run to run).
+ * Errors: AF1_ERR_NULL for a NULL L, BuT, BvT, scale, x, dy, saved or ds_*;
+ * AF1_ERR_SHAPE / AF1_ERR_BATCH / AF1_ERR_ALIGN as for the forward;
+ * AF1_ERR_WORKSPACE for a short saved or ws; AF1_ERR_ALIAS when an output
+ * (dx, ds_*, ws) overlaps another output or any input.
+ */
+AF1_API size_t af1_train_saved_bytes(int64_t m, int64_t n, int64_t r, int64_t T);
+AF1_API size_t af1_train_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T);
+AF1_API af1_status af1_linear_forward_train(const af1_factorized_linear *L, const uint16_t *x,
+                                            int64_t T, uint16_t *y, void *saved,
+                                            size_t saved_bytes, void *ws, size_t ws_bytes,
+                                            void *stream);
+AF1_API af1_status af1_linear_backward(const af1_factorized_linear *L, const uint32_t *BuT,
+                                       const uint32_t *BvT, const uint16_t *x,
+                                       const uint16_t *dy, int64_t T, const void *saved,
+                                       size_t saved_bytes, uint16_t *dx, float *ds_out,
+                                       float *ds_mid, float *ds_in, int32_t accumulate,
+                                       void *ws, size_t ws_bytes, void *stream);
+
 /* Deployable storage bits of one layer: r*(m+n) + 16*(m+n+r) (App. A.3,
  * label eq:app_af1_memory).  Returns -1 for negative arguments. */
 AF1_API int64_t af1_storage_bits(int64_t m, int64_t n, int64_t r);

@@ -64,6 +64,15 @@ def lib():
     L.af1_gemm_workspace_bytes.argtypes = [I64, I64, I64, I64]
     L.af1_gemm_workspace_bytes.restype = SZ
     L.af1_linear_gemm.argtypes = [ctypes.POINTER(af1_factorized_linear), P, I64, P, P, SZ, P]
+    L.af1_pack_transpose.argtypes = [P, I64, I64, P, P]
+    L.af1_train_saved_bytes.argtypes = [I64, I64, I64, I64]
+    L.af1_train_saved_bytes.restype = SZ
+    L.af1_train_workspace_bytes.argtypes = [I64, I64, I64, I64]
+    L.af1_train_workspace_bytes.restype = SZ
+    L.af1_linear_forward_train.argtypes = [ctypes.POINTER(af1_factorized_linear), P, I64, P, P,
+                                           SZ, P, SZ, P]
+    L.af1_linear_backward.argtypes = [ctypes.POINTER(af1_factorized_linear), P, P, P, P, I64, P,
+                                      SZ, P, P, P, P, I32, P, SZ, P]
     L.af1_storage_bits.argtypes = [I64, I64, I64]
     L.af1_storage_bits.restype = I64
     L.af1_budget_rank.argtypes = [I64, I64]
@@ -72,7 +81,8 @@ def lib():
     L.af1_status_string.restype = ctypes.c_char_p
     L.af1_version.restype = ctypes.c_char_p
     for fn in ("af1_pack", "af1_unpack", "af1_linear_gemv", "af1_linear_gemv_multi",
-               "af1_linear_gemm"):
+               "af1_linear_gemm", "af1_pack_transpose", "af1_linear_forward_train",
+               "af1_linear_backward"):
         getattr(L, fn).restype = I32
     _lib = L
     return L
@@ -174,6 +184,44 @@ def af1_linear_gemm(layer, x, T: int, y, ws, ws_bytes: int, stream=None, check=T
     st = lib().af1_linear_gemm(ref, _addr(x), T, _addr(y), _addr(ws), ws_bytes, _stream(stream))
     if check:
         _check(st, "af1_linear_gemm")
+    return st
+
+
+def af1_pack_transpose(src, rows: int, cols: int, dst, stream=None, check=True) -> int:
+    st = lib().af1_pack_transpose(_addr(src), rows, cols, _addr(dst), _stream(stream))
+    if check:
+        _check(st, "af1_pack_transpose")
+    return st
+
+
+def af1_train_saved_bytes(m, n, r, T) -> int:
+    return int(lib().af1_train_saved_bytes(m, n, r, T))
+
+
+def af1_train_workspace_bytes(m, n, r, T) -> int:
+    return int(lib().af1_train_workspace_bytes(m, n, r, T))
+
+
+def af1_linear_forward_train(layer, x, T: int, y, saved, saved_bytes: int, ws, ws_bytes: int,
+                             stream=None, check=True) -> int:
+    ref = ctypes.byref(layer) if layer is not None else None
+    st = lib().af1_linear_forward_train(ref, _addr(x), T, _addr(y), _addr(saved), saved_bytes,
+                                        _addr(ws), ws_bytes, _stream(stream))
+    if check:
+        _check(st, "af1_linear_forward_train")
+    return st
+
+
+def af1_linear_backward(layer, BuT, BvT, x, dy, T: int, saved, saved_bytes: int, dx, ds_out,
+                        ds_mid, ds_in, accumulate: int, ws, ws_bytes: int, stream=None,
+                        check=True) -> int:
+    ref = ctypes.byref(layer) if layer is not None else None
+    st = lib().af1_linear_backward(ref, _addr(BuT), _addr(BvT), _addr(x), _addr(dy), T,
+                                   _addr(saved), saved_bytes, _addr(dx), _addr(ds_out),
+                                   _addr(ds_mid), _addr(ds_in), int(accumulate), _addr(ws),
+                                   ws_bytes, _stream(stream))
+    if check:
+        _check(st, "af1_linear_backward")
     return st
 
 

@@ -11,7 +11,7 @@
 
 namespace {
 
-constexpr const char *kVersion = "af1-mi355x 0.2.0 (gfx950)";
+constexpr const char *kVersion = "af1-mi355x 0.3.0 (gfx950)";
 
 bool dim_ok(int64_t d) { return d >= 32 && d <= AF1_MAX_DIM && d % 32 == 0; }
 
@@ -190,6 +190,118 @@ af1_status af1_linear_gemm(const af1_factorized_linear *L, const uint16_t *x, in
   if (st != AF1_OK) return st;
   return hip_status(af1::launch_gemm(L->m, L->n, L->r, L->Bu, L->Bv, L->s_out, L->s_mid,
                                      L->s_in, x, T, y, ws, as_stream(stream)));
+}
+
+af1_status af1_pack_transpose(const uint32_t *src, int64_t rows, int64_t cols, uint32_t *dst,
+                              void *stream) {
+  if (!src || !dst) return AF1_ERR_NULL;
+  if (rows < 0 || cols < 0 || rows % 32 != 0 || cols % 32 != 0 || rows > AF1_TRANSPOSE_MAX_DIM ||
+      cols > AF1_TRANSPOSE_MAX_DIM || (rows > 0 && cols > (((int64_t)1 << 40) / rows)))
+    return AF1_ERR_SHAPE;
+  if (!aligned16(src) || !aligned16(dst)) return AF1_ERR_ALIGN;
+  const uint64_t bytes = (uint64_t)rows * (uint64_t)cols / 8;
+  if (overlap(span(src, bytes), span(dst, bytes))) return AF1_ERR_ALIAS;
+  return hip_status(af1::launch_transpose(src, rows, cols, dst, as_stream(stream)));
+}
+
+namespace {
+
+// Token limit of the training entry points: every [T, m], [T, n] and
+// [T, r] bf16/fp16 operand is addressed with 32-bit byte offsets.
+int64_t train_max_tokens(const af1_factorized_linear *L) {
+  int64_t widest = L->m > L->n ? L->m : L->n;
+  if (L->r > widest) widest = L->r;
+  const int64_t limit = INT32_MAX / (2 * widest);
+  return limit < AF1_GEMM_MAX_TOKENS ? limit : AF1_GEMM_MAX_TOKENS;
+}
+
+bool dims_ok(const af1_factorized_linear *L) {
+  return L && dim_ok(L->m) && dim_ok(L->n) && dim_ok(L->r);
+}
+
+// Sign matrices of the layer (forward) or of its transpose (backward) below
+// 2 GiB: m*r/8 and r*n/8 bytes either way.
+bool signs_fit(const af1_factorized_linear *L) {
+  return L->m * (L->r / 32) * 4 <= INT32_MAX && L->r * (L->n / 32) * 4 <= INT32_MAX &&
+         L->r * (L->m / 32) * 4 <= INT32_MAX && L->n * (L->r / 32) * 4 <= INT32_MAX;
+}
+
+}  // namespace
+
+size_t af1_train_saved_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
+  if (!dim_ok(m) || !dim_ok(n) || !dim_ok(r) || T < 1 || T > AF1_GEMM_MAX_TOKENS) return 0;
+  return af1::train_saved_bytes(m, n, r, T);
+}
+
+size_t af1_train_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
+  if (!dim_ok(m) || !dim_ok(n) || !dim_ok(r) || T < 1 || T > AF1_GEMM_MAX_TOKENS) return 0;
+  return af1::train_workspace_bytes(m, n, r, T);
+}
+
+af1_status af1_linear_forward_train(const af1_factorized_linear *L, const uint16_t *x, int64_t T,
+                                    uint16_t *y, void *saved, size_t saved_bytes, void *ws,
+                                    size_t ws_bytes, void *stream) {
+  int64_t max_tokens = AF1_GEMM_MAX_TOKENS;
+  if (dims_ok(L)) {
+    if (!signs_fit(L)) return AF1_ERR_SHAPE;
+    max_tokens = train_max_tokens(L);
+  }
+  const bool sized = dims_ok(L) && T >= 1 && T <= max_tokens;
+  const size_t need = sized ? af1::train_workspace_bytes(L->m, L->n, L->r, T) : 0;
+  af1_status st = check_forward(L, x, T, max_tokens, y, ws, ws_bytes, need);
+  if (st != AF1_OK) return st;
+  if (!saved) return AF1_ERR_NULL;
+  if (!aligned16(saved)) return AF1_ERR_ALIGN;
+  const size_t saved_need = af1::train_saved_bytes(L->m, L->n, L->r, T);
+  if (saved_bytes < saved_need) return AF1_ERR_WORKSPACE;
+  const int64_t m = L->m, n = L->n, r = L->r;
+  const Span ss = span(saved, saved_need);
+  const Span others[] = {span(x, (uint64_t)T * n * 2), span(L->Bu, (uint64_t)m * r / 8),
+                         span(L->Bv, (uint64_t)r * n / 8), span(L->s_out, (uint64_t)m * 2),
+                         span(L->s_mid, (uint64_t)r * 2), span(L->s_in, (uint64_t)n * 2),
+                         span(y, (uint64_t)T * m * 2), span(ws, need)};
+  for (const Span &o : others)
+    if (overlap(ss, o)) return AF1_ERR_ALIAS;
+  return hip_status(af1::launch_forward_train(m, n, r, L->Bu, L->Bv, L->s_out, L->s_mid,
+                                              L->s_in, x, T, y, saved, ws, as_stream(stream)));
+}
+
+af1_status af1_linear_backward(const af1_factorized_linear *L, const uint32_t *BuT,
+                               const uint32_t *BvT, const uint16_t *x, const uint16_t *dy,
+                               int64_t T, const void *saved, size_t saved_bytes, uint16_t *dx,
+                               float *ds_out, float *ds_mid, float *ds_in, int32_t accumulate,
+                               void *ws, size_t ws_bytes, void *stream) {
+  if (!L) return AF1_ERR_NULL;
+  if (!dims_ok(L) || !signs_fit(L)) return AF1_ERR_SHAPE;
+  if (!BuT || !BvT || !L->s_out || !L->s_mid || !L->s_in || !x || !dy || !saved || !ds_out ||
+      !ds_mid || !ds_in)
+    return AF1_ERR_NULL;
+  if (T < 1 || T > train_max_tokens(L)) return AF1_ERR_BATCH;
+  if (!aligned16(BuT) || !aligned16(BvT) || !aligned16(L->s_out) || !aligned16(L->s_mid) ||
+      !aligned16(L->s_in) || !aligned16(x) || !aligned16(dy) || !aligned16(saved) ||
+      (dx && !aligned16(dx)) || !aligned16(ds_out) || !aligned16(ds_mid) || !aligned16(ds_in) ||
+      (ws && !aligned16(ws)))
+    return AF1_ERR_ALIGN;
+  const int64_t m = L->m, n = L->n, r = L->r;
+  const size_t saved_need = af1::train_saved_bytes(m, n, r, T);
+  const size_t need = af1::train_workspace_bytes(m, n, r, T);
+  if (saved_bytes < saved_need || !ws || ws_bytes < need) return AF1_ERR_WORKSPACE;
+  const Span outs[] = {span(dx, dx ? (uint64_t)T * n * 2 : 0), span(ds_out, (uint64_t)m * 4),
+                       span(ds_mid, (uint64_t)r * 4), span(ds_in, (uint64_t)n * 4),
+                       span(ws, need)};
+  const Span ins[] = {span(BuT, (uint64_t)r * m / 8), span(BvT, (uint64_t)n * r / 8),
+                      span(L->s_out, (uint64_t)m * 2), span(L->s_mid, (uint64_t)r * 2),
+                      span(L->s_in, (uint64_t)n * 2), span(x, (uint64_t)T * n * 2),
+                      span(dy, (uint64_t)T * m * 2), span(saved, saved_need)};
+  for (size_t i = 0; i < sizeof(outs) / sizeof(outs[0]); ++i) {
+    for (const Span &in : ins)
+      if (overlap(outs[i], in)) return AF1_ERR_ALIAS;
+    for (size_t j = i + 1; j < sizeof(outs) / sizeof(outs[0]); ++j)
+      if (overlap(outs[i], outs[j])) return AF1_ERR_ALIAS;
+  }
+  return hip_status(af1::launch_backward(m, n, r, BuT, BvT, L->s_out, L->s_mid, L->s_in, x, dy,
+                                         T, saved, dx, ds_out, ds_mid, ds_in, accumulate ? 1 : 0,
+                                         ws, as_stream(stream)));
 }
 
 int64_t af1_storage_bits(int64_t m, int64_t n, int64_t r) {

@@ -55,6 +55,20 @@ typedef float float2v __attribute__((ext_vector_type(2)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+// What one launch of the contraction computes (the A operand, the sign
+// words and the tiling are the same in all of them).
+//   kMid     forward G1: fp16 operands; C = fp16(acc), pair order.
+//   kOut     forward G2: fp16 operands; C = bf16(rowscale * acc).
+//   kOutSave kOut, and F = acc (fp32, natural order) for the backward.
+//   kBwdMid  backward, first product: bf16 operands, B = +-1;
+//            C = bf16(rowscale * acc), pair order; F = per-tile token sums
+//            of acc * S, S fp16 in pair order.
+//   kBwdIn   backward, second product: bf16 operands, B = +-1;
+//            C = bf16(rowscale * acc) when C is given; F = per-tile token
+//            sums of acc * S, S bf16 in natural order.
+enum Mode : int { kMid = 0, kOut = 1, kOutSave = 2, kBwdMid = 3, kBwdIn = 4 };
 
 constexpr int BM = 128;          // tokens per tile
 constexpr int BN = 256;          // weight rows per tile
@@ -84,11 +98,6 @@ static_assert(kATile + 3 * 32 * kARow + kARow < 65536, "immediate LDS offsets");
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef int i32x4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, int64_t bytes) {
-  const int n = bytes > 0x7fffffff ? 0x7fffffff : (bytes < 0 ? 0 : (int)bytes);
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, n, 0x00020000);
-}
 
 // The same raw buffer resource (stride 0, raw dword access) as four scalar
 // dwords, for the copy instructions below.
@@ -191,13 +200,16 @@ __global__ __launch_bounds__(256) void prep_kernel(const uint16_t *__restrict__ 
   }
 }
 
-// C = rowscale * (A_pairorder x (sign(W) * colscale)^T).  kOutBf16: C is
-// bf16 in natural column order (y); otherwise fp16 in pair order (Z).
-template <bool kOutBf16, int kBM>
+// C = rowscale * (A_pairorder x (sign(W) * colscale)^T), the forms listed
+// under Mode.  In the bf16 modes the column scale is 1 (the backward folds
+// its column scales into A), so no scale pairs are staged.
+template <int kMode, int kBM>
 __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     const uint16_t *__restrict__ A, int T, int K, const uint32_t *__restrict__ W, int N,
     const uint32_t *__restrict__ cspairs, int Kpad, const uint16_t *__restrict__ rowscale,
-    uint16_t *__restrict__ C) {
+    uint16_t *__restrict__ C, const uint16_t *__restrict__ S, float *__restrict__ F) {
+  constexpr bool kBf16 = kMode >= kBwdMid;
+  constexpr bool kPairOut = kMode == kMid || kMode == kBwdMid;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -249,7 +261,7 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       copy16(as, lds + kA0 + buf * kATile + (kACopies * wave + jj) * 1024, a_off[jj]);
 #pragma unroll
     for (int i = 0; i < 4; ++i) copy4(ws, lds + kW0 + buf * kWTile + (64 * wave + 16 * i) * 16, w_off[i]);
-    if (wave == 0) {
+    if (!kBf16 && wave == 0) {
       const i32x4 cs =
           copy_rsrc(cspairs + step * (kCsTile / 4), (int64_t)Kpad * 2 - (int64_t)step * kCsTile);
       copy4(cs, lds + kCs0 + buf * kCsTile, 4 * lane);
@@ -289,6 +301,7 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
 
   uint32_t kSignMask;
   asm volatile("v_mov_b32 %0, 0x80008000" : "=v"(kSignMask));
+  constexpr uint32_t kBf16OnePair = 0x3f803f80u;  // bf16 +1, +1
 
   wait_copies();
   __syncthreads();
@@ -307,7 +320,7 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
 #pragma unroll
       for (int i = 0; i < kTokBlocks; ++i)
         af[slot][i] = *reinterpret_cast<const half8 *>(abase + a_rd[ks] + 32 * i * kARow);
-      c4[slot] = cs[2 * ks + g];
+      if constexpr (!kBf16) c4[slot] = cs[2 * ks + g];
     };
     read_ops(0, 0);
     static_for<2 * kWords>([&](auto KS) {
@@ -317,17 +330,32 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       // Keep the next step's LDS reads ahead of this step's MFMAs (the
       // scheduler would otherwise sink them next to their use).
       __builtin_amdgcn_sched_barrier(0);
-      const uint32_t cpair[4] = {c4[cur].x, c4[cur].y, c4[cur].z, c4[cur].w};
+      uint32_t cpair[4];
+      if constexpr (kBf16) {
+        // Words past the row end (a partial last K step) meet +-0, as the
+        // zero column-scale padding does in the fp16 modes.
+        const uint32_t one = step * kWords + (ks >> 1) < kw ? kBf16OnePair : 0u;
+        cpair[0] = cpair[1] = cpair[2] = cpair[3] = one;
+      } else {
+        cpair[0] = c4[cur].x; cpair[1] = c4[cur].y; cpair[2] = c4[cur].z; cpair[3] = c4[cur].w;
+      }
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const uint32_t w = wj[j][ks >> 1];
         uint32_t bd[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) bd[e] = cpair[e] ^ ((w << sh[ks & 1][e]) & kSignMask);
-        const half8 bf = __builtin_bit_cast(half8, make_uint4(bd[0], bd[1], bd[2], bd[3]));
+        const uint4 bq = make_uint4(bd[0], bd[1], bd[2], bd[3]);
 #pragma unroll
-        for (int i = 0; i < kTokBlocks; ++i)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[cur][i], bf, acc[i][j], 0, 0, 0);
+        for (int i = 0; i < kTokBlocks; ++i) {
+          if constexpr (kBf16)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf16x8, af[cur][i]), __builtin_bit_cast(bf16x8, bq), acc[i][j],
+                0, 0, 0);
+          else
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
+                af[cur][i], __builtin_bit_cast(half8, bq), acc[i][j], 0, 0, 0);
+        }
       }
     });
     wait_copies();
@@ -344,9 +372,30 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int n = wrow0 + 32 * j;
+    if constexpr (kMode == kBwdMid || kMode == kBwdIn) {
+      // Token sum of acc * S over this tile for weight row n: the lane's
+      // sixteen tokens per block, then its partner half (lane XOR 32).
+      float part = 0.f;
+      if (n < N) {
+        const int spos = kMode == kBwdMid ? pair_pos(n) : n;
+#pragma unroll
+        for (int i = 0; i < kTokBlocks; ++i)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int t = t0 + 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
+            if (t < T) {
+              const uint16_t sv = S[(size_t)t * N + spos];
+              part += acc[i][j][e] * (kMode == kBwdMid ? f16_to_f32(sv) : bf16_to_f32(sv));
+            }
+          }
+      }
+      part += __shfl_xor(part, 32, 64);
+      if (g == 0 && n < N) F[(size_t)(t0 / kBM) * N + n] = part;
+    }
     if (n >= N) continue;
+    if (kMode == kBwdIn && !C) continue;
     const float rs = rowscale ? f16_to_f32(rowscale[n]) : 1.0f;
-    const int cpos = kOutBf16 ? n : pair_pos(n);
+    const int cpos = kPairOut ? pair_pos(n) : n;
 #pragma unroll
     for (int i = 0; i < kTokBlocks; ++i) {
 #pragma unroll
@@ -354,16 +403,210 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
         const int t = t0 + 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
         if (t < T) {
           const float v = acc[i][j][e] * rs;
-          C[(size_t)t * N + cpos] = kOutBf16 ? f32_to_bf16(v) : f32_to_f16(v);
+          C[(size_t)t * N + cpos] = kMode == kMid ? f32_to_f16(v) : f32_to_bf16(v);
+          if constexpr (kMode == kOutSave) F[(size_t)t * N + n] = acc[i][j][e];
         }
       }
     }
   }
 }
 
+// Backward preparation, one launch: dy (bf16, [T][m]) -> A1 = bf16(dy *
+// s_out) in pair order, the A operand of the first backward product, and
+// per-64-token partial sums of dy * z (z = the saved pre-scale forward
+// output, fp32 [T][m]) for the gradient of s_out.  Thread (ty, ux) of a
+// block handles the 16 columns of unit ux (as in pair_order_unit) for
+// tokens t0 + ty + 16 q; the 16 ty partials of a column are added in a
+// fixed order through LDS.
+constexpr int kPrepTokens = 64;
+__global__ __launch_bounds__(256) void bwd_prep_kernel(const uint16_t *__restrict__ dy,
+                                                       const uint16_t *__restrict__ s_out,
+                                                       const float *__restrict__ z, int T, int m,
+                                                       uint16_t *__restrict__ A1,
+                                                       float *__restrict__ part) {
+  __shared__ float red[16][256 + 4];
+  const int ux = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  const int ur = blockIdx.x * 16 + ux;                       // unit within the row
+  const int c = (ur >> 1) * 32 + 8 * (ur & 1);               // first of its columns
+  const int tb = blockIdx.y;
+  const bool live = c < m;
+  float so[16], acc[16];
+#pragma unroll
+  for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+  if (live) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      so[q] = f16_to_f32(s_out[c + q]);
+      so[8 + q] = f16_to_f32(s_out[c + 16 + q]);
+    }
+  }
+#pragma unroll
+  for (int q4 = 0; q4 < kPrepTokens / 16; ++q4) {
+    const int t = tb * kPrepTokens + ty + 16 * q4;
+    if (!live || t >= T) continue;
+    const uint16_t *src = dy + (size_t)t * m + c;
+    const u32x4 lo = *reinterpret_cast<const u32x4 *>(src);
+    const u32x4 hi = *reinterpret_cast<const u32x4 *>(src + 16);
+    const float *zr = z + (size_t)t * m + c;
+    const float4 z0 = *reinterpret_cast<const float4 *>(zr);
+    const float4 z1 = *reinterpret_cast<const float4 *>(zr + 4);
+    const float4 z2 = *reinterpret_cast<const float4 *>(zr + 16);
+    const float4 z3 = *reinterpret_cast<const float4 *>(zr + 20);
+    const float zl[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
+    const float zh[8] = {z2.x, z2.y, z2.z, z2.w, z3.x, z3.y, z3.z, z3.w};
+    uint32_t d[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float g0 = __uint_as_float(lo[e] << 16), g1 = __uint_as_float(lo[e] & 0xffff0000u);
+      const float h0 = __uint_as_float(hi[e] << 16), h1 = __uint_as_float(hi[e] & 0xffff0000u);
+      acc[2 * e] += g0 * zl[2 * e];
+      acc[2 * e + 1] += g1 * zl[2 * e + 1];
+      acc[8 + 2 * e] += h0 * zh[2 * e];
+      acc[8 + 2 * e + 1] += h1 * zh[2 * e + 1];
+      // pair dword: column c+k (low half) with its partner c+16+k (high)
+      d[2 * e] = (uint32_t)f32_to_bf16(g0 * so[2 * e]) |
+                 ((uint32_t)f32_to_bf16(h0 * so[8 + 2 * e]) << 16);
+      d[2 * e + 1] = (uint32_t)f32_to_bf16(g1 * so[2 * e + 1]) |
+                     ((uint32_t)f32_to_bf16(h1 * so[8 + 2 * e + 1]) << 16);
+    }
+    uint4 *dst = reinterpret_cast<uint4 *>(A1 + (size_t)t * m + (c & ~31) + 2 * (c & 15));
+    dst[0] = make_uint4(d[0], d[1], d[2], d[3]);
+    dst[1] = make_uint4(d[4], d[5], d[6], d[7]);
+  }
+  // columns of this block: unit ux covers local columns lc .. lc+7 and
+  // lc+16 .. lc+23 of the block's 256
+  const int lc = (ux >> 1) * 32 + 8 * (ux & 1);
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    red[ty][lc + q] = acc[q];
+    red[ty][lc + 16 + q] = acc[8 + q];
+  }
+  __syncthreads();
+  const int col = blockIdx.x * 256 + threadIdx.x;
+  if (col < m) {
+    float sum = 0.f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) sum += red[k][threadIdx.x];
+    part[(size_t)tb * m + col] = sum;
+  }
+}
+
+// ds[c] = (accumulate ? ds[c] : 0) + sum over tiles of part[tile][c], for
+// the three scale gradients in one launch (tile sums in a fixed order).
+__global__ __launch_bounds__(256) void bwd_finish_kernel(
+    const float *__restrict__ p_out, int n_out_tiles, float *__restrict__ ds_out, int m,
+    const float *__restrict__ p_mid, int n_mid_tiles, float *__restrict__ ds_mid, int r,
+    const float *__restrict__ p_in, int n_in_tiles, float *__restrict__ ds_in, int n,
+    int accumulate) {
+  int idx = blockIdx.x * 256 + threadIdx.x;
+  const float *p;
+  float *ds;
+  int tiles, len;
+  if (idx < m) {
+    p = p_out; ds = ds_out; tiles = n_out_tiles; len = m;
+  } else if ((idx -= m) < r) {
+    p = p_mid; ds = ds_mid; tiles = n_mid_tiles; len = r;
+  } else if ((idx -= r) < n) {
+    p = p_in; ds = ds_in; tiles = n_in_tiles; len = n;
+  } else {
+    return;
+  }
+  float sum = accumulate ? ds[idx] : 0.f;
+  float tot = 0.f;
+  for (int k = 0; k < tiles; ++k) tot += p[(size_t)k * len + idx];
+  ds[idx] = sum + tot;
+}
+
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
 int64_t kpad(int64_t K) { return (K + BK - 1) / BK * BK; }
+
+// One contraction C[T, N] over K on the stream.  A grid of 128-token tiles
+// that gives each compute unit at most one workgroup (one wave per SIMD)
+// uses 64-token tiles instead: twice the workgroups, each expanding its
+// signs for half as many tokens.  Measured on 8192x8192 G1 (+2%); grids
+// between one and two workgroups per unit were slower with it.  *tile_tokens
+// receives the token-tile height used (the row count of F's per-tile sums).
+template <int kMode>
+hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *W, int64_t N,
+                       const uint32_t *cs, const uint16_t *rs, uint16_t *C, const uint16_t *S,
+                       float *F, hipStream_t s, int *tile_tokens = nullptr) {
+  const int cus = device_cus();
+  const unsigned gx = (unsigned)((N + BN - 1) / BN);
+  const int64_t tiles128 = (int64_t)gx * ((T + BM - 1) / BM);
+  if (tiles128 <= (int64_t)cus && T > 64) {
+    dim3 g(gx, (unsigned)((T + 63) / 64));
+    bingemm_kernel<kMode, 64><<<g, kThreads, Lds<64>::kBytes, s>>>(
+        A, (int)T, (int)K, W, (int)N, cs, (int)kpad(K), rs, C, S, F);
+    if (tile_tokens) *tile_tokens = 64;
+  } else {
+    dim3 g(gx, (unsigned)((T + BM - 1) / BM));
+    bingemm_kernel<kMode, BM><<<g, kThreads, Lds<BM>::kBytes, s>>>(
+        A, (int)T, (int)K, W, (int)N, cs, (int)kpad(K), rs, C, S, F);
+    if (tile_tokens) *tile_tokens = BM;
+  }
+  return hipGetLastError();
+}
+
+// x -> pair-order fp16 and the two column-scale pair arrays, in one launch.
+hipError_t prepare_forward(int64_t n, int64_t r, const uint16_t *s_mid, const uint16_t *s_in,
+                           const uint16_t *x, int64_t T, uint16_t *xp, uint32_t *cs1,
+                           uint32_t *cs2, hipStream_t s) {
+  const int64_t units = T * (n / 16);
+  const int nbx = (int)((units + 255) / 256);
+  const int nb1 = (int)((kpad(n) / 2 + 255) / 256);
+  const int nb2 = (int)((kpad(r) / 2 + 255) / 256);
+  prep_kernel<<<(unsigned)(nbx + nb1 + nb2), 256, 0, s>>>(x, xp, (int)T, (int)n, s_in, cs1,
+                                                           (int)kpad(n), s_mid, cs2, (int)r,
+                                                           (int)kpad(r), nbx, nb1);
+  return hipGetLastError();
+}
+
+struct FwdWs {
+  uint16_t *xp, *Z;
+  uint32_t *cs1, *cs2;
+};
+
+FwdWs forward_ws(void *ws, int64_t n, int64_t r, int64_t T) {
+  uint8_t *base = static_cast<uint8_t *>(ws);
+  FwdWs w;
+  w.xp = reinterpret_cast<uint16_t *>(base);
+  base += align256((size_t)T * n * 2);
+  w.Z = reinterpret_cast<uint16_t *>(base);
+  base += align256((size_t)T * r * 2);
+  w.cs1 = reinterpret_cast<uint32_t *>(base);
+  base += align256((size_t)kpad(n) * 2);
+  w.cs2 = reinterpret_cast<uint32_t *>(base);
+  return w;
+}
+
+int64_t tiles64(int64_t T) { return (T + 63) / 64; }
+
+struct BwdWs {
+  uint16_t *A1, *Zb;
+  float *p_out, *p_mid, *p_in;
+};
+
+BwdWs backward_ws(void *ws, int64_t m, int64_t n, int64_t r, int64_t T) {
+  uint8_t *base = static_cast<uint8_t *>(ws);
+  BwdWs w;
+  w.A1 = reinterpret_cast<uint16_t *>(base);
+  base += align256((size_t)T * m * 2);
+  w.Zb = reinterpret_cast<uint16_t *>(base);
+  base += align256((size_t)T * r * 2);
+  w.p_out = reinterpret_cast<float *>(base);
+  base += align256((size_t)tiles64(T) * m * 4);
+  w.p_mid = reinterpret_cast<float *>(base);
+  base += align256((size_t)tiles64(T) * r * 4);
+  w.p_in = reinterpret_cast<float *>(base);
+  return w;
+}
+
+size_t backward_ws_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
+  return align256((size_t)T * m * 2) + align256((size_t)T * r * 2) +
+         align256((size_t)tiles64(T) * m * 4) + align256((size_t)tiles64(T) * r * 4) +
+         align256((size_t)tiles64(T) * n * 4);
+}
 
 }  // namespace
 
@@ -385,48 +628,74 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
   if (T * n * 2 > 0x7fffffff || T * r * 2 > 0x7fffffff || m * (r / 32) * 4 > 0x7fffffff ||
       r * (n / 32) * 4 > 0x7fffffff)
     return hipErrorInvalidValue;
-  uint8_t *base = static_cast<uint8_t *>(ws);
-  uint16_t *xp = reinterpret_cast<uint16_t *>(base);
-  base += align256((size_t)T * n * 2);
-  uint16_t *Z = reinterpret_cast<uint16_t *>(base);
-  base += align256((size_t)T * r * 2);
-  uint32_t *cs1 = reinterpret_cast<uint32_t *>(base);
-  base += align256((size_t)kpad(n) * 2);
-  uint32_t *cs2 = reinterpret_cast<uint32_t *>(base);
-  const int64_t units = T * (n / 16);
-  const int nbx = (int)((units + 255) / 256);
-  const int nb1 = (int)((kpad(n) / 2 + 255) / 256);
-  const int nb2 = (int)((kpad(r) / 2 + 255) / 256);
-  prep_kernel<<<(unsigned)(nbx + nb1 + nb2), 256, 0, s>>>(x, xp, (int)T, (int)n, s_in, cs1,
-                                                           (int)kpad(n), s_mid, cs2, (int)r,
-                                                           (int)kpad(r), nbx, nb1);
+  const FwdWs w = forward_ws(ws, n, r, T);
+  hipError_t e = prepare_forward(n, r, s_mid, s_in, x, T, w.xp, w.cs1, w.cs2, s);
+  if (e != hipSuccess) return e;
+  e = contraction<kMid>(w.xp, T, n, Bv, r, w.cs1, nullptr, w.Z, nullptr, nullptr, s);
+  if (e != hipSuccess) return e;
+  return contraction<kOut>(w.Z, T, r, Bu, m, w.cs2, s_out, y, nullptr, nullptr, s);
+}
+
+size_t train_saved_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
+  (void)n;
+  // the pre-scale intermediate v = Bv (s_in .* x), fp16 in pair order, and
+  // the pre-scale output z = Bu (s_mid .* v), fp32
+  return align256((size_t)T * r * 2) + align256((size_t)T * m * 4);
+}
+
+size_t train_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
+  const size_t f = gemm_workspace_bytes(m, n, r, T), b = backward_ws_bytes(m, n, r, T);
+  return f > b ? f : b;
+}
+
+hipError_t launch_forward_train(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
+                                const uint32_t *Bv, const uint16_t *s_out,
+                                const uint16_t *s_mid, const uint16_t *s_in,
+                                const uint16_t *x, int64_t T, uint16_t *y, void *saved,
+                                void *ws, hipStream_t s) {
+  if (T * n * 2 > 0x7fffffff || T * r * 2 > 0x7fffffff || m * (r / 32) * 4 > 0x7fffffff ||
+      r * (n / 32) * 4 > 0x7fffffff)
+    return hipErrorInvalidValue;
+  const FwdWs w = forward_ws(ws, n, r, T);
+  uint16_t *v = static_cast<uint16_t *>(saved);
+  float *z = reinterpret_cast<float *>(static_cast<uint8_t *>(saved) + align256((size_t)T * r * 2));
+  hipError_t e = prepare_forward(n, r, s_mid, s_in, x, T, w.xp, w.cs1, w.cs2, s);
+  if (e != hipSuccess) return e;
+  e = contraction<kMid>(w.xp, T, n, Bv, r, w.cs1, nullptr, v, nullptr, nullptr, s);
+  if (e != hipSuccess) return e;
+  return contraction<kOutSave>(v, T, r, Bu, m, w.cs2, s_out, y, nullptr, z, s);
+}
+
+hipError_t launch_backward(int64_t m, int64_t n, int64_t r, const uint32_t *BuT,
+                           const uint32_t *BvT, const uint16_t *s_out, const uint16_t *s_mid,
+                           const uint16_t *s_in, const uint16_t *x, const uint16_t *dy,
+                           int64_t T, const void *saved, uint16_t *dx, float *ds_out,
+                           float *ds_mid, float *ds_in, int accumulate, void *ws,
+                           hipStream_t s) {
+  if (T * m * 2 > 0x7fffffff || T * r * 2 > 0x7fffffff || r * (m / 32) * 4 > 0x7fffffff ||
+      n * (r / 32) * 4 > 0x7fffffff)
+    return hipErrorInvalidValue;
+  const BwdWs w = backward_ws(ws, m, n, r, T);
+  const uint16_t *v = static_cast<const uint16_t *>(saved);
+  const float *z = reinterpret_cast<const float *>(static_cast<const uint8_t *>(saved) +
+                                                   align256((size_t)T * r * 2));
+  const dim3 gp((unsigned)((m + 255) / 256), (unsigned)tiles64(T));
+  bwd_prep_kernel<<<gp, 256, 0, s>>>(dy, s_out, z, (int)T, (int)m, w.A1, w.p_out);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // A grid of 128-token tiles that gives each compute unit at most one
-  // workgroup (one wave per SIMD) uses 64-token tiles instead: twice the
-  // workgroups, each expanding its signs for half as many tokens.  Measured
-  // on 8192x8192 G1 (+2%); grids between one and two workgroups per unit
-  // were slower with it.
-  const int cus = device_cus();
-  auto launch = [&](auto kOut, const uint16_t *A, int64_t K, const uint32_t *W, int64_t N,
-                    const uint32_t *cs, const uint16_t *rs, uint16_t *C) {
-    constexpr bool kOutBf16 = decltype(kOut)::value;
-    const unsigned gx = (unsigned)((N + BN - 1) / BN);
-    const int64_t tiles128 = (int64_t)gx * ((T + BM - 1) / BM);
-    if (tiles128 <= (int64_t)cus && T > 64) {
-      dim3 g(gx, (unsigned)((T + 63) / 64));
-      bingemm_kernel<kOutBf16, 64><<<g, kThreads, Lds<64>::kBytes, s>>>(
-          A, (int)T, (int)K, W, (int)N, cs, (int)kpad(K), rs, C);
-    } else {
-      dim3 g(gx, (unsigned)((T + BM - 1) / BM));
-      bingemm_kernel<kOutBf16, BM><<<g, kThreads, Lds<BM>::kBytes, s>>>(
-          A, (int)T, (int)K, W, (int)N, cs, (int)kpad(K), rs, C);
-    }
-    return hipGetLastError();
-  };
-  e = launch(std::false_type{}, xp, n, Bv, r, cs1, nullptr, Z);
+  // dt = Bu^T (s_out .* dy): weight rows are the r rows of Bu^T; the output
+  // is s_mid .* dt in pair order (the next A operand); sums dt .* v.
+  int tm = 0, ti = 0;
+  e = contraction<kBwdMid>(w.A1, T, m, BuT, r, nullptr, s_mid, w.Zb, v, w.p_mid, s, &tm);
   if (e != hipSuccess) return e;
-  return launch(std::true_type{}, Z, r, Bu, m, cs2, s_out, y);
+  // du = Bv^T (s_mid .* dt): dx = s_in .* du; sums du .* x.
+  e = contraction<kBwdIn>(w.Zb, T, r, BvT, n, nullptr, s_in, dx, x, w.p_in, s, &ti);
+  if (e != hipSuccess) return e;
+  const int total = (int)(m + r + n);
+  bwd_finish_kernel<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(
+      w.p_out, (int)tiles64(T), ds_out, (int)m, w.p_mid, (int)((T + tm - 1) / tm), ds_mid,
+      (int)r, w.p_in, (int)((T + ti - 1) / ti), ds_in, (int)n, accumulate);
+  return hipGetLastError();
 }
 
 }  // namespace af1

@@ -17,6 +17,11 @@ hipError_t launch_pack(const void *src, int dtype, int64_t rows, int64_t cols,
 hipError_t launch_unpack(const uint32_t *words, int64_t rows, int64_t cols,
                          int8_t *dst, hipStream_t s);
 
+// dst (cols x rows signs) = transpose of src (rows x cols signs); rows and
+// cols are multiples of 32.
+hipError_t launch_transpose(const uint32_t *src, int64_t rows, int64_t cols, uint32_t *dst,
+                            hipStream_t s);
+
 size_t gemv_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t b);
 hipError_t launch_gemv(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
                        const uint32_t *Bv, const uint16_t *s_out,
@@ -40,5 +45,22 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
                        const uint16_t *s_mid, const uint16_t *s_in,
                        const uint16_t *x, int64_t T, uint16_t *y, void *ws,
                        hipStream_t s);
+
+// Scale-only reconstruction (sign matrices frozen): a forward that keeps
+// the two pre-scale intermediates, and the gradients with respect to the
+// scales and x from the transposed factors.
+size_t train_saved_bytes(int64_t m, int64_t n, int64_t r, int64_t T);
+size_t train_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T);
+hipError_t launch_forward_train(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
+                                const uint32_t *Bv, const uint16_t *s_out,
+                                const uint16_t *s_mid, const uint16_t *s_in,
+                                const uint16_t *x, int64_t T, uint16_t *y, void *saved,
+                                void *ws, hipStream_t s);
+hipError_t launch_backward(int64_t m, int64_t n, int64_t r, const uint32_t *BuT,
+                           const uint32_t *BvT, const uint16_t *s_out, const uint16_t *s_mid,
+                           const uint16_t *s_in, const uint16_t *x, const uint16_t *dy,
+                           int64_t T, const void *saved, uint16_t *dx, float *ds_out,
+                           float *ds_mid, float *ds_in, int accumulate, void *ws,
+                           hipStream_t s);
 
 }  // namespace af1

@@ -63,6 +63,51 @@ class DeviceLayer:
         af1.af1_linear_gemm(self.desc, x, T, y, ws, ws.numel(), stream)
         return y
 
+    # -- scale-only reconstruction: signs frozen, scales trained -----------
+
+    def transposed(self, stream=None):
+        """(Bu^T, Bv^T) in the packed format, made once on the device."""
+        if getattr(self, "_T", None) is None:
+            BuT = torch.empty((self.r, self.m // 32), dtype=torch.int32, device=self.Bu.device)
+            BvT = torch.empty((self.n, self.r // 32), dtype=torch.int32, device=self.Bu.device)
+            af1.af1_pack_transpose(self.Bu, self.m, self.r, BuT, stream)
+            af1.af1_pack_transpose(self.Bv, self.r, self.n, BvT, stream)
+            self._T = (BuT, BvT)
+        return self._T
+
+    def forward_train(self, x, y=None, saved=None, ws=None, stream=None):
+        T = x.shape[0]
+        if y is None:
+            y = torch.empty((T, self.m), dtype=torch.int16, device=x.device)
+        if saved is None:
+            saved = torch.empty(af1.af1_train_saved_bytes(self.m, self.n, self.r, T),
+                                dtype=torch.uint8, device=x.device)
+        if ws is None:
+            ws = torch.empty(af1.af1_train_workspace_bytes(self.m, self.n, self.r, T),
+                             dtype=torch.uint8, device=x.device)
+        af1.af1_linear_forward_train(self.desc, x, T, y, saved, saved.numel(), ws, ws.numel(),
+                                     stream)
+        return y, saved
+
+    def backward(self, x, dy, saved, dx=None, grads=None, accumulate=False, ws=None,
+                 stream=None, want_dx=True):
+        """dx ([T, n] bf16 patterns, or None) and the fp32 scale gradients
+        (ds_out, ds_mid, ds_in)."""
+        T = x.shape[0]
+        BuT, BvT = self.transposed(stream)
+        if dx is None and want_dx:
+            dx = torch.empty((T, self.n), dtype=torch.int16, device=x.device)
+        if grads is None:
+            grads = tuple(torch.empty(k, dtype=torch.float32, device=x.device)
+                          for k in (self.m, self.r, self.n))
+        if ws is None:
+            ws = torch.empty(af1.af1_train_workspace_bytes(self.m, self.n, self.r, T),
+                             dtype=torch.uint8, device=x.device)
+        af1.af1_linear_backward(self.desc, BuT, BvT, x, dy, T, saved, saved.numel(), dx,
+                                grads[0], grads[1], grads[2], int(bool(accumulate)), ws,
+                                ws.numel(), stream)
+        return dx, grads
+
 
 def gemv_multi(layers, x: torch.Tensor, ys=None, ws: torch.Tensor = None, stream=None):
     """One decode step of several layers that read the same x (same n)."""

@@ -188,3 +188,89 @@ def test_binding_raises_on_error():
     with pytest.raises(af1.Af1Error) as ei:
         af1.af1_linear_gemv(None, X, 1, Y, WS, 1 << 20, stream=0)
     assert ei.value.status == af1.AF1_ERR_NULL
+
+
+def test_transpose_validation():
+    Tp = af1.af1_pack_transpose
+    call = lambda src=X, rows=64, cols=96, dst=Y: Tp(src, rows, cols, dst, stream=0, check=False)
+    assert call(src=None) == af1.AF1_ERR_NULL
+    assert call(dst=None) == af1.AF1_ERR_NULL
+    for rows, cols in [(48, 96), (64, 40), (-32, 64), (64, -32),
+                       ((1 << 24) + 32, 32), (32, (1 << 24) + 32), (1 << 21, 1 << 20)]:
+        assert call(rows=rows, cols=cols) == af1.AF1_ERR_SHAPE, (rows, cols)
+    assert call(src=X + 4) == af1.AF1_ERR_ALIGN
+    assert call(dst=Y + 8) == af1.AF1_ERR_ALIGN
+    assert call(dst=X + 256) == af1.AF1_ERR_ALIAS   # 64 x 96 bits = 768 bytes
+
+
+SAVED = BASE + 600 * MB
+BUT = BASE + 700 * MB
+BVT = BASE + 800 * MB
+DY = BASE + 900 * MB
+DX = BASE + 1000 * MB
+G_OUT, G_MID, G_IN = BASE + 1100 * MB, BASE + 1101 * MB, BASE + 1102 * MB
+
+
+def fwd_train(layer, x=X, T=16, y=Y, saved=SAVED, saved_bytes=1 << 30, ws=WS, ws_bytes=1 << 30):
+    return af1.af1_linear_forward_train(layer, x, T, y, saved, saved_bytes, ws, ws_bytes,
+                                        stream=0, check=False)
+
+
+def bwd(layer, BuT=BUT, BvT=BVT, x=X, dy=DY, T=16, saved=SAVED, saved_bytes=1 << 30, dx=DX,
+        g=(G_OUT, G_MID, G_IN), acc=0, ws=WS, ws_bytes=1 << 30):
+    return af1.af1_linear_backward(layer, BuT, BvT, x, dy, T, saved, saved_bytes, dx, g[0], g[1],
+                                   g[2], acc, ws, ws_bytes, stream=0, check=False)
+
+
+def test_forward_train_validation():
+    assert fwd_train(None) == af1.AF1_ERR_NULL
+    assert fwd_train(fake_layer(4096, 4096, 33)) == af1.AF1_ERR_SHAPE
+    assert fwd_train(fake_layer(), saved=None) == af1.AF1_ERR_NULL
+    assert fwd_train(fake_layer(), saved=SAVED + 8) == af1.AF1_ERR_ALIGN
+    assert fwd_train(fake_layer(), T=0) == af1.AF1_ERR_BATCH
+    # T * max(m, n, r) * 2 < 2^31: m is the widest here
+    assert fwd_train(fake_layer(65536, 1024, 512), T=16384, saved_bytes=1 << 40,
+                     ws_bytes=1 << 40) == af1.AF1_ERR_BATCH
+    need = af1.af1_train_saved_bytes(4096, 4096, 2016, 16)
+    assert need >= 16 * 2016 * 2 + 16 * 4096 * 4
+    assert fwd_train(fake_layer(), saved_bytes=need - 1) == af1.AF1_ERR_WORKSPACE
+    wneed = af1.af1_train_workspace_bytes(4096, 4096, 2016, 16)
+    assert wneed >= af1.af1_gemm_workspace_bytes(4096, 4096, 2016, 16)
+    assert fwd_train(fake_layer(), ws_bytes=wneed - 1) == af1.AF1_ERR_WORKSPACE
+    assert fwd_train(fake_layer(), saved=X) == af1.AF1_ERR_ALIAS
+    assert fwd_train(fake_layer(), saved=Y) == af1.AF1_ERR_ALIAS
+    assert fwd_train(fake_layer(), saved=WS + 1024) == af1.AF1_ERR_ALIAS
+    assert fwd_train(fake_layer(), y=SAVED) == af1.AF1_ERR_ALIAS
+    assert af1.af1_train_saved_bytes(4096, 4096, 2016, 0) == 0
+    assert af1.af1_train_workspace_bytes(4096, 33, 2016, 1) == 0
+
+
+def test_backward_validation():
+    L = fake_layer()
+    assert bwd(None) == af1.AF1_ERR_NULL
+    assert bwd(fake_layer(4096, 48, 2016)) == af1.AF1_ERR_SHAPE
+    for kw in ("BuT", "BvT", "x", "dy", "saved"):
+        assert bwd(L, **{kw: None}) == af1.AF1_ERR_NULL, kw
+    assert bwd(L, g=(None, G_MID, G_IN)) == af1.AF1_ERR_NULL
+    assert bwd(L, g=(G_OUT, G_MID, None)) == af1.AF1_ERR_NULL
+    Lnull = fake_layer()
+    Lnull.Bu = None
+    Lnull.Bv = None                  # the forward factors are not read: the
+    assert bwd(Lnull, T=0) == af1.AF1_ERR_BATCH   # next check is reached
+    Ls = fake_layer()
+    Ls.s_mid = None
+    assert bwd(Ls) == af1.AF1_ERR_NULL
+    assert bwd(L, T=0) == af1.AF1_ERR_BATCH
+    assert bwd(L, T=(1 << 20) + 1) == af1.AF1_ERR_BATCH
+    assert bwd(L, dy=DY + 2) == af1.AF1_ERR_ALIGN
+    assert bwd(L, g=(G_OUT + 4, G_MID, G_IN)) == af1.AF1_ERR_ALIGN
+    need = af1.af1_train_saved_bytes(4096, 4096, 2016, 16)
+    assert bwd(L, saved_bytes=need - 1) == af1.AF1_ERR_WORKSPACE
+    assert bwd(L, ws=None, ws_bytes=0) == af1.AF1_ERR_WORKSPACE
+    # outputs against inputs and against each other
+    assert bwd(L, dx=DY) == af1.AF1_ERR_ALIAS
+    assert bwd(L, dx=SAVED + 256) == af1.AF1_ERR_ALIAS
+    assert bwd(L, g=(G_OUT, G_OUT + 1024, G_IN)) == af1.AF1_ERR_ALIAS
+    assert bwd(L, g=(BASE + 128 * MB, G_MID, G_IN)) == af1.AF1_ERR_ALIAS
+    assert bwd(L, ws=BUT) == af1.AF1_ERR_ALIAS
+    assert bwd(L, dx=WS) == af1.AF1_ERR_ALIAS

@@ -1,0 +1,204 @@
+"""GPU parity of the scale-only reconstruction path (Sec. 4.1: sign matrices
+frozen, s_out / s_mid / s_in trained) through the C ABI against the fp64
+oracle on the same seeded inputs.
+
+Bars: the packed transpose bit-exact; the training forward's y bit-identical
+to the inference forward's; dx within relative L2 5e-3 per token (max over
+tokens) and each scale gradient within relative L2 5e-3 of the oracle's;
+gradient accumulation, dx skipping and repeated calls bit-exact."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_06161_amd import af1, synth
+from paper_2609_06161_amd.layer import DeviceLayer, bf16_bits_to_f64, to_device
+
+pytestmark = pytest.mark.gpu
+
+TOL = 5e-3
+
+
+def rel_l2(a, e):
+    a = np.asarray(a, np.float64)
+    e = np.asarray(e, np.float64)
+    return float(np.linalg.norm(a - e) / np.linalg.norm(e))
+
+
+def max_row_rel_l2(y, ref):
+    worst = 0.0
+    for a, e in zip(np.asarray(y, np.float64), np.asarray(ref, np.float64)):
+        ne = np.linalg.norm(e)
+        if ne == 0.0:
+            assert np.all(a == 0.0)
+            continue
+        worst = max(worst, np.linalg.norm(a - e) / ne)
+    return worst
+
+
+def f32(t):
+    return t.detach().cpu().numpy().astype(np.float64)
+
+
+def run_train(lin, dy, accumulate_into=None, want_dx=True):
+    print(f"train m={lin.m} n={lin.n} r={lin.r} T={lin.x.shape[0]}", flush=True)
+    L = DeviceLayer.from_host(lin)
+    x = to_device(lin.x)
+    d_dy = to_device(dy)
+    y, saved = L.forward_train(x)
+    dx, grads = L.backward(x, d_dy, saved, want_dx=want_dx)
+    torch.cuda.synchronize()
+    return L, x, d_dy, y, saved, dx, grads
+
+
+def check_against_oracle(oracle, lin, dy, tol=TOL):
+    _, _, _, y, _, dx, grads = run_train(lin, dy)
+    rdx, rout, rmid, rin = oracle.backward(lin.m, lin.n, lin.r, lin.Bu, lin.Bv, lin.s_out,
+                                           lin.s_mid, lin.s_in, lin.x, dy)
+    e = max_row_rel_l2(bf16_bits_to_f64(dx), rdx)
+    eo, em, ei = rel_l2(f32(grads[0]), rout), rel_l2(f32(grads[1]), rmid), rel_l2(f32(grads[2]), rin)
+    print(f"  dx {e:.2e} ds_out {eo:.2e} ds_mid {em:.2e} ds_in {ei:.2e}", flush=True)
+    assert e <= tol and eo <= tol and em <= tol and ei <= tol
+    return y
+
+
+# --------------------------------------------------------------------------
+# packed transpose
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("rows,cols", [(32, 32), (64, 96), (544, 1056), (2016, 4096),
+                                       (4096, 2016), (96, 8224)])
+def test_transpose_bit_exact(oracle, rows, cols):
+    print(f"transpose {rows}x{cols}", flush=True)
+    W = synth.random_words(np.random.default_rng(rows + 3 * cols), rows, cols)
+    want = oracle.transpose_packed(W, cols)
+    d = torch.full((cols, rows // 32), -1, dtype=torch.int32, device="cuda")
+    af1.af1_pack_transpose(to_device(W), rows, cols, d)
+    torch.cuda.synchronize()
+    assert np.array_equal(d.cpu().numpy().view(np.uint32), want)
+
+
+@pytest.mark.parametrize("name", ["sq8192", "mlp_up28672x8192"])
+def test_transpose_full_size_factors(oracle, name):
+    m, n, r = synth.SHAPES[name]
+    print(f"transpose factors of {name}", flush=True)
+    rng = np.random.default_rng(17)
+    for rows, cols in ((m, r), (r, n)):
+        W = synth.random_words(rng, rows, cols)
+        want = oracle.transpose_packed(W, cols)
+        d = torch.empty((cols, rows // 32), dtype=torch.int32, device="cuda")
+        af1.af1_pack_transpose(to_device(W), rows, cols, d)
+        torch.cuda.synchronize()
+        assert np.array_equal(d.cpu().numpy().view(np.uint32), want)
+
+
+def test_transpose_twice_restores():
+    W = synth.random_words(np.random.default_rng(5), 1088, 3072)
+    d = to_device(W)
+    t = torch.empty((3072, 1088 // 32), dtype=torch.int32, device="cuda")
+    back = torch.empty_like(d)
+    af1.af1_pack_transpose(d, 1088, 3072, t)
+    af1.af1_pack_transpose(t, 3072, 1088, back)
+    torch.cuda.synchronize()
+    assert torch.equal(back, d)
+
+
+# --------------------------------------------------------------------------
+# forward with saved intermediates, and the gradients
+# --------------------------------------------------------------------------
+
+SHAPES = [(32, 32, 32, 1), (256, 320, 96, 200), (1056, 2080, 160, 130), (1024, 1024, 480, 300),
+          (4096, 4096, 2016, 65), (2080, 544, 4064, 64)]
+
+
+@pytest.mark.parametrize("m,n,r,T", SHAPES)
+def test_backward_matches_oracle(oracle, m, n, r, T):
+    lin = synth.make_linear(300 + m + n + r + T, m, n, r, T)
+    dy = synth.make_output_grad(900 + T, T, m)
+    check_against_oracle(oracle, lin, dy)
+
+
+def test_forward_train_output_is_the_inference_output():
+    m, n, r, T = 1024, 4096, 800, 257
+    lin = synth.make_linear(41, m, n, r, T)
+    L = DeviceLayer.from_host(lin)
+    x = to_device(lin.x)
+    y_inf = L.gemm(x)
+    y_tr, _ = L.forward_train(x)
+    torch.cuda.synchronize()
+    assert torch.equal(y_inf, y_tr)
+
+
+@pytest.mark.parametrize("name", ["attn4096", "sq8192"])
+def test_backward_full_size_dims(oracle, name):
+    m, n, r = synth.SHAPES[name]
+    lin = synth.make_linear(77, m, n, r, 64)
+    dy = synth.make_output_grad(78, 64, m)
+    check_against_oracle(oracle, lin, dy)
+
+
+def test_backward_rank_above_dimensions(oracle):
+    lin = synth.make_linear(81, 256, 256, 384, 100)
+    dy = synth.make_output_grad(82, 100, 256)
+    check_against_oracle(oracle, lin, dy)
+
+
+def test_backward_tiny_gradients_keep_their_digits(oracle):
+    """Upstream gradients around 2^-30 (far below fp16's range): the bf16
+    operands keep fp32's exponent range, so the relative error bar holds."""
+    lin = synth.make_linear(85, 512, 768, 224, 96)
+    dy = synth.make_output_grad(86, 96, 512, scale=2.0 ** -30)
+    check_against_oracle(oracle, lin, dy)
+
+
+def test_backward_accumulate_skip_dx_and_repeat_are_exact():
+    m, n, r, T = 1024, 1024, 480, 200
+    lin = synth.make_linear(91, m, n, r, T)
+    dy = synth.make_output_grad(92, T, m)
+    L, x, d_dy, _, saved, dx, grads = run_train(lin, dy)
+    dx2, grads2 = L.backward(x, d_dy, saved)                          # repeat
+    _, grads3 = L.backward(x, d_dy, saved, want_dx=False)             # no dx
+    acc = tuple(g.clone() for g in grads)
+    L.backward(x, d_dy, saved, grads=acc, accumulate=True, want_dx=False)
+    torch.cuda.synchronize()
+    assert torch.equal(dx, dx2)
+    for a, b, c, d in zip(grads, grads2, grads3, acc):
+        assert torch.equal(a, b) and torch.equal(a, c)
+        assert torch.equal(d, 2 * a)
+
+
+def test_backward_zero_upstream_gradient():
+    m, n, r, T = 256, 320, 96, 70
+    lin = synth.make_linear(95, m, n, r, T)
+    dy = np.zeros((T, m), np.uint16)
+    _, _, _, _, _, dx, grads = run_train(lin, dy)
+    assert not dx.any()
+    for g in grads:
+        assert not g.any()
+
+
+def test_backward_bench_size_dx_rows_and_token_additivity(oracle):
+    """The benchmark's size, sq8192 at T = 2048: dx rows of sampled tokens
+    against the oracle (a token's dx depends on that token alone), and the
+    scale gradients equal to the sum of those of 64-token chunks (each chunk
+    shape is pinned to the oracle by the tests above)."""
+    m, n, r = synth.SHAPES["sq8192"]
+    T = 2048
+    lin = synth.make_linear(101, m, n, r, T)
+    dy = synth.make_output_grad(102, T, m)
+    L, x, d_dy, _, saved, dx, grads = run_train(lin, dy)
+    rows = [0, 1, 63, 64, 1000, 2047]
+    rdx, _, _, _ = oracle.backward(m, n, r, lin.Bu, lin.Bv, lin.s_out, lin.s_mid, lin.s_in,
+                                   lin.x[rows], dy[rows])
+    assert max_row_rel_l2(bf16_bits_to_f64(dx)[rows], rdx) <= TOL
+    total = [torch.zeros_like(g) for g in grads]
+    chunk = 64
+    ws = torch.empty(af1.af1_train_workspace_bytes(m, n, r, chunk), dtype=torch.uint8,
+                     device="cuda")
+    for c0 in range(0, T, chunk):
+        xs = x[c0:c0 + chunk].contiguous()
+        _, sv = L.forward_train(xs, ws=ws)
+        L.backward(xs, d_dy[c0:c0 + chunk].contiguous(), sv, grads=tuple(total),
+                   accumulate=True, ws=ws, want_dx=False)
+    torch.cuda.synchronize()
+    for g, t in zip(grads, total):
+        assert rel_l2(f32(g), f32(t)) <= 1e-5
