@@ -64,7 +64,7 @@ def parse():
     p.add_argument("--no-decode-table", action="store_true")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
-    p.add_argument("--only", choices=("all", "gemv", "gemm"), default="all",
+    p.add_argument("--only", choices=("all", "gemv", "gemm", "train"), default="all",
                    help="profiling aid: run one part only")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="profiling aid: first run a 64 MiB device copy five times, the "
@@ -279,6 +279,60 @@ def bench_gemm(args, torch, stream):
     return out
 
 
+def bench_train(args, torch, stream):
+    """Scale-only reconstruction step (Sec. 4.1: signs frozen, the three
+    scale vectors trained) on sq8192 at T = 2048: the training forward (y
+    and the saved intermediates) and the backward (dx and the three scale
+    gradients).  Algorithmic flops: 2*T*r*(m+n) per direction."""
+    from paper_2609_06161_amd import af1, synth
+    from paper_2609_06161_amd.layer import DeviceLayer, to_device
+    T = 2048
+    m, n, r = synth.SHAPES["sq8192"]
+    lin = synth.make_linear(57, m, n, r, T)
+    L = DeviceLayer.from_host(lin)
+    x = to_device(lin.x)
+    dy = to_device(synth.make_output_grad(58, T, m))
+    y = torch.empty((T, m), dtype=torch.int16, device="cuda")
+    saved = torch.empty(af1.af1_train_saved_bytes(m, n, r, T), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(af1.af1_train_workspace_bytes(m, n, r, T), dtype=torch.uint8, device="cuda")
+    dx = torch.empty((T, n), dtype=torch.int16, device="cuda")
+    grads = tuple(torch.empty(k, dtype=torch.float32, device="cuda") for k in (m, r, n))
+    # the one-time transposes of the frozen factors
+    BuT = torch.empty((r, m // 32), dtype=torch.int32, device="cuda")
+    BvT = torch.empty((n, r // 32), dtype=torch.int32, device="cuda")
+    ft = lambda i: (af1.af1_pack_transpose(L.Bu, m, r, BuT, stream),
+                    af1.af1_pack_transpose(L.Bv, r, n, BvT, stream))
+    time_events(ft, 3, stream)
+    ms_t = time_events(ft, 20, stream) / 20
+    L._T = (BuT, BvT)
+    fwd = lambda i: L.forward_train(x, y, saved, ws, stream)
+    bwd = lambda i: L.backward(x, dy, saved, dx, grads, False, ws, stream)
+    step = lambda i: (fwd(i), bwd(i))
+    inf = lambda i: L.gemm(x, y, ws, stream)
+    for f in (fwd, bwd, step, inf):
+        time_events(f, 3, stream)
+    ms_f = time_events(fwd, args.gemm_steps, stream) / args.gemm_steps
+    ms_b = time_events(bwd, args.gemm_steps, stream) / args.gemm_steps
+    ms_s = time_events(step, args.gemm_steps, stream) / args.gemm_steps
+    ms_i = time_events(inf, args.gemm_steps, stream) / args.gemm_steps
+    flops = 2.0 * T * r * (m + n)
+    tb = lambda ms, f=flops: round(f / (ms * 1e-3) / 1e12, 1)
+    sign_bytes = 2 * (m * r + r * n) / 8          # read + write, both factors
+    return {"workload": f"scale-only reconstruction step, sq8192 ({m}x{n} r={r}), T={T}",
+            "us_forward_train": round(ms_f * 1e3, 2), "tflops_forward_train": tb(ms_f),
+            "us_forward_inference": round(ms_i * 1e3, 2),
+            "us_backward": round(ms_b * 1e3, 2), "tflops_backward": tb(ms_b),
+            "us_step": round(ms_s * 1e3, 2), "tflops_step": tb(ms_s, 2 * flops),
+            "tokens_per_s_step": round(T / (ms_s * 1e-3), 0),
+            "us_transpose_both_factors": round(ms_t * 1e3, 2),
+            "transpose_gbs": round(sign_bytes / (ms_t * 1e-3) / 1e9, 1),
+            "roofline_backward": {"bound": "mfma", "achieved": tb(ms_b),
+                                  "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                  "frac": round(flops / (ms_b * 1e-3) / 1e12
+                                                / MFMA_F16_PEAK_TFLOPS, 4),
+                                  "traffic": None}}
+
+
 def bench_pack(args, torch, stream):
     """Sign -> bit packing of a 16384 x 16384 matrix from each source type:
     HBM-bound, algorithmic bytes = source bytes + packed bytes."""
@@ -352,6 +406,9 @@ def main():
         out = bench_gemm(args, torch, stream)
         print(json.dumps({"gemm": out}), flush=True)
         return
+    if args.only == "train":
+        print(json.dumps({"train": bench_train(args, torch, stream)}), flush=True)
+        return
 
     from paper_2609_06161_amd import synth
     m, n, r = synth.SHAPES["attn4096"]
@@ -391,6 +448,7 @@ def main():
     if not args.no_gemm and args.only == "all":
         result["gemm"] = bench_gemm(args, torch, stream)
         result["gemm"]["peak_tflops"] = MFMA_F16_PEAK_TFLOPS
+        result["train"] = bench_train(args, torch, stream)
     if not args.no_cpu_baseline and args.only == "all":
         result["cpu_baseline"] = bench_cpu_oracle(args)
     print(json.dumps(result), flush=True)

@@ -369,26 +369,43 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
 
   // Epilogue.  32x32 accumulator layout: lane l holds column (l mod 32) and
   // rows 8*(e/4) + 4*(l/32) + (e mod 4), e = 0..15.
+  if constexpr (kMode == kBwdMid || kMode == kBwdIn) {
+    // The S block of this tile (kBM tokens x 256 weight rows, 512 bytes a
+    // token) goes into the idle activation buffers with LDS copies, two
+    // token rows per copy instruction; a row's 16-byte chunk c lands at
+    // position c XOR 4 * ((row / 4) mod 2), so the two lane halves below
+    // (tokens four apart) read distinct banks.  Tokens past T read zeros.
+    constexpr int kSCopies = kBM / 8;  // per wave
+    const i32x4 srs = copy_rsrc(S, (int64_t)T * N * 2);
+#pragma unroll
+    for (int jj = 0; jj < kSCopies; ++jj) {
+      const int row = 2 * (kSCopies * wave + jj) + (lane >> 5);
+      const int chunk = (lane & 31) ^ (((row >> 2) & 1) << 2);
+      const int off = t0 + row < T ? (t0 + row) * N * 2 + n0 * 2 + 16 * chunk : kOob;
+      copy16(srs, lds + (kSCopies * wave + jj) * 1024, off);
+    }
+    wait_copies();
+    __syncthreads();
+  }
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int n = wrow0 + 32 * j;
     if constexpr (kMode == kBwdMid || kMode == kBwdIn) {
       // Token sum of acc * S over this tile for weight row n: the lane's
       // sixteen tokens per block, then its partner half (lane XOR 32).
+      // Tokens past T have zero accumulators and zero S.
+      const int lpos = (kMode == kBwdMid ? pair_pos(n) : n) - n0;
+      const int cbyte = 2 * (lpos & 7);
       float part = 0.f;
-      if (n < N) {
-        const int spos = kMode == kBwdMid ? pair_pos(n) : n;
 #pragma unroll
-        for (int i = 0; i < kTokBlocks; ++i)
+      for (int i = 0; i < kTokBlocks; ++i)
 #pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int t = t0 + 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
-            if (t < T) {
-              const uint16_t sv = S[(size_t)t * N + spos];
-              part += acc[i][j][e] * (kMode == kBwdMid ? f16_to_f32(sv) : bf16_to_f32(sv));
-            }
-          }
-      }
+        for (int e = 0; e < 16; ++e) {
+          const int row = 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
+          const int pos = ((lpos >> 3) ^ (((row >> 2) & 1) << 2)) * 16 + cbyte;
+          const uint16_t sv = *reinterpret_cast<const uint16_t *>(lds + row * 512 + pos);
+          part += acc[i][j][e] * (kMode == kBwdMid ? f16_to_f32(sv) : bf16_to_f32(sv));
+        }
       part += __shfl_xor(part, 32, 64);
       if (g == 0 && n < N) F[(size_t)(t0 / kBM) * N + n] = part;
     }
@@ -492,29 +509,50 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const uint16_t *__restric
 }
 
 // ds[c] = (accumulate ? ds[c] : 0) + sum over tiles of part[tile][c], for
-// the three scale gradients in one launch (tile sums in a fixed order).
+// the three scale gradients in one launch.  A block takes 64 columns; wave
+// w adds tiles w, w+4, w+8, ... in order (all its loads in flight at
+// once), and wave 0 adds the four wave sums in order, so the result does
+// not depend on timing.
+constexpr int kFinishCols = 64;
 __global__ __launch_bounds__(256) void bwd_finish_kernel(
     const float *__restrict__ p_out, int n_out_tiles, float *__restrict__ ds_out, int m,
     const float *__restrict__ p_mid, int n_mid_tiles, float *__restrict__ ds_mid, int r,
     const float *__restrict__ p_in, int n_in_tiles, float *__restrict__ ds_in, int n,
     int accumulate) {
-  int idx = blockIdx.x * 256 + threadIdx.x;
-  const float *p;
-  float *ds;
-  int tiles, len;
+  __shared__ float quarter[4][kFinishCols];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int idx = blockIdx.x * kFinishCols + lane;
+  const float *p = nullptr;
+  float *ds = nullptr;
+  int tiles = 0, len = 0;
   if (idx < m) {
     p = p_out; ds = ds_out; tiles = n_out_tiles; len = m;
   } else if ((idx -= m) < r) {
     p = p_mid; ds = ds_mid; tiles = n_mid_tiles; len = r;
   } else if ((idx -= r) < n) {
     p = p_in; ds = ds_in; tiles = n_in_tiles; len = n;
-  } else {
-    return;
   }
-  float sum = accumulate ? ds[idx] : 0.f;
-  float tot = 0.f;
-  for (int k = 0; k < tiles; ++k) tot += p[(size_t)k * len + idx];
-  ds[idx] = sum + tot;
+  float tot = 0.f, old = 0.f;
+  if (p) {
+    if (wave == 0 && accumulate) old = ds[idx];
+    // Unconditional loads (indices clamped into the array, surplus values
+    // dropped afterwards), so all sixteen are in flight together.
+    float v[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int k = wave + 4 * q;
+      v[q] = p[(size_t)(k < tiles ? k : tiles - 1) * len + idx];
+    }
+#pragma unroll
+    for (int q = 0; q < 16; ++q) tot += wave + 4 * q < tiles ? v[q] : 0.f;
+    for (int k = wave + 64; k < tiles; k += 4) tot += p[(size_t)k * len + idx];
+  }
+  quarter[wave][lane] = tot;
+  __syncthreads();
+  if (wave == 0 && p) {
+    const float s4 = ((quarter[0][lane] + quarter[1][lane]) + quarter[2][lane]) + quarter[3][lane];
+    ds[idx] = old + s4;
+  }
 }
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
@@ -692,7 +730,7 @@ hipError_t launch_backward(int64_t m, int64_t n, int64_t r, const uint32_t *BuT,
   e = contraction<kBwdIn>(w.Zb, T, r, BvT, n, nullptr, s_in, dx, x, w.p_in, s, &ti);
   if (e != hipSuccess) return e;
   const int total = (int)(m + r + n);
-  bwd_finish_kernel<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(
+  bwd_finish_kernel<<<(unsigned)((total + kFinishCols - 1) / kFinishCols), 256, 0, s>>>(
       w.p_out, (int)tiles64(T), ds_out, (int)m, w.p_mid, (int)((T + tm - 1) / tm), ds_mid,
       (int)r, w.p_in, (int)((T + ti - 1) / ti), ds_in, (int)n, accumulate);
   return hipGetLastError();
