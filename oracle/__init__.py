@@ -17,6 +17,10 @@ source, the passage of the paper it follows:
 - ``transpose_packed``: the packed storage of a sign matrix's transpose.
 - ``backward``: the gradients of the scale-only reconstruction of Sec. 4.1
   (sign matrices frozen) with respect to s_out, s_mid, s_in and x.
+
+The NABF building blocks (surrogate, SVID, null-space projector, ADMM
+proxies, scale fits, one iteration of Algorithm nabf) are in ``nabf.py``,
+fp64 numpy.
 """
 import ctypes
 import os
