@@ -1,4 +1,5 @@
-"""Build ``libaf1.so`` (HIP kernels + C ABI) for gfx950 with hipcc.
+"""Build ``libaf1.so`` (HIP kernels + C ABI) and ``libaf1_nabf.so`` (the NABF
+building blocks) for gfx950 with hipcc.
 
 Every call recompiles.  Objects go to ``_build/`` beside this file; the
 shared library lands in the package directory, where the binding loads it.
@@ -13,6 +14,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libaf1.so")
+NABF_LIB = os.path.join(HERE, "libaf1_nabf.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
@@ -40,16 +42,27 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
-    with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), srcs))
-    cmd = [HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", LIB + ".tmp", *objs]
+def _link(out: str, objs, libs, verbose: bool) -> None:
+    cmd = [HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", out + ".tmp", *objs, *libs]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(LIB + ".tmp", LIB)
+    os.replace(out + ".tmp", out)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every source; link libaf1.so (the layer) and libaf1_nabf.so
+    (the offline NABF building blocks, which also need rocBLAS and rocSOLVER
+    and reuse the sign-packing kernel).  Returns the path of libaf1.so."""
+    os.makedirs(BUILD, exist_ok=True)
+    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+    with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+        objs = dict(zip(srcs, ex.map(lambda s: _compile(s, verbose), srcs)))
+    nabf_src = os.path.join(CSRC, "af1_nabf.hip")
+    pack_src = os.path.join(CSRC, "af1_pack.hip")
+    _link(LIB, [o for s, o in objs.items() if s != nabf_src], [], verbose)
+    _link(NABF_LIB, [objs[nabf_src], objs[pack_src]],
+          ["-L/opt/rocm/lib", "-lrocsolver", "-lrocblas"], verbose)
     return LIB
 
 
