@@ -64,7 +64,7 @@ def parse():
     p.add_argument("--no-decode-table", action="store_true")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0)
-    p.add_argument("--only", choices=("all", "gemv", "gemm", "train"), default="all",
+    p.add_argument("--only", choices=("all", "gemv", "gemm", "train", "nabf"), default="all",
                    help="profiling aid: run one part only")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="profiling aid: first run a 64 MiB device copy five times, the "
@@ -333,6 +333,119 @@ def bench_train(args, torch, stream):
                                   "traffic": None}}
 
 
+def bench_nabf(args, torch, stream):
+    """One iteration of the NABF loop (Algorithm nabf) on a synthetic
+    surrogate W' = A* B* + noise, and its building blocks, at 4096x4096,
+    r = 2016 (fp32 products on rocBLAS, fp64 eigenproblems on rocSOLVER),
+    plus the fp64 oracle's iteration at 1024x1024, r = 480 on the host."""
+    import numpy as np
+    from paper_2609_06161_amd import af1, nabf
+    from paper_2609_06161_amd.layer import to_device
+    out = {}
+
+    def state(m, n, r, seed):
+        g = torch.Generator(device="cuda")
+        g.manual_seed(seed)
+        rn = lambda *sh, s=1.0: torch.randn(*sh, device="cuda", generator=g) * s
+        As, Bs = rn(m, r, s=0.2), rn(r, n, s=0.2)
+        Wp = (As @ Bs + 0.03 * rn(m, n)).contiguous()
+        D = dict(A=(As + rn(m, r, s=0.05)).contiguous(), B=(Bs + rn(r, n, s=0.05)).contiguous(),
+                 UA=torch.zeros(m, r, device="cuda"), UB=torch.zeros(r, n, device="cuda"),
+                 A_bits=torch.empty(m, r // 32, dtype=torch.int32, device="cuda"),
+                 B_bits=torch.empty(r, n // 32, dtype=torch.int32, device="cuda"),
+                 a=torch.empty(m, device="cuda"), m1=torch.empty(r, device="cuda"),
+                 m2=torch.empty(r, device="cuda"), b=torch.empty(n, device="cuda"))
+        return Wp, D
+
+    m = n = 4096
+    r = 2016
+    Wp, D = state(m, n, r, 5)
+    ws = torch.empty(nabf.af1_nabf_workspace_bytes(m, n, r), dtype=torch.uint8, device="cuda")
+    nb = ws.numel()
+    # the start: SVID of the perturbed factors, as the loop's initialisation
+    nabf.af1_svid(D["A"], m, r, 30, D["A_bits"], D["a"], D["m1"], ws, nb, stream)
+    nabf.af1_svid(D["B"], r, n, 30, D["B_bits"], D["m2"], D["b"], ws, nb, stream)
+    out_m_r = torch.empty(m, r, device="cuda")
+    C = (D["B"] @ D["B"].T).contiguous()
+    P = torch.empty(r, r, device="cuda")
+    fit = torch.empty(r, device="cuda")
+    legs = {
+        "admm_left": lambda i: nabf.af1_admm_proxy(0, Wp, m, n, r, D["A"], D["B"], D["UA"], 0.5,
+                                                   out_m_r, ws, nb, stream),
+        "svid_30_passes_4096x2016": lambda i: nabf.af1_svid(out_m_r, m, r, 30, D["A_bits"],
+                                                            D["a"], D["m1"], ws, nb, stream),
+        "nullspace_projector_r2016": lambda i: nabf.af1_nullspace_projector(C, r, 0.01, P, None,
+                                                                            ws, nb, stream),
+        "scale_fit_left": lambda i: nabf.af1_scale_fit(0, out_m_r, D["A_bits"], D["a"], D["m1"],
+                                                       m, r, P, fit, ws, nb, stream),
+    }
+    for name, fn in legs.items():
+        time_events(fn, 1, stream)
+        out[f"ms_{name}"] = round(time_events(fn, 3, stream) / 3, 3)
+    # rebuild a consistent state, then time whole iterations
+    Wp, D = state(m, n, r, 5)
+    nabf.af1_svid(D["A"], m, r, 30, D["A_bits"], D["a"], D["m1"], ws, nb, stream)
+    nabf.af1_svid(D["B"], r, n, 30, D["B_bits"], D["m2"], D["b"], ws, nb, stream)
+    st = nabf.make_state(m, n, r, D["A"], D["B"], D["UA"], D["UB"], D["A_bits"], D["B_bits"],
+                         D["a"], D["m1"], D["m2"], D["b"])
+    # dense factors equal to their binary-scaled forms (set-up, not timed)
+    for key, bits, left, right, rows, cols in (("A", "A_bits", "a", "m1", m, r),
+                                               ("B", "B_bits", "m2", "b", r, n)):
+        signs = torch.empty(rows, cols, dtype=torch.int8, device="cuda")
+        af1.af1_unpack(D[bits], rows, cols, signs, stream)
+        D[key].copy_(D[left][:, None] * signs.float() * D[right][None, :])
+
+    def recon():
+        torch.cuda.synchronize()
+        A, B, W = D["A"].double(), D["B"].double(), Wp.double()
+        return float(torch.linalg.norm(W - A @ B) / torch.linalg.norm(W))
+    err0 = recon()
+    it = lambda i: nabf.af1_nabf_iteration(Wp, st, 0.5, 0.01, 30, ws, nb, stream)
+    time_events(it, 1, stream)
+    ms = time_events(it, 3, stream) / 3
+    out["workload"] = (f"NABF iteration (both factors) on a synthetic surrogate {m}x{n}, r={r}: "
+                       "W' = A*B* + noise, start from SVID of perturbed factors; rho=0.5, "
+                       "eta=0.01, 30 power-iteration passes")
+    out["ms_iteration"] = round(ms, 2)
+    out["relative_error_start"] = round(err0, 4)
+    out["relative_error_after_4_iterations"] = round(recon(), 4)
+    # left: B B^T, W' B^T, the Cholesky solve, E P; right: A^T A, A^T W', the
+    # two triangular solves, P E
+    fp32 = (2 * r * r * n + 2 * m * n * r + 2 * r * r * m + 2 * m * r * r) \
+        + (2 * r * r * m + 2 * m * n * r + 2 * r * r * n + 2 * r * r * n)
+    out["fp32_gflop_per_iteration_products"] = round(fp32 / 1e9, 1)
+    out["fp64_gflop_per_iteration_projectors"] = round(2 * 2 * r ** 3 / 1e9, 1)
+    del Wp, D, ws, C, P, out_m_r
+    # the oracle's iteration on the host, at a smaller shape
+    if not args.no_cpu_baseline:
+        import time
+        from oracle import nabf as onabf
+        mm = nn = 1024
+        rr = 480
+        rng = np.random.default_rng(9)
+        As, Bs = rng.standard_normal((mm, rr)) * 0.2, rng.standard_normal((rr, nn)) * 0.2
+        Wph = As @ Bs + 0.03 * rng.standard_normal((mm, nn))
+        Ab, a, m1 = onabf.svid((As + 0.05 * rng.standard_normal((mm, rr))).astype(np.float32), 30)
+        Bb, m2, b = onabf.svid((Bs + 0.05 * rng.standard_normal((rr, nn))).astype(np.float32), 30)
+        S = dict(A_bits=Ab, B_bits=Bb, a=a, m1=m1, m2=m2, b=b,
+                 A=onabf.binary_scaled(Ab, a, m1, rr), B=onabf.binary_scaled(Bb, m2, b, nn),
+                 UA=np.zeros((mm, rr)), UB=np.zeros((rr, nn)))
+        t0 = time.perf_counter()
+        onabf.nabf_iteration(Wph, S, 0.5, 0.01, 30)
+        out["cpu_oracle_ms_iteration_1024x1024_r480"] = round((time.perf_counter() - t0) * 1e3, 1)
+        Wg = to_device(Wph.astype(np.float32))
+        Dg = {k: to_device(np.ascontiguousarray(v.astype(np.float32) if v.dtype == np.float64
+                                                else v)) for k, v in S.items()}
+        wsg = torch.empty(nabf.af1_nabf_workspace_bytes(mm, nn, rr), dtype=torch.uint8,
+                          device="cuda")
+        stg = nabf.make_state(mm, nn, rr, Dg["A"], Dg["B"], Dg["UA"], Dg["UB"], Dg["A_bits"],
+                              Dg["B_bits"], Dg["a"], Dg["m1"], Dg["m2"], Dg["b"])
+        itg = lambda i: nabf.af1_nabf_iteration(Wg, stg, 0.5, 0.01, 30, wsg, wsg.numel(), stream)
+        time_events(itg, 1, stream)
+        out["gpu_ms_iteration_1024x1024_r480"] = round(time_events(itg, 3, stream) / 3, 2)
+    return out
+
+
 def bench_pack(args, torch, stream):
     """Sign -> bit packing of a 16384 x 16384 matrix from each source type:
     HBM-bound, algorithmic bytes = source bytes + packed bytes."""
@@ -408,6 +521,9 @@ def main():
         return
     if args.only == "train":
         print(json.dumps({"train": bench_train(args, torch, stream)}), flush=True)
+        return
+    if args.only == "nabf":
+        print(json.dumps({"nabf": bench_nabf(args, torch, stream)}), flush=True)
         return
 
     from paper_2609_06161_amd import synth

@@ -27,9 +27,9 @@
  *   through that handle.  Calls on one device are serialised on the host
  *   while they enqueue work.  Unlike af1.h, these entry points are an
  *   offline path: they may synchronise internally where rocSOLVER does.
- * Workspace: every call takes a device workspace of at least
- *   af1_nabf_workspace_bytes(m, n, r, T) bytes for the shapes involved
- *   (one query covers every entry point).
+ * Workspace: every call takes a device workspace; af1_nabf_workspace_bytes
+ *   (m, n, r, T) bytes cover every entry point for a layer of those
+ *   dimensions (af1_svid of its m x r or r x n factor included).
  * Errors: as in af1.h (argument errors before any work, AF1_ERR_HIP when
  *   HIP, rocBLAS or rocSOLVER reject a call).
  */

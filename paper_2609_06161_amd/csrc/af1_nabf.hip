@@ -320,6 +320,19 @@ __global__ __launch_bounds__(256) void rowfit_kernel(const float *__restrict__ h
     fit[k] = (((rn[0] + rn[1]) + rn[2]) + rn[3]) / ((((rd[0] + rd[1]) + rd[2]) + rd[3]) + eps);
 }
 
+// X[i + j * ld] /= (D[j or i] + rho): dim 0 scales the rows of a
+// column-major block (index i), dim 1 its columns (index j).
+__global__ __launch_bounds__(256) void inv_shift_scale_kernel(float *__restrict__ X, int64_t rows,
+                                                              int64_t cols,
+                                                              const double *__restrict__ D,
+                                                              float rho, int dim) {
+  const int64_t n = rows * cols;
+  for (int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x; k < n; k += (int64_t)gridDim.x * 256) {
+    const int64_t e = dim == 0 ? k % rows : k / rows;
+    X[k] = (float)((double)X[k] / (D[e] + (double)rho));
+  }
+}
+
 __global__ __launch_bounds__(256) void mul_kernel(float *__restrict__ x, const float *__restrict__ y,
                                                   int n) {
   const int j = blockIdx.x * 256 + threadIdx.x;
@@ -459,6 +472,24 @@ size_t ws_layout(int64_t m, int64_t n, int64_t r, int64_t T, uint8_t *base, Ws *
   return off;
 }
 
+// The scratch of a stand-alone SVID of a rows x cols matrix (the power
+// iteration's partial sums), laid out from the start of the workspace; it
+// never exceeds the layout above for a layer that has such a factor.
+size_t svid_layout(int64_t rows, int64_t cols, uint8_t *base, Ws *w) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    uint8_t *p = base ? base + off : nullptr;
+    off += al(bytes);
+    return p;
+  };
+  Ws t{};
+  t.svid_part = (float *)take((size_t)chunks_of(rows) * cols * 4);
+  t.svid_w = (float *)take((size_t)cols * 4);
+  t.svid_sq = (float *)take((size_t)blocks_for(cols) * 4);
+  if (w) *w = t;
+  return off;
+}
+
 // ---- building blocks (arguments already validated) ------------------------
 
 af1_status run_svid(const float *Z, int64_t rows, int64_t cols, int iters, uint32_t *bits,
@@ -486,13 +517,21 @@ af1_status run_svid(const float *Z, int64_t rows, int64_t cols, int iters, uint3
   return AF1_OK;
 }
 
-af1_status run_projector(rocblas_handle h, const float *C, int64_t r, float eta, float *P,
-                         int *k_out, const Ws &w, hipStream_t s) {
+// C = U diag(D) U^T in fp64 (U column-major in w.c64, D ascending in w.d).
+af1_status run_eig(rocblas_handle h, const float *C, int64_t r, const Ws &w, hipStream_t s) {
   const int64_t rr = r * r;
   to_f64_kernel<<<grid_cap(rr), 256, 0, s>>>(C, w.c64, rr);
   CHECK_LAUNCH();
   CHECK_RB(rocsolver_dsyevd(h, rocblas_evect_original, rocblas_fill_upper, (rocblas_int)r, w.c64,
                             (rocblas_int)r, w.d, w.e64, w.info));
+  return AF1_OK;
+}
+
+// P from the decomposition in w.c64 / w.d (the eigenvectors are masked in
+// place, so any other use of them comes first).
+af1_status projector_from_eig(rocblas_handle h, int64_t r, float eta, float *P, int *k_out,
+                              const Ws &w, hipStream_t s) {
+  const int64_t rr = r * r;
   cutoff_kernel<<<1, 64, 0, s>>>(w.d, (int)r, (double)eta, kEps, w.pre, w.count, k_out);
   CHECK_LAUNCH();
   mask_columns_kernel<<<grid_cap(rr), 256, 0, s>>>(w.c64, (int)r, w.count);
@@ -503,6 +542,13 @@ af1_status run_projector(rocblas_handle h, const float *C, int64_t r, float eta,
   to_f32_kernel<<<grid_cap(rr), 256, 0, s>>>(w.p64, P, rr);
   CHECK_LAUNCH();
   return AF1_OK;
+}
+
+af1_status run_projector(rocblas_handle h, const float *C, int64_t r, float eta, float *P,
+                         int *k_out, const Ws &w, hipStream_t s) {
+  af1_status st = run_eig(h, C, r, w, s);
+  if (st != AF1_OK) return st;
+  return projector_from_eig(h, r, eta, P, k_out, w, s);
 }
 
 // Left proxy into out (m x r).  The Gram matrix B B^T is left in w.c.
@@ -583,17 +629,54 @@ af1_status run_fit(rocblas_handle h, int side, const float *hat, const uint32_t 
   return AF1_OK;
 }
 
+// The proxies of one iteration, solved with the eigendecomposition of the
+// Gram matrix that the null-space projector needs anyway:
+// (C + rho I)^-1 = U diag(1 / (D + rho)) U^T.  w.c holds C on entry; on
+// exit w.c64 / w.d hold its decomposition and w.g the fp32 eigenvectors.
+af1_status proxy_by_eig(rocblas_handle h, int side, const float *Wp, int64_t m, int64_t n,
+                        int64_t r, const float *A, const float *B, const float *U, float rho,
+                        float *out, const Ws &w, hipStream_t s) {
+  af1_status st = run_eig(h, w.c, r, w, s);
+  if (st != AF1_OK) return st;
+  to_f32_kernel<<<grid_cap(r * r), 256, 0, s>>>(w.c64, w.g, r * r);
+  CHECK_LAUNCH();
+  if (side == 0) {
+    scaled_diff_kernel<<<grid_cap(m * r), 256, 0, s>>>(A, U, rho, out, m * r);
+    CHECK_LAUNCH();
+    st = sgemm(h, kT, kN, r, m, n, B, n, Wp, n, 1.f, out, r);   // R^T += B W'^T
+    if (st != AF1_OK) return st;
+    // X^T = U diag U^T R^T (column-major r x m)
+    st = sgemm(h, kT, kN, r, m, r, w.g, r, out, r, 0.f, w.ep, r);
+    if (st != AF1_OK) return st;
+    inv_shift_scale_kernel<<<grid_cap(m * r), 256, 0, s>>>(w.ep, r, m, w.d, rho, 0);
+    CHECK_LAUNCH();
+    return sgemm(h, kN, kN, r, m, r, w.g, r, w.ep, r, 0.f, out, r);
+  }
+  scaled_diff_kernel<<<grid_cap(r * n), 256, 0, s>>>(B, U, rho, out, r * n);
+  CHECK_LAUNCH();
+  st = sgemm(h, kN, kT, n, r, m, Wp, n, A, r, 1.f, out, n);      // R^T += W'^T A
+  if (st != AF1_OK) return st;
+  // X^T = R^T U diag U^T (column-major n x r)
+  st = sgemm(h, kN, kN, n, r, r, out, n, w.g, r, 0.f, w.ep, n);
+  if (st != AF1_OK) return st;
+  inv_shift_scale_kernel<<<grid_cap(n * r), 256, 0, s>>>(w.ep, n, r, w.d, rho, 1);
+  CHECK_LAUNCH();
+  return sgemm(h, kN, kT, n, r, r, w.ep, n, w.g, r, 0.f, out, n);
+}
+
 af1_status run_iteration(rocblas_handle h, const float *Wp, const af1_nabf_state *S, float rho,
                          float eta, int iters, const Ws &w, hipStream_t s) {
   const int64_t m = S->m, n = S->n, r = S->r;
-  // left-factor update
-  af1_status st = run_admm_left(h, Wp, m, n, r, S->A, S->B, S->UA, rho, w.hat_a, w, s);
+  // left-factor update: C_B = B B^T gives both the proxy's solve and P_B
+  af1_status st = sgemm(h, kT, kN, r, r, n, S->B, n, S->B, n, 0.f, w.c, r);
+  if (st != AF1_OK) return st;
+  st = proxy_by_eig(h, 0, Wp, m, n, r, S->A, S->B, S->UA, rho, w.hat_a, w, s);
   if (st != AF1_OK) return st;
   add_kernel<<<grid_cap(m * r), 256, 0, s>>>(w.hat_a, S->UA, w.z, m * r);
   CHECK_LAUNCH();
   st = run_svid(w.z, m, r, iters, S->A_bits, S->a, S->m1, w, s);
   if (st != AF1_OK) return st;
-  st = run_projector(h, w.c, r, eta, w.p, nullptr, w, s);   // null space of B B^T
+  st = projector_from_eig(h, r, eta, w.p, nullptr, w, s);   // null space of B B^T
   if (st != AF1_OK) return st;
   st = run_fit(h, 0, w.hat_a, S->A_bits, S->a, S->m1, m, r, w.p, w.fit, w, s);
   if (st != AF1_OK) return st;
@@ -602,14 +685,16 @@ af1_status run_iteration(rocblas_handle h, const float *Wp, const af1_nabf_state
   rebuild_kernel<<<dim3(blocks_for(r), rows_grid(m)), 256, 0, s>>>(S->A_bits, S->a, S->m1, m,
                                                                    (int)r, w.hat_a, S->A, S->UA);
   CHECK_LAUNCH();
-  // right-factor update, with the new left factor
-  st = run_admm_right(h, Wp, m, n, r, S->A, S->B, S->UB, rho, w.hat_b, w, s);
+  // right-factor update with the new left factor: C_A = A^T A
+  st = sgemm(h, kN, kT, r, r, m, S->A, r, S->A, r, 0.f, w.c, r);
+  if (st != AF1_OK) return st;
+  st = proxy_by_eig(h, 1, Wp, m, n, r, S->A, S->B, S->UB, rho, w.hat_b, w, s);
   if (st != AF1_OK) return st;
   add_kernel<<<grid_cap(r * n), 256, 0, s>>>(w.hat_b, S->UB, w.z, r * n);
   CHECK_LAUNCH();
   st = run_svid(w.z, r, n, iters, S->B_bits, S->m2, S->b, w, s);
   if (st != AF1_OK) return st;
-  st = run_projector(h, w.c, r, eta, w.p, nullptr, w, s);   // null space of A^T A
+  st = projector_from_eig(h, r, eta, w.p, nullptr, w, s);   // null space of A^T A
   if (st != AF1_OK) return st;
   st = run_fit(h, 1, w.hat_b, S->B_bits, S->m2, S->b, r, n, w.p, w.fit, w, s);
   if (st != AF1_OK) return st;
@@ -695,9 +780,7 @@ af1_status af1_svid(const float *Z, int64_t rows, int64_t cols, int32_t iters, u
     return AF1_ERR_SHAPE;
   if (!a16(Z) || !a16(bits) || !a16(left) || !a16(right) || (ws && !a16(ws))) return AF1_ERR_ALIGN;
   Ws w;
-  // the SVID scratch of a rows x cols matrix fits the layout of m = rows,
-  // n = r = cols
-  const size_t need = ws_layout(rows, cols, cols, 0, static_cast<uint8_t *>(ws), &w);
+  const size_t need = svid_layout(rows, cols, static_cast<uint8_t *>(ws), &w);
   if (!ws || ws_bytes < need) return AF1_ERR_WORKSPACE;
   return run_svid(Z, rows, cols, iters, bits, left, right, w, as_stream(stream));
 }

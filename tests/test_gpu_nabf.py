@@ -197,19 +197,25 @@ def test_iteration_matches_oracle(m, n, r):
     torch.cuda.synchronize()
     S64 = {k: (v.astype(np.float64) if v.dtype == np.float32 else v) for k, v in S.items()}
     T = onabf.nabf_iteration(Wp.astype(np.float64), S64, rho, eta, iters)
-    # signs of A_hat + UA, compared where clearly away from zero
-    z = T["Ahat"] + S64["UA"]
-    clear = np.abs(z) > 1e-4 * np.sqrt(np.mean(z * z))
-    got = oracle.unpack(D["A_bits"].cpu().numpy().view(np.uint32), r)
-    want = oracle.unpack(T["A_bits"], r)
-    assert np.array_equal(got[clear], want[clear])
-    z = T["Bhat"] + S64["UB"]
-    clear = np.abs(z) > 1e-4 * np.sqrt(np.mean(z * z))
-    got = oracle.unpack(D["B_bits"].cpu().numpy().view(np.uint32), n)
-    want = oracle.unpack(T["B_bits"], n)
-    assert np.array_equal(got[clear], want[clear])
-    for key in ("a", "m1", "m2", "b", "A", "B", "UA", "UB"):
+    # signs of A_hat + UA (and B_hat + UB): equal wherever the value is clear
+    # of zero; the dense factors and duals are compared where the two sides
+    # took the same sign decision (a flip near zero is a different but valid
+    # rounding of the same projection)
+    agree = {}
+    for bits, hat, U, cols, key in (("A_bits", "Ahat", "UA", r, "A"), ("B_bits", "Bhat", "UB", n, "B")):
+        z = T[hat] + S64[U]
+        clear = np.abs(z) > 1e-4 * np.sqrt(np.mean(z * z))
+        got = oracle.unpack(D[bits].cpu().numpy().view(np.uint32), cols)
+        want = oracle.unpack(T[bits], cols)
+        assert np.array_equal(got[clear], want[clear])
+        agree[key] = got == want
+        print(f"  {key}: {int((~agree[key]).sum())} sign(s) differ near zero", flush=True)
+    for key in ("a", "m1", "m2", "b"):
         e = rel(host(D[key]), T[key])
+        print(f"  {key}: {e:.2e}", flush=True)
+        assert e < 2e-3, key
+    for key, mask in (("A", agree["A"]), ("UA", agree["A"]), ("B", agree["B"]), ("UB", agree["B"])):
+        e = rel(host(D[key])[mask], T[key][mask])
         print(f"  {key}: {e:.2e}", flush=True)
         assert e < 2e-3, key
 
