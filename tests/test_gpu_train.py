@@ -202,3 +202,45 @@ def test_backward_bench_size_dx_rows_and_token_additivity(oracle):
     torch.cuda.synchronize()
     for g, t in zip(grads, total):
         assert rel_l2(f32(g), f32(t)) <= 1e-5
+
+
+def test_training_step_replays_in_a_hip_graph():
+    """Training forward + backward captured once and replayed several times,
+    with eager work and synchronisation between replays: every replay equals
+    the eager result bit for bit (the path issues no memsets)."""
+    m, n, r, T = 1024, 1024, 480, 256
+    lin = synth.make_linear(121, m, n, r, T)
+    dy = synth.make_output_grad(122, T, m)
+    L = DeviceLayer.from_host(lin)
+    x, d_dy = to_device(lin.x), to_device(dy)
+    L.transposed()
+    y = torch.empty((T, m), dtype=torch.int16, device="cuda")
+    saved = torch.empty(af1.af1_train_saved_bytes(m, n, r, T), dtype=torch.uint8, device="cuda")
+    ws = torch.empty(af1.af1_train_workspace_bytes(m, n, r, T), dtype=torch.uint8, device="cuda")
+    dx = torch.empty((T, n), dtype=torch.int16, device="cuda")
+    grads = tuple(torch.empty(k, dtype=torch.float32, device="cuda") for k in (m, r, n))
+
+    def step(stream):
+        L.forward_train(x, y, saved, ws, stream)
+        L.backward(x, d_dy, saved, dx, grads, False, ws, stream)
+
+    step(None)
+    torch.cuda.synchronize()
+    ref = [t.clone() for t in (y, dx) + grads]
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        step(s)                       # warm up on the capture stream
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        step(s)
+    for rep in range(4):
+        for t in (y, dx) + grads:
+            t.fill_(7)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for got, want in zip((y, dx) + grads, ref):
+            assert torch.equal(got, want), rep
+        step(None)                    # eager work between replays
+        torch.cuda.synchronize()
