@@ -246,12 +246,16 @@ AF1_API af1_status af1_pack_transpose(const uint32_t *src, int64_t rows, int64_t
  *           call's sums to their contents (gradient accumulation over
  *           micro-batches).
  *   ws    : device, at least af1_train_workspace_bytes(m, n, r, T) bytes.
- * Arithmetic: both products run on bf16 MFMA with fp32 accumulation (bf16
- * keeps the range of fp32, so small gradients do not underflow): s_out .* dy
- * and s_mid .* dt are rounded once to bf16 and multiplied by exact +-1
- * operands; the token sums are taken in fp32 from the fp32 accumulators,
- * per tile and then over tiles in a fixed order, so results are
- * deterministic (bit-identical from run to run).
+ * Arithmetic: both products run on fp16 MFMA with fp32 accumulation against
+ * exact +-1 operands.  Their A operands, s_out .* dy and s_mid .* dt, carry
+ * a power-of-two scale per group of 64 tokens, chosen from the group's
+ * largest entry and a bound on the first product's outputs.  So each
+ * operand is rounded once to fp16 (2^-12 relative) with no overflow, and
+ * the fp16 range limits nothing: gradients far below 2^-24 keep their
+ * digits.  The scales are exact powers of two and are undone in fp32.  dx
+ * is rounded to bfloat16.  The token sums are taken in fp32 from the
+ * accumulators, per tile and then over tiles in a fixed order, so results
+ * are bit-identical from run to run.
  * Errors: AF1_ERR_NULL for a NULL L, BuT, BvT, scale, x, dy, saved or ds_*;
  * AF1_ERR_SHAPE / AF1_ERR_BATCH / AF1_ERR_ALIGN as for the forward;
  * AF1_ERR_WORKSPACE for a short saved or ws; AF1_ERR_ALIAS when an output

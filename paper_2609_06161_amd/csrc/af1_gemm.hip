@@ -55,19 +55,22 @@ typedef float float2v __attribute__((ext_vector_type(2)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 // What one launch of the contraction computes (the A operand, the sign
 // words and the tiling are the same in all of them).
 //   kMid     forward G1: fp16 operands; C = fp16(acc), pair order.
 //   kOut     forward G2: fp16 operands; C = bf16(rowscale * acc).
 //   kOutSave kOut, and F = acc (fp32, natural order) for the backward.
-//   kBwdMid  backward, first product: bf16 operands, B = +-1;
-//            C = bf16(rowscale * acc), pair order; F = per-tile token sums
-//            of acc * S, S fp16 in pair order.
-//   kBwdIn   backward, second product: bf16 operands, B = +-1;
-//            C = bf16(rowscale * acc) when C is given; F = per-tile token
-//            sums of acc * S, S bf16 in natural order.
+//   kBwdMid  backward, first product, B = +-1: acc times gscale[2G] (G =
+//            the token's 64-token group) is dt; C = fp16(rowscale * acc *
+//            gscale[2G + 1]), pair order; F = per-tile token sums of dt * S,
+//            S fp16 in pair order.
+//   kBwdIn   backward, second product, B = +-1: acc gscale[2G] /
+//            gscale[2G + 1] is du; C = bf16(rowscale * du) when C is given;
+//            F = per-tile token sums of du * S, S bf16 in natural order.
+// The backward's A operands are fp16 carrying the column scales and a
+// power-of-two scale per 64-token group (see bwd_prep_kernel), each rounded
+// once to fp16.
 enum Mode : int { kMid = 0, kOut = 1, kOutSave = 2, kBwdMid = 3, kBwdIn = 4 };
 
 constexpr int BM = 128;          // tokens per tile
@@ -79,17 +82,17 @@ constexpr int kARow = BK * 2;                // bytes of one token row of a K st
 constexpr int kATile = BM * kARow;           // 32 KiB
 constexpr int kWTile = BN * kWords * 4;      // 4 KiB
 constexpr int kCsTile = kWords * 16 * 4;     // column-scale pair dwords of one K step
-// LDS map: A0 | A1 | W0 | W1 | CS0 | CS1 (both activation buffers first, so
-// every operand read is a 16-bit immediate offset from one address), for a
-// token tile of kBM rows (128, or 64 for grids that would give each compute
-// unit at most one workgroup).
-template <int kBM>
+// LDS map: A0 .. A(S-1) | W0 .. W(S-1) | CS0 .. CS(S-1) for S pipeline
+// stages (the activation buffers first, so operand reads are immediate
+// offsets from one address), for a token tile of kBM rows (128, or 64 for
+// grids that would give each compute unit at most one workgroup).
+template <int kBM, int kStages>
 struct Lds {
   static constexpr int kATileT = kBM * kARow;
   static constexpr int kA0 = 0;
-  static constexpr int kW0 = 2 * kATileT;
-  static constexpr int kCs0 = kW0 + 2 * kWTile;
-  static constexpr int kBytes = kCs0 + 2 * kCsTile;
+  static constexpr int kW0 = kStages * kATileT;
+  static constexpr int kCs0 = kW0 + kStages * kWTile;
+  static constexpr int kBytes = kCs0 + kStages * kCsTile;
 };
 constexpr int kOob = (int)0x80000000u;
 static_assert(BM * kARow == 32 * 1024 && kThreads == 256, "eight 1 KiB copies per wave at BM");
@@ -122,6 +125,14 @@ __device__ __forceinline__ void copy4(i32x4 r, uint8_t *dst, int voff) {
 }
 
 __device__ __forceinline__ void wait_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Wait until at most N vector memory operations of this wave are in flight
+// (s_waitcnt with the expcnt and lgkmcnt fields at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_copies_but() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
 
 template <typename F, int... I>
 __device__ __forceinline__ void static_for_impl(F &&f, std::integer_sequence<int, I...>) {
@@ -200,25 +211,34 @@ __global__ __launch_bounds__(256) void prep_kernel(const uint16_t *__restrict__ 
   }
 }
 
-// C = rowscale * (A_pairorder x (sign(W) * colscale)^T), the forms listed
-// under Mode.  In the bf16 modes the column scale is 1 (the backward folds
-// its column scales into A), so no scale pairs are staged.
-template <int kMode, int kBM>
+// C = rowscale * (A_pairorder x (sign(W) * colscale)^T), in the forms listed
+// under Mode.
+template <int kMode, int kBM, int kStages>
 __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     const uint16_t *__restrict__ A, int T, int K, const uint32_t *__restrict__ W, int N,
     const uint32_t *__restrict__ cspairs, int Kpad, const uint16_t *__restrict__ rowscale,
-    uint16_t *__restrict__ C, const uint16_t *__restrict__ S, float *__restrict__ F) {
-  constexpr bool kBf16 = kMode >= kBwdMid;
+    uint16_t *__restrict__ C, const uint16_t *__restrict__ S, float *__restrict__ F,
+    const float *__restrict__ gscale) {
   constexpr bool kPairOut = kMode == kMid || kMode == kBwdMid;
+  constexpr bool kBwd = kMode == kBwdMid || kMode == kBwdIn;
+  // The backward folds its column scales into A: its B operand is +-1 and
+  // no scale pairs are staged.
+  constexpr bool kUnitB = kBwd;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  using LM = Lds<kBM>;
+  using LM = Lds<kBM, kStages>;
+  static_assert(kStages == 2 || kStages == 3, "pipeline depth");
   constexpr int kA0 = LM::kA0, kW0 = LM::kW0, kCs0 = LM::kCs0, kATile = LM::kATileT;
   constexpr int kLdsBytes = LM::kBytes;
   constexpr int kTokBlocks = kBM / 32;          // 32-token MFMA blocks per wave
   constexpr int kACopies = kBM * kARow / 1024 / 4;  // 1 KiB copies per wave per step
+  // Copy instructions per wave per step.  With three stages every wave
+  // copies the column-scale pairs too (identical bytes), so the count is
+  // the same in all waves and one s_waitcnt leaves exactly the newest
+  // step's copies in flight.
+  constexpr int kCopiesPerStep = kACopies + 4 + (kUnitB ? 0 : 1);
 
   // Tile assignment: consecutive workgroups land on consecutive XCDs; give
   // each XCD a contiguous range of tiles (weight-row tiles fastest).
@@ -261,7 +281,7 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       copy16(as, lds + kA0 + buf * kATile + (kACopies * wave + jj) * 1024, a_off[jj]);
 #pragma unroll
     for (int i = 0; i < 4; ++i) copy4(ws, lds + kW0 + buf * kWTile + (64 * wave + 16 * i) * 16, w_off[i]);
-    if (!kBf16 && wave == 0) {
+    if (!kUnitB && (kStages == 3 || wave == 0)) {
       const i32x4 cs =
           copy_rsrc(cspairs + step * (kCsTile / 4), (int64_t)Kpad * 2 - (int64_t)step * kCsTile);
       copy4(cs, lds + kCs0 + buf * kCsTile, 4 * lane);
@@ -274,6 +294,7 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     *reinterpret_cast<uint4 *>(lds + o) = make_uint4(0u, 0u, 0u, 0u);
   __syncthreads();
   issue(0, 0);
+  if (kStages == 3 && nk > 1) issue(1, 1);
 
   // This lane's weight rows: block j -> tile row 64*wave + 32*j + (l mod 32).
   const int wrow_l = 64 * wave + (lane & 31);
@@ -301,14 +322,23 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
 
   uint32_t kSignMask;
   asm volatile("v_mov_b32 %0, 0x80008000" : "=v"(kSignMask));
-  constexpr uint32_t kBf16OnePair = 0x3f803f80u;  // bf16 +1, +1
+  constexpr uint32_t kOnePair = 0x3c003c00u;  // fp16 +1, +1
 
-  wait_copies();
+  if (kStages == 3 && nk > 1)
+    wait_copies_but<kCopiesPerStep>();
+  else
+    wait_copies();
   __syncthreads();
 
   auto run_step = [&](int step, auto BUF) {
     constexpr int buf = decltype(BUF)::value;
-    if (step + 1 < nk) issue(step + 1, buf ^ 1);
+    if constexpr (kStages == 2) {
+      if (step + 1 < nk) issue(step + 1, buf ^ 1);
+    } else {
+      // the buffer of step + 2 held step - 1, which every wave finished
+      // before the last barrier
+      if (step + 2 < nk) issue(step + 2, (buf + 2) % 3);
+    }
     const uint8_t *abase = lds + kA0 + buf * kATile;
     const uint4 *wt = reinterpret_cast<const uint4 *>(lds + kW0 + buf * kWTile);
     const uint4 *cs = reinterpret_cast<const uint4 *>(lds + kCs0 + buf * kCsTile);
@@ -320,7 +350,7 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
 #pragma unroll
       for (int i = 0; i < kTokBlocks; ++i)
         af[slot][i] = *reinterpret_cast<const half8 *>(abase + a_rd[ks] + 32 * i * kARow);
-      if constexpr (!kBf16) c4[slot] = cs[2 * ks + g];
+      if constexpr (!kUnitB) c4[slot] = cs[2 * ks + g];
     };
     read_ops(0, 0);
     static_for<2 * kWords>([&](auto KS) {
@@ -331,10 +361,10 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       // scheduler would otherwise sink them next to their use).
       __builtin_amdgcn_sched_barrier(0);
       uint32_t cpair[4];
-      if constexpr (kBf16) {
-        // Words past the row end (a partial last K step) meet +-0, as the
-        // zero column-scale padding does in the fp16 modes.
-        const uint32_t one = step * kWords + (ks >> 1) < kw ? kBf16OnePair : 0u;
+      if constexpr (kUnitB) {
+        // words past the row end (a partial last K step) meet +-0, as the
+        // zero scale-pair padding does in the forward modes
+        const uint32_t one = step * kWords + (ks >> 1) < kw ? kOnePair : 0u;
         cpair[0] = cpair[1] = cpair[2] = cpair[3] = one;
       } else {
         cpair[0] = c4[cur].x; cpair[1] = c4[cur].y; cpair[2] = c4[cur].z; cpair[3] = c4[cur].w;
@@ -347,29 +377,36 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
         for (int e = 0; e < 4; ++e) bd[e] = cpair[e] ^ ((w << sh[ks & 1][e]) & kSignMask);
         const uint4 bq = make_uint4(bd[0], bd[1], bd[2], bd[3]);
 #pragma unroll
-        for (int i = 0; i < kTokBlocks; ++i) {
-          if constexpr (kBf16)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                __builtin_bit_cast(bf16x8, af[cur][i]), __builtin_bit_cast(bf16x8, bq), acc[i][j],
-                0, 0, 0);
-          else
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
-                af[cur][i], __builtin_bit_cast(half8, bq), acc[i][j], 0, 0, 0);
-        }
+        for (int i = 0; i < kTokBlocks; ++i)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[cur][i], __builtin_bit_cast(half8, bq),
+                                                             acc[i][j], 0, 0, 0);
       }
     });
-    wait_copies();
+    // the next step's copies must have landed; with three stages the
+    // copies of the step after it may stay in flight
+    if (kStages == 3 && step + 2 < nk)
+      wait_copies_but<kCopiesPerStep>();
+    else
+      wait_copies();
     __syncthreads();
   };
 
-  for (int step = 0; step < nk; step += 2) {
-    run_step(step, std::integral_constant<int, 0>{});
-    if (step + 1 < nk) run_step(step + 1, std::integral_constant<int, 1>{});
+  if constexpr (kStages == 2) {
+    for (int step = 0; step < nk; step += 2) {
+      run_step(step, std::integral_constant<int, 0>{});
+      if (step + 1 < nk) run_step(step + 1, std::integral_constant<int, 1>{});
+    }
+  } else {
+    for (int step = 0; step < nk; step += 3) {
+      run_step(step, std::integral_constant<int, 0>{});
+      if (step + 1 < nk) run_step(step + 1, std::integral_constant<int, 1>{});
+      if (step + 2 < nk) run_step(step + 2, std::integral_constant<int, 2>{});
+    }
   }
 
   // Epilogue.  32x32 accumulator layout: lane l holds column (l mod 32) and
   // rows 8*(e/4) + 4*(l/32) + (e mod 4), e = 0..15.
-  if constexpr (kMode == kBwdMid || kMode == kBwdIn) {
+  if constexpr (kBwd) {
     // The S block of this tile (kBM tokens x 256 weight rows, 512 bytes a
     // token) goes into the idle activation buffers with LDS copies, two
     // token rows per copy instruction; a row's 16-byte chunk c lands at
@@ -386,14 +423,23 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     }
     wait_copies();
     __syncthreads();
-  }
+    // The 32-token block i lies in 64-token group (t0 + 32 i) / 64; its
+    // factors are uniform over the wave (zero past T).
+    float fg[kTokBlocks], fz[kTokBlocks];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int n = wrow0 + 32 * j;
-    if constexpr (kMode == kBwdMid || kMode == kBwdIn) {
-      // Token sum of acc * S over this tile for weight row n: the lane's
-      // sixteen tokens per block, then its partner half (lane XOR 32).
-      // Tokens past T have zero accumulators and zero S.
+    for (int i = 0; i < kTokBlocks; ++i) {
+      const int tb = t0 + 32 * i;
+      const float2 gs = tb < T ? reinterpret_cast<const float2 *>(gscale)[tb >> 6]
+                               : make_float2(0.f, 1.f);
+      fg[i] = kMode == kBwdMid ? gs.x : gs.x / gs.y;
+      fz[i] = gs.y;
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int n = wrow0 + 32 * j;
+      // Token sum of gradient * S for weight row n: the lane's sixteen
+      // tokens per block, then its partner half (lane XOR 32).  Tokens past
+      // T have zero accumulators and zero S.
       const int lpos = (kMode == kBwdMid ? pair_pos(n) : n) - n0;
       const int cbyte = 2 * (lpos & 7);
       float part = 0.f;
@@ -404,13 +450,31 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
           const int row = 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
           const int pos = ((lpos >> 3) ^ (((row >> 2) & 1) << 2)) * 16 + cbyte;
           const uint16_t sv = *reinterpret_cast<const uint16_t *>(lds + row * 512 + pos);
-          part += acc[i][j][e] * (kMode == kBwdMid ? f16_to_f32(sv) : bf16_to_f32(sv));
+          part += acc[i][j][e] * fg[i] * (kMode == kBwdMid ? f16_to_f32(sv) : bf16_to_f32(sv));
         }
       part += __shfl_xor(part, 32, 64);
       if (g == 0 && n < N) F[(size_t)(t0 / kBM) * N + n] = part;
+      if (n >= N || !C) continue;
+      const float rs = f16_to_f32(rowscale[n]);
+#pragma unroll
+      for (int i = 0; i < kTokBlocks; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int t = t0 + 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
+          if (t < T) {
+            if constexpr (kMode == kBwdMid)
+              C[(size_t)t * N + pair_pos(n)] = f32_to_f16(acc[i][j][e] * rs * fz[i]);
+            else
+              C[(size_t)t * N + n] = f32_to_bf16(acc[i][j][e] * fg[i] * rs);
+          }
+        }
     }
+    return;
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int n = wrow0 + 32 * j;
     if (n >= N) continue;
-    if (kMode == kBwdIn && !C) continue;
     const float rs = rowscale ? f16_to_f32(rowscale[n]) : 1.0f;
     const int cpos = kPairOut ? pair_pos(n) : n;
 #pragma unroll
@@ -428,28 +492,96 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   }
 }
 
-// Backward preparation, one launch: dy (bf16, [T][m]) -> A1 = bf16(dy *
-// s_out) in pair order, the A operand of the first backward product, and
-// per-64-token partial sums of dy * z (z = the saved pre-scale forward
-// output, fp32 [T][m]) for the gradient of s_out.  Thread (ty, ux) of a
-// block handles the 16 columns of unit ux (as in pair_order_unit) for
-// tokens t0 + ty + 16 q; the 16 ty partials of a column are added in a
+// Backward operand statistics, one launch.  Block t < T takes token t:
+// tstat[2t] = max_i |dy[t][i] s_out[i]| and tstat[2t + 1] = sum_i
+// |dy[t][i] s_out[i]|, each thread reading 8 columns of every 2048 (four
+// such loads in flight).  Block T stores max_k |s_mid[k]| in tstat[2T].
+constexpr int kExpClamp = 100;
+__global__ __launch_bounds__(256) void bwd_rowstat_kernel(const uint16_t *__restrict__ dy,
+                                                          const uint16_t *__restrict__ s_out,
+                                                          int T, int m, float *__restrict__ tstat,
+                                                          const uint16_t *__restrict__ s_mid,
+                                                          int r) {
+  __shared__ float rmx[4], rl1[4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int t = blockIdx.x;
+  float mx = 0.f, l1 = 0.f;
+  if (t == T) {
+    for (int k = threadIdx.x; k < r; k += 256) mx = fmaxf(mx, fabsf(f16_to_f32(s_mid[k])));
+  } else {
+    const uint16_t *row = dy + (size_t)t * m;
+    for (int c0 = threadIdx.x * 8; c0 < m; c0 += 4 * 2048) {
+      u32x4 v[4], so[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int c = c0 + q * 2048;
+        v[q] = c < m ? *reinterpret_cast<const u32x4 *>(row + c) : u32x4{0u, 0u, 0u, 0u};
+        so[q] = c < m ? *reinterpret_cast<const u32x4 *>(s_out + c) : u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const half2v sp = __builtin_bit_cast(half2v, so[q][e]);
+          const float a = fabsf(__uint_as_float(v[q][e] << 16) * (float)sp[0]);
+          const float b = fabsf(__uint_as_float(v[q][e] & 0xffff0000u) * (float)sp[1]);
+          mx = fmaxf(mx, fmaxf(a, b));
+          l1 += a + b;
+        }
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+    l1 += __shfl_xor(l1, off, 64);
+  }
+  if (lane == 0) {
+    rmx[wave] = mx;
+    rl1[wave] = l1;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const float m4 = fmaxf(fmaxf(rmx[0], rmx[1]), fmaxf(rmx[2], rmx[3]));
+    if (t == T) {
+      tstat[2 * T] = m4;
+    } else {
+      tstat[2 * t] = m4;
+      tstat[2 * t + 1] = ((rl1[0] + rl1[1]) + rl1[2]) + rl1[3];
+    }
+  }
+}
+
+// Backward preparation, one launch.  Block row tb is the 64-token group G.
+// From the statistics of dy * s_out, with M the group's largest entry,
+// L_t the per-token sums of |entries| and S the largest |s_mid|: e
+// (M 2^e in [2^13, 2^14)) puts fp16(dy s_out 2^e) at full fp16 precision
+// down to M 2^-27, and c (2^e L_t S < 2^(14 + c) for every token of the
+// group) bounds the first product's scaled outputs, |acc s_mid| <=
+// 2^e L_t S, so fp16(acc s_mid 2^-c) cannot overflow; e and c are clamped
+// to +-100 and are 0 for an all-zero group.  Block column 0 stores
+// gscale[2G] = 2^-e and gscale[2G + 1] = 2^-c.  Every block then writes
+// A1 = fp16(dy s_out 2^e) in pair order (the A operand of the first
+// backward product) and the per-group partial sums of dy * z (z = the
+// saved pre-scale forward output, fp32 [T][m]) for the gradient of s_out.
+// Thread (ty, ux) handles the 16 columns of unit ux (as in pair_order_unit)
+// for tokens t0 + ty + 16 q; the 16 ty partials of a column are added in a
 // fixed order through LDS.
 constexpr int kPrepTokens = 64;
 __global__ __launch_bounds__(256) void bwd_prep_kernel(const uint16_t *__restrict__ dy,
                                                        const uint16_t *__restrict__ s_out,
                                                        const float *__restrict__ z, int T, int m,
+                                                       const float *__restrict__ tstat,
+                                                       float *__restrict__ gscale,
                                                        uint16_t *__restrict__ A1,
                                                        float *__restrict__ part) {
   __shared__ float red[16][256 + 4];
+  __shared__ int gexp[2];
   const int ux = threadIdx.x & 15, ty = threadIdx.x >> 4;
   const int ur = blockIdx.x * 16 + ux;                       // unit within the row
   const int c = (ur >> 1) * 32 + 8 * (ur & 1);               // first of its columns
   const int tb = blockIdx.y;
   const bool live = c < m;
-  float so[16], acc[16];
-#pragma unroll
-  for (int q = 0; q < 16; ++q) acc[q] = 0.f;
+  float so[16];
   if (live) {
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
@@ -457,6 +589,37 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const uint16_t *__restric
       so[8 + q] = f16_to_f32(s_out[c + 16 + q]);
     }
   }
+  // group exponents: wave 0 reduces the 64 tokens' statistics
+  if (threadIdx.x < 64) {
+    const int t = tb * kPrepTokens + threadIdx.x;
+    float mx = t < T ? tstat[2 * t] : 0.f;
+    for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+    int e = 0, c = 0;
+    if (mx > 0.f) {
+      int k;
+      frexpf(mx, &k);  // mx = f 2^k, f in [0.5, 1)
+      e = 14 - k;
+      e = e > kExpClamp ? kExpClamp : (e < -kExpClamp ? -kExpClamp : e);
+      float bound = t < T ? ldexpf(tstat[2 * t + 1], e) * tstat[2 * T] : 0.f;
+      for (int off = 32; off > 0; off >>= 1) bound = fmaxf(bound, __shfl_xor(bound, off, 64));
+      frexpf(bound, &k);  // every 2^e L_t < 2^k
+      c = k - 14;
+      c = c > kExpClamp ? kExpClamp : (c < -kExpClamp ? -kExpClamp : c);
+    }
+    if (threadIdx.x == 0) {
+      gexp[0] = e;
+      gexp[1] = c;
+      if (blockIdx.x == 0) {
+        gscale[2 * tb] = ldexpf(1.f, -e);
+        gscale[2 * tb + 1] = ldexpf(1.f, -c);
+      }
+    }
+  }
+  __syncthreads();
+  const float up = ldexpf(1.f, gexp[0]);  // 2^e, exact
+  float acc[16];
+#pragma unroll
+  for (int q = 0; q < 16; ++q) acc[q] = 0.f;
 #pragma unroll
   for (int q4 = 0; q4 < kPrepTokens / 16; ++q4) {
     const int t = tb * kPrepTokens + ty + 16 * q4;
@@ -481,10 +644,8 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const uint16_t *__restric
       acc[8 + 2 * e] += h0 * zh[2 * e];
       acc[8 + 2 * e + 1] += h1 * zh[2 * e + 1];
       // pair dword: column c+k (low half) with its partner c+16+k (high)
-      d[2 * e] = (uint32_t)f32_to_bf16(g0 * so[2 * e]) |
-                 ((uint32_t)f32_to_bf16(h0 * so[8 + 2 * e]) << 16);
-      d[2 * e + 1] = (uint32_t)f32_to_bf16(g1 * so[2 * e + 1]) |
-                     ((uint32_t)f32_to_bf16(h1 * so[8 + 2 * e + 1]) << 16);
+      d[2 * e] = pack_f16x2(g0 * so[2 * e] * up, h0 * so[8 + 2 * e] * up);
+      d[2 * e + 1] = pack_f16x2(g1 * so[2 * e + 1] * up, h1 * so[8 + 2 * e + 1] * up);
     }
     uint4 *dst = reinterpret_cast<uint4 *>(A1 + (size_t)t * m + (c & ~31) + 2 * (c & 15));
     dst[0] = make_uint4(d[0], d[1], d[2], d[3]);
@@ -559,6 +720,16 @@ size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
 int64_t kpad(int64_t K) { return (K + BK - 1) / BK * BK; }
 
+// Copy pipeline depth per token-tile height.
+#ifndef AF1_GEMM_STAGES_128
+#define AF1_GEMM_STAGES_128 2
+#endif
+#ifndef AF1_GEMM_STAGES_64
+#define AF1_GEMM_STAGES_64 2
+#endif
+constexpr int kStages128 = AF1_GEMM_STAGES_128;
+constexpr int kStages64 = AF1_GEMM_STAGES_64;
+
 // One contraction C[T, N] over K on the stream.  A grid of 128-token tiles
 // that gives each compute unit at most one workgroup (one wave per SIMD)
 // uses 64-token tiles instead: twice the workgroups, each expanding its
@@ -568,19 +739,20 @@ int64_t kpad(int64_t K) { return (K + BK - 1) / BK * BK; }
 template <int kMode>
 hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *W, int64_t N,
                        const uint32_t *cs, const uint16_t *rs, uint16_t *C, const uint16_t *S,
-                       float *F, hipStream_t s, int *tile_tokens = nullptr) {
+                       float *F, hipStream_t s, int *tile_tokens = nullptr,
+                       const float *gscale = nullptr) {
   const int cus = device_cus();
   const unsigned gx = (unsigned)((N + BN - 1) / BN);
   const int64_t tiles128 = (int64_t)gx * ((T + BM - 1) / BM);
   if (tiles128 <= (int64_t)cus && T > 64) {
     dim3 g(gx, (unsigned)((T + 63) / 64));
-    bingemm_kernel<kMode, 64><<<g, kThreads, Lds<64>::kBytes, s>>>(
-        A, (int)T, (int)K, W, (int)N, cs, (int)kpad(K), rs, C, S, F);
+    bingemm_kernel<kMode, 64, kStages64><<<g, kThreads, Lds<64, kStages64>::kBytes, s>>>(
+        A, (int)T, (int)K, W, (int)N, cs, (int)kpad(K), rs, C, S, F, gscale);
     if (tile_tokens) *tile_tokens = 64;
   } else {
     dim3 g(gx, (unsigned)((T + BM - 1) / BM));
-    bingemm_kernel<kMode, BM><<<g, kThreads, Lds<BM>::kBytes, s>>>(
-        A, (int)T, (int)K, W, (int)N, cs, (int)kpad(K), rs, C, S, F);
+    bingemm_kernel<kMode, BM, kStages128><<<g, kThreads, Lds<BM, kStages128>::kBytes, s>>>(
+        A, (int)T, (int)K, W, (int)N, cs, (int)kpad(K), rs, C, S, F, gscale);
     if (tile_tokens) *tile_tokens = BM;
   }
   return hipGetLastError();
@@ -622,7 +794,7 @@ int64_t tiles64(int64_t T) { return (T + 63) / 64; }
 
 struct BwdWs {
   uint16_t *A1, *Zb;
-  float *p_out, *p_mid, *p_in;
+  float *p_out, *p_mid, *p_in, *tstat, *gscale;
 };
 
 BwdWs backward_ws(void *ws, int64_t m, int64_t n, int64_t r, int64_t T) {
@@ -637,13 +809,18 @@ BwdWs backward_ws(void *ws, int64_t m, int64_t n, int64_t r, int64_t T) {
   w.p_mid = reinterpret_cast<float *>(base);
   base += align256((size_t)tiles64(T) * r * 4);
   w.p_in = reinterpret_cast<float *>(base);
+  base += align256((size_t)tiles64(T) * n * 4);
+  w.tstat = reinterpret_cast<float *>(base);
+  base += align256((size_t)T * 8 + 4);
+  w.gscale = reinterpret_cast<float *>(base);
   return w;
 }
 
 size_t backward_ws_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
   return align256((size_t)T * m * 2) + align256((size_t)T * r * 2) +
          align256((size_t)tiles64(T) * m * 4) + align256((size_t)tiles64(T) * r * 4) +
-         align256((size_t)tiles64(T) * n * 4);
+         align256((size_t)tiles64(T) * n * 4) + align256((size_t)T * 8 + 4) +
+         align256((size_t)tiles64(T) * 8);
 }
 
 }  // namespace
@@ -717,17 +894,25 @@ hipError_t launch_backward(int64_t m, int64_t n, int64_t r, const uint32_t *BuT,
   const uint16_t *v = static_cast<const uint16_t *>(saved);
   const float *z = reinterpret_cast<const float *>(static_cast<const uint8_t *>(saved) +
                                                    align256((size_t)T * r * 2));
-  const dim3 gp((unsigned)((m + 255) / 256), (unsigned)tiles64(T));
-  bwd_prep_kernel<<<gp, 256, 0, s>>>(dy, s_out, z, (int)T, (int)m, w.A1, w.p_out);
+  // per-token statistics of dy * s_out, and the largest |s_mid|
+  bwd_rowstat_kernel<<<(unsigned)(T + 1), 256, 0, s>>>(dy, s_out, (int)T, (int)m, w.tstat, s_mid,
+                                                       (int)r);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // dt = Bu^T (s_out .* dy): weight rows are the r rows of Bu^T; the output
-  // is s_mid .* dt in pair order (the next A operand); sums dt .* v.
-  int tm = 0, ti = 0;
-  e = contraction<kBwdMid>(w.A1, T, m, BuT, r, nullptr, s_mid, w.Zb, v, w.p_mid, s, &tm);
+  const dim3 gp((unsigned)((m + 255) / 256), (unsigned)tiles64(T));
+  bwd_prep_kernel<<<gp, 256, 0, s>>>(dy, s_out, z, (int)T, (int)m, w.tstat, w.gscale, w.A1,
+                                     w.p_out);
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // du = Bv^T (s_mid .* dt): dx = s_in .* du; sums du .* x.
-  e = contraction<kBwdIn>(w.Zb, T, r, BvT, n, nullptr, s_in, dx, x, w.p_in, s, &ti);
+  // dt 2^e = Bu^T (s_out .* dy 2^e): weight rows are the r rows of Bu^T;
+  // the output fp16(s_mid .* dt 2^(e - c)) in pair order is the next A
+  // operand; sums dt .* v.
+  int tm = 0, ti = 0;
+  e = contraction<kBwdMid>(w.A1, T, m, BuT, r, nullptr, s_mid, w.Zb, v, w.p_mid, s, &tm,
+                           w.gscale);
+  if (e != hipSuccess) return e;
+  // du 2^(e - c) = Bv^T (s_mid .* dt 2^(e - c)): dx = s_in .* du; sums du .* x.
+  e = contraction<kBwdIn>(w.Zb, T, r, BvT, n, nullptr, s_in, dx, x, w.p_in, s, &ti, w.gscale);
   if (e != hipSuccess) return e;
   const int total = (int)(m + r + n);
   bwd_finish_kernel<<<(unsigned)((total + kFinishCols - 1) / kFinishCols), 256, 0, s>>>(

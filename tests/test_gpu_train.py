@@ -4,8 +4,10 @@ oracle on the same seeded inputs.
 
 Bars: the packed transpose bit-exact; the training forward's y bit-identical
 to the inference forward's; dx within relative L2 5e-3 per token (max over
-tokens) and each scale gradient within relative L2 5e-3 of the oracle's;
-gradient accumulation, dx skipping and repeated calls bit-exact."""
+tokens; dx is rounded to bfloat16) and each fp32 scale gradient within
+relative L2 1e-3 of the oracle's (the products' operands are exact or
+rounded once to fp16); gradient accumulation, dx skipping and repeated calls
+bit-exact."""
 import numpy as np
 import pytest
 import torch
@@ -16,6 +18,7 @@ from paper_2609_06161_amd.layer import DeviceLayer, bf16_bits_to_f64, to_device
 pytestmark = pytest.mark.gpu
 
 TOL = 5e-3
+GRAD_TOL = 1e-3
 
 
 def rel_l2(a, e):
@@ -50,14 +53,14 @@ def run_train(lin, dy, accumulate_into=None, want_dx=True):
     return L, x, d_dy, y, saved, dx, grads
 
 
-def check_against_oracle(oracle, lin, dy, tol=TOL):
+def check_against_oracle(oracle, lin, dy, tol=TOL, grad_tol=GRAD_TOL):
     _, _, _, y, _, dx, grads = run_train(lin, dy)
     rdx, rout, rmid, rin = oracle.backward(lin.m, lin.n, lin.r, lin.Bu, lin.Bv, lin.s_out,
                                            lin.s_mid, lin.s_in, lin.x, dy)
     e = max_row_rel_l2(bf16_bits_to_f64(dx), rdx)
     eo, em, ei = rel_l2(f32(grads[0]), rout), rel_l2(f32(grads[1]), rmid), rel_l2(f32(grads[2]), rin)
     print(f"  dx {e:.2e} ds_out {eo:.2e} ds_mid {em:.2e} ds_in {ei:.2e}", flush=True)
-    assert e <= tol and eo <= tol and em <= tol and ei <= tol
+    assert e <= tol and eo <= grad_tol and em <= grad_tol and ei <= grad_tol
     return y
 
 
@@ -143,10 +146,25 @@ def test_backward_rank_above_dimensions(oracle):
 
 
 def test_backward_tiny_gradients_keep_their_digits(oracle):
-    """Upstream gradients around 2^-30 (far below fp16's range): the bf16
-    operands keep fp32's exponent range, so the relative error bar holds."""
+    """Upstream gradients around 2^-30 (far below fp16's range): the fp16
+    operands carry a power-of-two scale per 64-token group, so the relative
+    error bar holds."""
     lin = synth.make_linear(85, 512, 768, 224, 96)
     dy = synth.make_output_grad(86, 96, 512, scale=2.0 ** -30)
+    check_against_oracle(oracle, lin, dy)
+
+
+def test_backward_tokens_of_very_different_magnitudes(oracle):
+    """Upstream gradients whose per-token scale spans 10^6 (and an all-zero
+    64-token group): the operands are scaled per 64-token group, so every
+    token keeps its relative accuracy."""
+    m, n, r, T = 512, 768, 224, 200
+    lin = synth.make_linear(87, m, n, r, T)
+    dy = synth.make_output_grad(88, T, m)
+    f = np.exp(np.random.default_rng(89).uniform(np.log(1e-3), np.log(1e3), T)).astype(np.float32)
+    g = (dy.astype(np.uint32) << 16).view(np.float32) * f[:, None]
+    g[64:128] = 0.0
+    dy = synth.f32_to_bf16_bits(g)
     check_against_oracle(oracle, lin, dy)
 
 
