@@ -131,11 +131,12 @@ def test_forward_train_output_is_the_inference_output():
     assert torch.equal(y_inf, y_tr)
 
 
-@pytest.mark.parametrize("name", ["attn4096", "sq8192"])
-def test_backward_full_size_dims(oracle, name):
+@pytest.mark.parametrize("name,T", [("attn4096", 64), ("sq8192", 64), ("mlp_up28672x8192", 32),
+                                    ("mlp_down8192x28672", 32)])
+def test_backward_full_size_dims(oracle, name, T):
     m, n, r = synth.SHAPES[name]
-    lin = synth.make_linear(77, m, n, r, 64)
-    dy = synth.make_output_grad(78, 64, m)
+    lin = synth.make_linear(77, m, n, r, T)
+    dy = synth.make_output_grad(78, T, m)
     check_against_oracle(oracle, lin, dy)
 
 
