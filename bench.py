@@ -149,7 +149,17 @@ def decode_time(args, torch, stream, m, n, r, b, seed, steps):
 
 DECODE_TABLE = [("sq1024", 1), ("attn4096", 8), ("kv1024x4096", 1), ("mlp_up14336x4096", 1),
                 ("mlp_up14336x4096", 4), ("mlp_up14336x4096", 16), ("mlp_down4096x14336", 1),
-                ("mlp_down4096x14336", 4), ("mlp_down4096x14336", 16)]
+                ("mlp_down4096x14336", 4), ("mlp_down4096x14336", 16),
+                ("attn4096_r5120_2.5bpw", 1), ("attn4096_r5120_2.5bpw", 8)]
+
+# The paper's other budget (2.5 bits per weight): rank round(2.5 mn / (m + n)),
+# above min(m, n), so the second sign matrix is the larger one.
+EXTRA_SHAPES = {"attn4096_r5120_2.5bpw": (4096, 4096, 5120)}
+
+
+def shape_of(name):
+    from paper_2609_06161_amd import synth
+    return EXTRA_SHAPES[name] if name in EXTRA_SHAPES else synth.SHAPES[name]
 
 
 STACK_LINEARS = [("q", 4096, 4096, 2016), ("k", 1024, 4096, 800), ("v", 1024, 4096, 800),
@@ -226,7 +236,7 @@ def bench_decode_table(args, torch, stream):
     from paper_2609_06161_amd import synth
     out = {}
     for name, b in DECODE_TABLE:
-        m, n, r = synth.SHAPES[name]
+        m, n, r = shape_of(name)
         d = decode_time(args, torch, stream, m, n, r, b, 2000 + b, max(200, args.steps // 4))
         out[f"{name}_b{b}"] = dict(us_per_layer=round(d["us_graph"], 3),
                                    us_per_layer_eager=round(d["us_eager"], 3),
@@ -269,6 +279,19 @@ def bench_gemm(args, torch, stream):
         out[name]["speedup_vs_dense_bf16"] = msd / ms
         del xd, wd
     out["all3_tflops"] = total_flops / (total_ms * 1e-3) / 1e12
+    # the 2.5-BPW setting at 4096^2 (context; not in the three-shape total)
+    m, n, r = EXTRA_SHAPES["attn4096_r5120_2.5bpw"]
+    lin = synth.make_linear(56, m, n, r, T)
+    L = DeviceLayer.from_host(lin)
+    x = to_device(lin.x)
+    y = torch.empty((T, m), dtype=torch.int16, device="cuda")
+    ws = torch.empty(af1.af1_gemm_workspace_bytes(m, n, r, T), dtype=torch.uint8, device="cuda")
+    fn = lambda i: L.gemm(x, y, ws, stream)
+    time_events(fn, 3, stream)
+    ms = time_events(fn, args.gemm_steps, stream) / args.gemm_steps
+    out["attn4096_r5120_2.5bpw"] = dict(m=m, n=n, r=r, T=T, us=ms * 1e3,
+                                        tflops=2.0 * T * r * (m + n) / (ms * 1e-3) / 1e12)
+    del L, x, y, ws
     # MFMA roofline of the prefill leg: algorithmic flops 2*T*r*(m+n) of the
     # three calls over their summed time, against the dense fp16 peak (the
     # contractions run on fp16 operands).

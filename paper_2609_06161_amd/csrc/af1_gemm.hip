@@ -1,5 +1,8 @@
 // Prefill-regime forward of the factorized binary linear on the gfx950
-// matrix cores (paper App. A.2.1, Diag form; Sec. 4.1):
+// matrix cores (paper App. A.2.1, Diag form; Sec. 4.1), and the contractions
+// of its scale-only reconstruction (Sec. 4.1: sign matrices frozen, the
+// gradients of the three scale vectors and of x through the transposed
+// factors; the modes are listed under Mode below):
 //
 //   G1:  Z[t, k] = fp16( sum_j x[t, j] * (Bv[k, j] * s_in[j]) )
 //   G2:  y[t, i] = bf16( s_out[i] * sum_k Z[t, k] * (Bu[i, k] * s_mid[k]) )
@@ -32,7 +35,8 @@
 // Staging.  Operands go from global memory straight into LDS (buffer loads
 // with the LDS destination), double-buffered: a K step issues the copies of
 // the next step, runs its MFMAs, waits for its copies and meets one
-// barrier.  No staging registers are needed, which leaves room to read the
+// barrier (a three-buffer variant, two steps ahead, is a template option;
+// it measured slower).  No staging registers are needed, which leaves room to read the
 // next MFMA step's operands from LDS while the current one runs.  An LDS
 // copy instruction writes 64 consecutive 16-byte chunks, one per lane, but
 // each lane chooses its source: the chunk of token row t holding columns
