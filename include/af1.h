@@ -171,15 +171,15 @@ AF1_API af1_status af1_linear_gemv_multi(const af1_factorized_linear *Ls, int32_
  *        kernels address operands with 32-bit byte offsets); otherwise
  *        AF1_ERR_BATCH.  A sign matrix of 2 GiB or more is AF1_ERR_SHAPE.
  *   ws : device workspace of at least af1_gemm_workspace_bytes(m, n, r, T)
- *        bytes; holds the fp16 copy of x, the [T, r] intermediate and the
- *        column-scale pairs.
- * Arithmetic: both products run on fp16 MFMA with fp32 accumulation.  The
- * sign of each factor entry is applied to the fp16 column scale (s_in for
- * the first product, s_mid for the second), so every operand is exact:
- * x enters as fp16 (exact for |x| < 65504), the intermediate is rounded
- * once to fp16 before the second product (|values| must stay below 65504;
- * values below 2^-14 keep fewer significant bits), s_out is applied in fp32
- * and y is rounded to bfloat16.
+ *        bytes; holds the fp16 operand s_in .* x and the [T, r]
+ *        intermediate.
+ * Arithmetic: both products run on fp16 MFMA with fp32 accumulation against
+ * exact +-1 sign operands; each scale vector is applied outside them.
+ * s_in .* x is rounded once to fp16 (the bf16 x fp16 product is exact in
+ * fp32), the intermediate s_mid .* (Bv (s_in .* x)) is rounded once to fp16
+ * before the second product, s_out is applied in fp32 and y is rounded to
+ * bfloat16.  Both fp16 operands must stay below 65504 in magnitude; values
+ * below 2^-14 keep fewer significant bits.
  */
 AF1_API size_t af1_gemm_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T);
 AF1_API af1_status af1_linear_gemm(const af1_factorized_linear *L, const uint16_t *x,
@@ -213,8 +213,9 @@ AF1_API af1_status af1_pack_transpose(const uint32_t *src, int64_t rows, int64_t
  *
  * af1_linear_forward_train -- y as af1_linear_gemm computes it (same
  * kernels and rounding, bit-identical y), and in `saved` the two pre-scale
- * intermediates the gradients need: v = Bv (s_in .* x) ([T, r], fp16, in a
- * layout private to the library) and z = Bu (s_mid .* v) ([T, m], fp32).
+ * intermediates the gradients need: v = Bv (s_in .* x) ([T, r], rounded to
+ * fp16, in a layout private to the library) and z = Bu (s_mid .* v)
+ * ([T, m], fp32, the second product's accumulator).
  *   saved : device, at least af1_train_saved_bytes(m, n, r, T) bytes,
  *           written; hand it unchanged to af1_linear_backward with the same
  *           layer, x and T.

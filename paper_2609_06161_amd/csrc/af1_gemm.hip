@@ -4,25 +4,26 @@
 // gradients of the three scale vectors and of x through the transposed
 // factors; the modes are listed under Mode below):
 //
-//   G1:  Z[t, k] = fp16( sum_j x[t, j] * (Bv[k, j] * s_in[j]) )
-//   G2:  y[t, i] = bf16( s_out[i] * sum_k Z[t, k] * (Bu[i, k] * s_mid[k]) )
+//   G1:  Z[t, k] = fp16( s_mid[k] * sum_j xs[t, j] * Bv[k, j] ),
+//        xs = fp16(s_in .* x)
+//   G2:  y[t, i] = bf16( s_out[i] * sum_k Z[t, k] * Bu[i, k] )
 //
-// Both are "activations x signed column scale" contractions,
-//   C[t, n] = rowscale[n] * sum_c A[t, c] * (sign(W[n, c]) * colscale[c]),
-// with A fp16 and W bit-packed.  Flipping the sign bit of the fp16 column
-// scale keeps both MFMA operands exact (x is converted bf16 -> fp16, exact
-// for |x| < 65504); accumulation is fp32.
+// Every contraction has the form
+//   C[t, n] = rowscale[n] * sum_c A[t, c] * sign(W[n, c]),
+// with A fp16 (the column scales already folded in, each product rounded
+// once to fp16) and W bit-packed, so the B operand of the matrix cores is
+// exactly +-1.  The other placement, the signed column scale as B and the
+// activations exact, costs the same instructions but draws more power per
+// MFMA (the B mantissas toggle); under the chip's power limit it ran 5-8%
+// slower on the 70B-shaped layers.  Accumulation is fp32.
 //
 // Pair order.  Within a 32-bit sign word, columns p and p+16 (p = 0..15)
 // form one MFMA operand dword, so one shift and one three-input bit
-// operation produce two fp16 operands (column-scale pair XOR the two sign
-// bits).  The activations are kept in the same order: inside every group
-// of 32 columns, column p sits at position 2p and column p+16 at 2p+1.  A
-// preparation pass writes x in that order (converting bf16 to fp16 once,
-// instead of once per weight-row tile) and the column scales as pair dwords
-// (one launch for all three), and G1
-// writes Z in that order, so the GEMMs stage their operands with plain
-// copies.
+// operation produce two fp16 operands (the +1 pair XOR the two sign bits).
+// The activations are kept in the same order: inside every group of 32
+// columns, column p sits at position 2p and column p+16 at 2p+1.  A
+// preparation pass writes fp16(s_in .* x) in that order, and G1 writes Z in
+// that order, so the GEMMs stage their operands with plain copies.
 //
 // Tiling.  A 256-thread workgroup computes a 128 (tokens) x 256 (weight
 // rows) tile of C over K steps of 128 columns.  The activation tile is the
@@ -61,21 +62,21 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // What one launch of the contraction computes (the A operand, the sign
-// words and the tiling are the same in all of them).
-//   kMid     forward G1: fp16 operands; C = fp16(acc), pair order.
-//   kOut     forward G2: fp16 operands; C = bf16(rowscale * acc).
+// words and the tiling are the same in all of them; the B operand is +-1).
+//   kMid     forward G1: C = fp16(rowscale * acc), pair order.
+//   kMidSave kMid, and V = fp16(acc) (pair order) for the backward.
+//   kOut     forward G2: C = bf16(rowscale * acc).
 //   kOutSave kOut, and F = acc (fp32, natural order) for the backward.
-//   kBwdMid  backward, first product, B = +-1: acc times gscale[2G] (G =
-//            the token's 64-token group) is dt; C = fp16(rowscale * acc *
+//   kBwdMid  backward, first product: acc times gscale[2G] (G = the token's
+//            64-token group) is dt; C = fp16(rowscale * acc *
 //            gscale[2G + 1]), pair order; F = per-tile token sums of dt * S,
 //            S fp16 in pair order.
-//   kBwdIn   backward, second product, B = +-1: acc gscale[2G] /
-//            gscale[2G + 1] is du; C = bf16(rowscale * du) when C is given;
-//            F = per-tile token sums of du * S, S bf16 in natural order.
-// The backward's A operands are fp16 carrying the column scales and a
-// power-of-two scale per 64-token group (see bwd_prep_kernel), each rounded
-// once to fp16.
-enum Mode : int { kMid = 0, kOut = 1, kOutSave = 2, kBwdMid = 3, kBwdIn = 4 };
+//   kBwdIn   backward, second product: acc gscale[2G] / gscale[2G + 1] is
+//            du; C = bf16(rowscale * du) when C is given; F = per-tile token
+//            sums of du * S, S bf16 in natural order.
+// The backward's A operands also carry a power-of-two scale per 64-token
+// group (see bwd_prep_kernel).
+enum Mode : int { kMid = 0, kMidSave = 1, kOut = 2, kOutSave = 3, kBwdMid = 4, kBwdIn = 5 };
 
 constexpr int BM = 128;          // tokens per tile
 constexpr int BN = 256;          // weight rows per tile
@@ -85,9 +86,7 @@ constexpr int kThreads = 256;
 constexpr int kARow = BK * 2;                // bytes of one token row of a K step
 constexpr int kATile = BM * kARow;           // 32 KiB
 constexpr int kWTile = BN * kWords * 4;      // 4 KiB
-constexpr int kCsTile = kWords * 16 * 4;     // column-scale pair dwords of one K step
-// LDS map: A0 .. A(S-1) | W0 .. W(S-1) | CS0 .. CS(S-1) for S pipeline
-// stages (the activation buffers first, so operand reads are immediate
+// LDS map: A0 .. A(S-1) | W0 .. W(S-1) for S pipeline stages (the activation buffers first, so operand reads are immediate
 // offsets from one address), for a token tile of kBM rows (128, or 64 for
 // grids that would give each compute unit at most one workgroup).
 template <int kBM, int kStages>
@@ -95,12 +94,10 @@ struct Lds {
   static constexpr int kATileT = kBM * kARow;
   static constexpr int kA0 = 0;
   static constexpr int kW0 = kStages * kATileT;
-  static constexpr int kCs0 = kW0 + kStages * kWTile;
-  static constexpr int kBytes = kCs0 + kStages * kCsTile;
+  static constexpr int kBytes = kW0 + kStages * kWTile;
 };
 constexpr int kOob = (int)0x80000000u;
 static_assert(BM * kARow == 32 * 1024 && kThreads == 256, "eight 1 KiB copies per wave at BM");
-static_assert(kCsTile == 64 * 4, "one 4-byte copy per lane of wave 0");
 static_assert(kATile + 3 * 32 * kARow + kARow < 65536, "immediate LDS offsets");
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -153,15 +150,24 @@ __device__ __forceinline__ uint32_t pack_f16x2(float lo_half, float hi_half) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, half2v));
 }
 
+// The low and high fp16 halves of a dword, as floats.  (Reading a dword
+// element of a vector through a bit cast to a half pair is avoided: the
+// compiler in use then reads element 0 whatever the index.)
+__device__ __forceinline__ float f16_lo(uint32_t w) { return f16_to_f32((uint16_t)(w & 0xffffu)); }
+__device__ __forceinline__ float f16_hi(uint32_t w) { return f16_to_f32((uint16_t)(w >> 16)); }
+
 // Position of column c inside its 32-column group in pair order.
 __device__ __forceinline__ int pair_pos(int c) {
   return (c & ~31) + 2 * (c & 15) + ((c >> 4) & 1);
 }
 
-// x (bf16, [T][K]) -> xp (fp16, [T][K], pair order).  One thread per 16
-// columns: 8 columns c .. c+7 and their partners c+16 .. c+23 become the
-// pair dwords 8h .. 8h+7 of their group.
+// x (bf16, [T][K]) and s (fp16, [K]) -> xp = fp16(x .* s) ([T][K], pair
+// order).  The product of a bf16 and an fp16 value is exact in fp32, so
+// each entry is rounded once.  One thread per 16 columns: 8 columns
+// c .. c+7 and their partners c+16 .. c+23 become the pair dwords
+// 8h .. 8h+7 of their group.
 __device__ __forceinline__ void pair_order_unit(const uint16_t *__restrict__ x,
+                                                const uint16_t *__restrict__ sc,
                                                 uint16_t *__restrict__ xp, int K, int64_t u) {
   const int units_per_row = K / 16;
   const int t = (int)(u / units_per_row);
@@ -170,79 +176,51 @@ __device__ __forceinline__ void pair_order_unit(const uint16_t *__restrict__ x,
   const uint16_t *src = x + (size_t)t * K + c;
   const u32x4 lo = *reinterpret_cast<const u32x4 *>(src);
   const u32x4 hi = *reinterpret_cast<const u32x4 *>(src + 16);
+  const u32x4 slo = *reinterpret_cast<const u32x4 *>(sc + c);
+  const u32x4 shi = *reinterpret_cast<const u32x4 *>(sc + c + 16);
   uint32_t d[8];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    d[2 * e] = pack_f16x2(__uint_as_float(lo[e] << 16), __uint_as_float(hi[e] << 16));
-    d[2 * e + 1] = pack_f16x2(__uint_as_float(lo[e] & 0xffff0000u), __uint_as_float(hi[e] & 0xffff0000u));
+    const uint32_t sl = slo[e], sh = shi[e];
+    d[2 * e] = pack_f16x2(__uint_as_float(lo[e] << 16) * f16_lo(sl),
+                          __uint_as_float(hi[e] << 16) * f16_lo(sh));
+    d[2 * e + 1] = pack_f16x2(__uint_as_float(lo[e] & 0xffff0000u) * f16_hi(sl),
+                              __uint_as_float(hi[e] & 0xffff0000u) * f16_hi(sh));
   }
   uint4 *dst = reinterpret_cast<uint4 *>(xp + (size_t)t * K + (c & ~31) + 2 * (c & 15));
   dst[0] = make_uint4(d[0], d[1], d[2], d[3]);
   dst[1] = make_uint4(d[4], d[5], d[6], d[7]);
 }
 
-// Column scales (fp16, [K]) -> pair dwords: dword 16q + p holds columns
-// 32q + p (low half) and 32q + p + 16 (high half); columns from K up to
-// Kpad (a multiple of BK) are zero, so a partial last K step adds nothing.
-__device__ __forceinline__ void colscale_pair(const uint16_t *__restrict__ s,
-                                              uint32_t *__restrict__ out, int K, int d) {
-  const int c = (d >> 4) * 32 + (d & 15);
-  const uint32_t lo = c < K ? s[c] : 0u;
-  const uint32_t hi = c + 16 < K ? s[c + 16] : 0u;
-  out[d] = lo | (hi << 16);
-}
-
-// The three operand preparations of one call in one launch: blocks
-// [0, nbx) convert x, the next nb1 build the G1 column-scale pairs (s_in),
-// the last ones the G2 pairs (s_mid).
+// The A operand of G1: fp16(s_in .* x) in pair order.
 __global__ __launch_bounds__(256) void prep_kernel(const uint16_t *__restrict__ x,
-                                                   uint16_t *__restrict__ xp, int T, int n,
                                                    const uint16_t *__restrict__ s_in,
-                                                   uint32_t *__restrict__ cs1, int npad,
-                                                   const uint16_t *__restrict__ s_mid,
-                                                   uint32_t *__restrict__ cs2, int r, int rpad,
-                                                   int nbx, int nb1) {
-  const int blk = blockIdx.x;
-  if (blk < nbx) {
-    const int64_t u = (int64_t)blk * 256 + threadIdx.x;
-    if (u < (int64_t)T * (n / 16)) pair_order_unit(x, xp, n, u);
-  } else if (blk < nbx + nb1) {
-    const int d = (blk - nbx) * 256 + threadIdx.x;
-    if (d < npad / 2) colscale_pair(s_in, cs1, n, d);
-  } else {
-    const int d = (blk - nbx - nb1) * 256 + threadIdx.x;
-    if (d < rpad / 2) colscale_pair(s_mid, cs2, r, d);
-  }
+                                                   uint16_t *__restrict__ xp, int T, int n) {
+  const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (u < (int64_t)T * (n / 16)) pair_order_unit(x, s_in, xp, n, u);
 }
 
-// C = rowscale * (A_pairorder x (sign(W) * colscale)^T), in the forms listed
-// under Mode.
+// C = rowscale * (A_pairorder x sign(W)^T), in the forms listed under Mode.
 template <int kMode, int kBM, int kStages>
 __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     const uint16_t *__restrict__ A, int T, int K, const uint32_t *__restrict__ W, int N,
-    const uint32_t *__restrict__ cspairs, int Kpad, const uint16_t *__restrict__ rowscale,
-    uint16_t *__restrict__ C, const uint16_t *__restrict__ S, float *__restrict__ F,
-    const float *__restrict__ gscale) {
-  constexpr bool kPairOut = kMode == kMid || kMode == kBwdMid;
+    const uint16_t *__restrict__ rowscale, uint16_t *__restrict__ C, uint16_t *__restrict__ V,
+    const uint16_t *__restrict__ S, float *__restrict__ F, const float *__restrict__ gscale) {
+  constexpr bool kPairOut = kMode == kMid || kMode == kMidSave || kMode == kBwdMid;
   constexpr bool kBwd = kMode == kBwdMid || kMode == kBwdIn;
-  // The backward folds its column scales into A: its B operand is +-1 and
-  // no scale pairs are staged.
-  constexpr bool kUnitB = kBwd;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   using LM = Lds<kBM, kStages>;
   static_assert(kStages == 2 || kStages == 3, "pipeline depth");
-  constexpr int kA0 = LM::kA0, kW0 = LM::kW0, kCs0 = LM::kCs0, kATile = LM::kATileT;
+  constexpr int kA0 = LM::kA0, kW0 = LM::kW0, kATile = LM::kATileT;
   constexpr int kLdsBytes = LM::kBytes;
   constexpr int kTokBlocks = kBM / 32;          // 32-token MFMA blocks per wave
   constexpr int kACopies = kBM * kARow / 1024 / 4;  // 1 KiB copies per wave per step
-  // Copy instructions per wave per step.  With three stages every wave
-  // copies the column-scale pairs too (identical bytes), so the count is
-  // the same in all waves and one s_waitcnt leaves exactly the newest
-  // step's copies in flight.
-  constexpr int kCopiesPerStep = kACopies + 4 + (kUnitB ? 0 : 1);
+  // Copy instructions per wave per step (the same in every wave, so one
+  // s_waitcnt leaves exactly the newest step's copies in flight).
+  constexpr int kCopiesPerStep = kACopies + 4;
 
   // Tile assignment: consecutive workgroups land on consecutive XCDs; give
   // each XCD a contiguous range of tiles (weight-row tiles fastest).
@@ -260,7 +238,7 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   //  token rows 4j .. 4j+3 of the tile; lane l fills chunk position l mod 16
   //  of row 4j + l/16 with the chunk whose index is that position XOR the
   //  row's low four bits.  Columns past K read the next row or zeros; they
-  //  meet zero column scales.
+  //  meet zero B operands (sign words past the row end).
   int a_off[kACopies];
 #pragma unroll
   for (int jj = 0; jj < kACopies; ++jj) {
@@ -285,11 +263,6 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       copy16(as, lds + kA0 + buf * kATile + (kACopies * wave + jj) * 1024, a_off[jj]);
 #pragma unroll
     for (int i = 0; i < 4; ++i) copy4(ws, lds + kW0 + buf * kWTile + (64 * wave + 16 * i) * 16, w_off[i]);
-    if (!kUnitB && (kStages == 3 || wave == 0)) {
-      const i32x4 cs =
-          copy_rsrc(cspairs + step * (kCsTile / 4), (int64_t)Kpad * 2 - (int64_t)step * kCsTile);
-      copy4(cs, lds + kCs0 + buf * kCsTile, 4 * lane);
-    }
   };
 
   // No stale LDS pattern (possibly a NaN) may ever meet an MFMA, even in
@@ -345,16 +318,13 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     }
     const uint8_t *abase = lds + kA0 + buf * kATile;
     const uint4 *wt = reinterpret_cast<const uint4 *>(lds + kW0 + buf * kWTile);
-    const uint4 *cs = reinterpret_cast<const uint4 *>(lds + kCs0 + buf * kCsTile);
     const uint4 wq0 = wt[wrow_l], wq1 = wt[wrow_l + 32];
     const uint32_t wj[2][kWords] = {{wq0.x, wq0.y, wq0.z, wq0.w}, {wq1.x, wq1.y, wq1.z, wq1.w}};
     half8 af[2][kTokBlocks];
-    uint4 c4[2];
     auto read_ops = [&](int ks, int slot) {
 #pragma unroll
       for (int i = 0; i < kTokBlocks; ++i)
         af[slot][i] = *reinterpret_cast<const half8 *>(abase + a_rd[ks] + 32 * i * kARow);
-      if constexpr (!kUnitB) c4[slot] = cs[2 * ks + g];
     };
     read_ops(0, 0);
     static_for<2 * kWords>([&](auto KS) {
@@ -364,21 +334,14 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       // Keep the next step's LDS reads ahead of this step's MFMAs (the
       // scheduler would otherwise sink them next to their use).
       __builtin_amdgcn_sched_barrier(0);
-      uint32_t cpair[4];
-      if constexpr (kUnitB) {
-        // words past the row end (a partial last K step) meet +-0, as the
-        // zero scale-pair padding does in the forward modes
-        const uint32_t one = step * kWords + (ks >> 1) < kw ? kOnePair : 0u;
-        cpair[0] = cpair[1] = cpair[2] = cpair[3] = one;
-      } else {
-        cpair[0] = c4[cur].x; cpair[1] = c4[cur].y; cpair[2] = c4[cur].z; cpair[3] = c4[cur].w;
-      }
+      // words past the row end (a partial last K step) meet +-0
+      const uint32_t one = step * kWords + (ks >> 1) < kw ? kOnePair : 0u;
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const uint32_t w = wj[j][ks >> 1];
         uint32_t bd[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) bd[e] = cpair[e] ^ ((w << sh[ks & 1][e]) & kSignMask);
+        for (int e = 0; e < 4; ++e) bd[e] = one ^ ((w << sh[ks & 1][e]) & kSignMask);
         const uint4 bq = make_uint4(bd[0], bd[1], bd[2], bd[3]);
 #pragma unroll
         for (int i = 0; i < kTokBlocks; ++i)
@@ -488,7 +451,8 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
         const int t = t0 + 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
         if (t < T) {
           const float v = acc[i][j][e] * rs;
-          C[(size_t)t * N + cpos] = kMode == kMid ? f32_to_f16(v) : f32_to_bf16(v);
+          C[(size_t)t * N + cpos] = kPairOut ? f32_to_f16(v) : f32_to_bf16(v);
+          if constexpr (kMode == kMidSave) V[(size_t)t * N + cpos] = f32_to_f16(acc[i][j][e]);
           if constexpr (kMode == kOutSave) F[(size_t)t * N + n] = acc[i][j][e];
         }
       }
@@ -526,9 +490,9 @@ __global__ __launch_bounds__(256) void bwd_rowstat_kernel(const uint16_t *__rest
       for (int q = 0; q < 4; ++q)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const half2v sp = __builtin_bit_cast(half2v, so[q][e]);
-          const float a = fabsf(__uint_as_float(v[q][e] << 16) * (float)sp[0]);
-          const float b = fabsf(__uint_as_float(v[q][e] & 0xffff0000u) * (float)sp[1]);
+          const uint32_t sp = so[q][e];
+          const float a = fabsf(__uint_as_float(v[q][e] << 16) * f16_lo(sp));
+          const float b = fabsf(__uint_as_float(v[q][e] & 0xffff0000u) * f16_hi(sp));
           mx = fmaxf(mx, fmaxf(a, b));
           l1 += a + b;
         }
@@ -722,8 +686,6 @@ __global__ __launch_bounds__(256) void bwd_finish_kernel(
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
-int64_t kpad(int64_t K) { return (K + BK - 1) / BK * BK; }
-
 // Copy pipeline depth per token-tile height.
 #ifndef AF1_GEMM_STAGES_128
 #define AF1_GEMM_STAGES_128 2
@@ -742,7 +704,7 @@ constexpr int kStages64 = AF1_GEMM_STAGES_64;
 // receives the token-tile height used (the row count of F's per-tile sums).
 template <int kMode>
 hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *W, int64_t N,
-                       const uint32_t *cs, const uint16_t *rs, uint16_t *C, const uint16_t *S,
+                       const uint16_t *rs, uint16_t *C, uint16_t *V, const uint16_t *S,
                        float *F, hipStream_t s, int *tile_tokens = nullptr,
                        const float *gscale = nullptr) {
   const int cus = device_cus();
@@ -751,46 +713,35 @@ hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *
   if (tiles128 <= (int64_t)cus && T > 64) {
     dim3 g(gx, (unsigned)((T + 63) / 64));
     bingemm_kernel<kMode, 64, kStages64><<<g, kThreads, Lds<64, kStages64>::kBytes, s>>>(
-        A, (int)T, (int)K, W, (int)N, cs, (int)kpad(K), rs, C, S, F, gscale);
+        A, (int)T, (int)K, W, (int)N, rs, C, V, S, F, gscale);
     if (tile_tokens) *tile_tokens = 64;
   } else {
     dim3 g(gx, (unsigned)((T + BM - 1) / BM));
     bingemm_kernel<kMode, BM, kStages128><<<g, kThreads, Lds<BM, kStages128>::kBytes, s>>>(
-        A, (int)T, (int)K, W, (int)N, cs, (int)kpad(K), rs, C, S, F, gscale);
+        A, (int)T, (int)K, W, (int)N, rs, C, V, S, F, gscale);
     if (tile_tokens) *tile_tokens = BM;
   }
   return hipGetLastError();
 }
 
-// x -> pair-order fp16 and the two column-scale pair arrays, in one launch.
-hipError_t prepare_forward(int64_t n, int64_t r, const uint16_t *s_mid, const uint16_t *s_in,
-                           const uint16_t *x, int64_t T, uint16_t *xp, uint32_t *cs1,
-                           uint32_t *cs2, hipStream_t s) {
+// fp16(s_in .* x) in pair order, the A operand of G1.
+hipError_t prepare_forward(int64_t n, const uint16_t *s_in, const uint16_t *x, int64_t T,
+                           uint16_t *xp, hipStream_t s) {
   const int64_t units = T * (n / 16);
-  const int nbx = (int)((units + 255) / 256);
-  const int nb1 = (int)((kpad(n) / 2 + 255) / 256);
-  const int nb2 = (int)((kpad(r) / 2 + 255) / 256);
-  prep_kernel<<<(unsigned)(nbx + nb1 + nb2), 256, 0, s>>>(x, xp, (int)T, (int)n, s_in, cs1,
-                                                           (int)kpad(n), s_mid, cs2, (int)r,
-                                                           (int)kpad(r), nbx, nb1);
+  prep_kernel<<<(unsigned)((units + 255) / 256), 256, 0, s>>>(x, s_in, xp, (int)T, (int)n);
   return hipGetLastError();
 }
 
 struct FwdWs {
   uint16_t *xp, *Z;
-  uint32_t *cs1, *cs2;
 };
 
-FwdWs forward_ws(void *ws, int64_t n, int64_t r, int64_t T) {
+FwdWs forward_ws(void *ws, int64_t n, int64_t T) {
   uint8_t *base = static_cast<uint8_t *>(ws);
   FwdWs w;
   w.xp = reinterpret_cast<uint16_t *>(base);
   base += align256((size_t)T * n * 2);
   w.Z = reinterpret_cast<uint16_t *>(base);
-  base += align256((size_t)T * r * 2);
-  w.cs1 = reinterpret_cast<uint32_t *>(base);
-  base += align256((size_t)kpad(n) * 2);
-  w.cs2 = reinterpret_cast<uint32_t *>(base);
   return w;
 }
 
@@ -831,11 +782,8 @@ size_t backward_ws_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
 
 size_t gemm_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
   (void)m;
-  // fp16 x in pair order, the fp16 intermediate Z (pair order), and the two
-  // column-scale pair arrays (s_in for G1, s_mid for G2), zero-padded to
-  // whole K steps
-  return align256((size_t)T * (size_t)n * 2) + align256((size_t)T * (size_t)r * 2) +
-         align256((size_t)kpad(n) * 2) + align256((size_t)kpad(r) * 2);
+  // fp16(s_in .* x) and the fp16 intermediate Z, both in pair order
+  return align256((size_t)T * (size_t)n * 2) + align256((size_t)T * (size_t)r * 2);
 }
 
 hipError_t launch_gemm(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
@@ -847,12 +795,12 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
   if (T * n * 2 > 0x7fffffff || T * r * 2 > 0x7fffffff || m * (r / 32) * 4 > 0x7fffffff ||
       r * (n / 32) * 4 > 0x7fffffff)
     return hipErrorInvalidValue;
-  const FwdWs w = forward_ws(ws, n, r, T);
-  hipError_t e = prepare_forward(n, r, s_mid, s_in, x, T, w.xp, w.cs1, w.cs2, s);
+  const FwdWs w = forward_ws(ws, n, T);
+  hipError_t e = prepare_forward(n, s_in, x, T, w.xp, s);
   if (e != hipSuccess) return e;
-  e = contraction<kMid>(w.xp, T, n, Bv, r, w.cs1, nullptr, w.Z, nullptr, nullptr, s);
+  e = contraction<kMid>(w.xp, T, n, Bv, r, s_mid, w.Z, nullptr, nullptr, nullptr, s);
   if (e != hipSuccess) return e;
-  return contraction<kOut>(w.Z, T, r, Bu, m, w.cs2, s_out, y, nullptr, nullptr, s);
+  return contraction<kOut>(w.Z, T, r, Bu, m, s_out, y, nullptr, nullptr, nullptr, s);
 }
 
 size_t train_saved_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
@@ -875,14 +823,15 @@ hipError_t launch_forward_train(int64_t m, int64_t n, int64_t r, const uint32_t 
   if (T * n * 2 > 0x7fffffff || T * r * 2 > 0x7fffffff || m * (r / 32) * 4 > 0x7fffffff ||
       r * (n / 32) * 4 > 0x7fffffff)
     return hipErrorInvalidValue;
-  const FwdWs w = forward_ws(ws, n, r, T);
+  const FwdWs w = forward_ws(ws, n, T);
   uint16_t *v = static_cast<uint16_t *>(saved);
   float *z = reinterpret_cast<float *>(static_cast<uint8_t *>(saved) + align256((size_t)T * r * 2));
-  hipError_t e = prepare_forward(n, r, s_mid, s_in, x, T, w.xp, w.cs1, w.cs2, s);
+  hipError_t e = prepare_forward(n, s_in, x, T, w.xp, s);
   if (e != hipSuccess) return e;
-  e = contraction<kMid>(w.xp, T, n, Bv, r, w.cs1, nullptr, v, nullptr, nullptr, s);
+  // the same G1 as the inference forward, which also keeps fp16(v)
+  e = contraction<kMidSave>(w.xp, T, n, Bv, r, s_mid, w.Z, v, nullptr, nullptr, s);
   if (e != hipSuccess) return e;
-  return contraction<kOutSave>(v, T, r, Bu, m, w.cs2, s_out, y, nullptr, z, s);
+  return contraction<kOutSave>(w.Z, T, r, Bu, m, s_out, y, nullptr, nullptr, z, s);
 }
 
 hipError_t launch_backward(int64_t m, int64_t n, int64_t r, const uint32_t *BuT,
@@ -912,11 +861,11 @@ hipError_t launch_backward(int64_t m, int64_t n, int64_t r, const uint32_t *BuT,
   // the output fp16(s_mid .* dt 2^(e - c)) in pair order is the next A
   // operand; sums dt .* v.
   int tm = 0, ti = 0;
-  e = contraction<kBwdMid>(w.A1, T, m, BuT, r, nullptr, s_mid, w.Zb, v, w.p_mid, s, &tm,
+  e = contraction<kBwdMid>(w.A1, T, m, BuT, r, s_mid, w.Zb, nullptr, v, w.p_mid, s, &tm,
                            w.gscale);
   if (e != hipSuccess) return e;
   // du 2^(e - c) = Bv^T (s_mid .* dt 2^(e - c)): dx = s_in .* du; sums du .* x.
-  e = contraction<kBwdIn>(w.Zb, T, r, BvT, n, nullptr, s_in, dx, x, w.p_in, s, &ti, w.gscale);
+  e = contraction<kBwdIn>(w.Zb, T, r, BvT, n, s_in, dx, nullptr, x, w.p_in, s, &ti, w.gscale);
   if (e != hipSuccess) return e;
   const int total = (int)(m + r + n);
   bwd_finish_kernel<<<(unsigned)((total + kFinishCols - 1) / kFinishCols), 256, 0, s>>>(

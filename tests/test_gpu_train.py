@@ -169,6 +169,19 @@ def test_backward_tokens_of_very_different_magnitudes(oracle):
     check_against_oracle(oracle, lin, dy)
 
 
+def test_backward_output_scales_that_differ_between_neighbouring_columns(oracle):
+    """s_out 2^10 larger on six of every eight columns: the per-group
+    exponents must see the scale of every column (an estimate from some
+    columns of each 16-byte chunk would overflow fp16 here)."""
+    m, n, r, T = 512, 768, 224, 130
+    lin = synth.make_linear(91, m, n, r, T)
+    so = lin.s_out.view(np.float16).astype(np.float32)
+    so[(np.arange(m) % 8) >= 2] *= 1024.0
+    lin.s_out = so.astype(np.float16).view(np.uint16)
+    dy = synth.make_output_grad(92, T, m)
+    check_against_oracle(oracle, lin, dy)
+
+
 def test_backward_accumulate_skip_dx_and_repeat_are_exact():
     m, n, r, T = 1024, 1024, 480, 200
     lin = synth.make_linear(91, m, n, r, T)
