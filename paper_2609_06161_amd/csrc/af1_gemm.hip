@@ -372,7 +372,45 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   }
 
   // Epilogue.  32x32 accumulator layout: lane l holds column (l mod 32) and
-  // rows 8*(e/4) + 4*(l/32) + (e mod 4), e = 0..15.
+  // rows 8*(e/4) + 4*(l/32) + (e mod 4), e = 0..15.  A 16-bit output tile (kBM tokens x 256 columns, 512 bytes a
+  // token) is assembled in the idle activation buffers and leaves in
+  // 16-byte stores, 512 contiguous bytes per token row; a token row's
+  // 16-byte chunk c sits at position c XOR 4 * ((row / 4) mod 2), so that
+  // the two lane halves (tokens four apart) write distinct banks.  kMidSave
+  // passes its second output V through the same buffer after C.
+  float rs[2];
+  int cpos[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int n = wrow0 + 32 * j;
+    rs[j] = n < N ? (rowscale ? f16_to_f32(rowscale[n]) : 1.0f) : 0.f;
+    cpos[j] = (kPairOut ? pair_pos(n) : n) - n0;
+  }
+  auto stage_tile = [&](auto value) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int cbyte = 2 * (cpos[j] & 7), chunk = (cpos[j] >> 3) ^ (4 * g);
+#pragma unroll
+      for (int i = 0; i < kTokBlocks; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int row = 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
+          *reinterpret_cast<uint16_t *>(lds + row * 512 + chunk * 16 + cbyte) = value(i, j, e);
+        }
+    }
+    __syncthreads();
+  };
+  auto store_tile = [&](uint16_t *__restrict__ dst) {
+    const int chunk = tid & 31;
+    const bool col_ok = n0 + 8 * chunk < N;
+#pragma unroll 4
+    for (int row = tid >> 5; row < kBM; row += kThreads / 32) {
+      const uint4 v = *reinterpret_cast<const uint4 *>(lds + row * 512 +
+                                                       ((chunk ^ (4 * ((row >> 2) & 1))) << 4));
+      if (col_ok && t0 + row < T)
+        *reinterpret_cast<uint4 *>(dst + (size_t)(t0 + row) * N + n0 + 8 * chunk) = v;
+    }
+  };
   if constexpr (kBwd) {
     // The S block of this tile (kBM tokens x 256 weight rows, 512 bytes a
     // token) goes into the idle activation buffers with LDS copies, two
@@ -421,62 +459,17 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
         }
       part += __shfl_xor(part, 32, 64);
       if (g == 0 && n < N) F[(size_t)(t0 / kBM) * N + n] = part;
-      if (n >= N || !C) continue;
-      const float rs = f16_to_f32(rowscale[n]);
-#pragma unroll
-      for (int i = 0; i < kTokBlocks; ++i)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int t = t0 + 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
-          if (t < T) {
-            if constexpr (kMode == kBwdMid)
-              C[(size_t)t * N + pair_pos(n)] = f32_to_f16(acc[i][j][e] * rs * fz[i]);
-            else
-              C[(size_t)t * N + n] = f32_to_bf16(acc[i][j][e] * fg[i] * rs);
-          }
-        }
+    }
+    if (C) {  // uniform: dx may be skipped
+      __syncthreads();  // every wave is done with the S block
+      stage_tile([&](int i, int j, int e) {
+        if constexpr (kMode == kBwdMid) return f32_to_f16(acc[i][j][e] * rs[j] * fz[i]);
+        else return f32_to_bf16(acc[i][j][e] * fg[i] * rs[j]);
+      });
+      store_tile(C);
     }
     return;
   }
-  // Forward epilogue.  The 16-bit C tile (kBM tokens x 256 columns, 512
-  // bytes a token) is assembled in the idle activation buffers and leaves
-  // in 16-byte stores, 512 contiguous bytes per token row; a token row's
-  // 16-byte chunk c sits at position c XOR 4 * ((row / 4) mod 2), so that
-  // the two lane halves (tokens four apart) write distinct banks.  kMidSave
-  // passes its second output V through the same buffer after C.
-  float rs[2];
-  int cpos[2];
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int n = wrow0 + 32 * j;
-    rs[j] = n < N ? (rowscale ? f16_to_f32(rowscale[n]) : 1.0f) : 0.f;
-    cpos[j] = (kPairOut ? pair_pos(n) : n) - n0;
-  }
-  auto stage_tile = [&](auto value) {
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int cbyte = 2 * (cpos[j] & 7), chunk = (cpos[j] >> 3) ^ (4 * g);
-#pragma unroll
-      for (int i = 0; i < kTokBlocks; ++i)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int row = 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
-          *reinterpret_cast<uint16_t *>(lds + row * 512 + chunk * 16 + cbyte) = value(i, j, e);
-        }
-    }
-    __syncthreads();
-  };
-  auto store_tile = [&](uint16_t *__restrict__ dst) {
-    const int chunk = tid & 31;
-    const bool col_ok = n0 + 8 * chunk < N;
-#pragma unroll 4
-    for (int row = tid >> 5; row < kBM; row += kThreads / 32) {
-      const uint4 v = *reinterpret_cast<const uint4 *>(lds + row * 512 +
-                                                       ((chunk ^ (4 * ((row >> 2) & 1))) << 4));
-      if (col_ok && t0 + row < T)
-        *reinterpret_cast<uint4 *>(dst + (size_t)(t0 + row) * N + n0 + 8 * chunk) = v;
-    }
-  };
   stage_tile([&](int i, int j, int e) {
     const float v = acc[i][j][e] * rs[j];
     return kPairOut ? f32_to_f16(v) : f32_to_bf16(v);
