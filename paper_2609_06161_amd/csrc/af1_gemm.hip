@@ -205,7 +205,8 @@ template <int kMode, int kBM, int kStages>
 __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     const uint16_t *__restrict__ A, int T, int K, const uint32_t *__restrict__ W, int N,
     const uint16_t *__restrict__ rowscale, uint16_t *__restrict__ C, uint16_t *__restrict__ V,
-    const uint16_t *__restrict__ S, float *__restrict__ F, const float *__restrict__ gscale) {
+    const uint16_t *__restrict__ S, float *__restrict__ F, const float *__restrict__ gscale,
+    int split_steps, float *__restrict__ P) {
   constexpr bool kPairOut = kMode == kMid || kMode == kMidSave || kMode == kBwdMid;
   constexpr bool kBwd = kMode == kBwdMid || kMode == kBwdIn;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
@@ -231,7 +232,12 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   const int n0 = (L % nN) * BN;
 
   const int kw = K / 32;                       // sign words per row
-  const int nk = (kw + kWords - 1) / kWords;   // K steps (the last may be partial)
+  // K steps of this workgroup: all of them, or with a split K (grid z > 1,
+  // forward modes only) the range of split blockIdx.z; the last step of the
+  // row may be partial.
+  const int nk_row = (kw + kWords - 1) / kWords;
+  const int k0 = gridDim.z > 1 ? (int)blockIdx.z * split_steps : 0;
+  const int nk = gridDim.z > 1 ? min(nk_row, k0 + split_steps) : nk_row;
 
   // Copy roles, fixed per lane (a step only moves the resources' bases).
   //  Activations: wave w issues copies j = kACopies*w + jj, each covering
@@ -270,8 +276,8 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   for (int o = tid * 16; o < kLdsBytes; o += kThreads * 16)
     *reinterpret_cast<uint4 *>(lds + o) = make_uint4(0u, 0u, 0u, 0u);
   __syncthreads();
-  issue(0, 0);
-  if (kStages == 3 && nk > 1) issue(1, 1);
+  issue(k0, 0);
+  if (kStages == 3 && k0 + 1 < nk) issue(k0 + 1, 1);
 
   // This lane's weight rows: block j -> tile row 64*wave + 32*j + (l mod 32).
   const int wrow_l = 64 * wave + (lane & 31);
@@ -301,7 +307,7 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   asm volatile("v_mov_b32 %0, 0x80008000" : "=v"(kSignMask));
   constexpr uint32_t kOnePair = 0x3c003c00u;  // fp16 +1, +1
 
-  if (kStages == 3 && nk > 1)
+  if (kStages == 3 && k0 + 1 < nk)
     wait_copies_but<kCopiesPerStep>();
   else
     wait_copies();
@@ -359,12 +365,12 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   };
 
   if constexpr (kStages == 2) {
-    for (int step = 0; step < nk; step += 2) {
+    for (int step = k0; step < nk; step += 2) {
       run_step(step, std::integral_constant<int, 0>{});
       if (step + 1 < nk) run_step(step + 1, std::integral_constant<int, 1>{});
     }
   } else {
-    for (int step = 0; step < nk; step += 3) {
+    for (int step = k0; step < nk; step += 3) {
       run_step(step, std::integral_constant<int, 0>{});
       if (step + 1 < nk) run_step(step + 1, std::integral_constant<int, 1>{});
       if (step + 2 < nk) run_step(step + 2, std::integral_constant<int, 2>{});
@@ -372,11 +378,33 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   }
 
   // Epilogue.  32x32 accumulator layout: lane l holds column (l mod 32) and
-  // rows 8*(e/4) + 4*(l/32) + (e mod 4), e = 0..15.  A 16-bit output tile (kBM tokens x 256 columns, 512 bytes a
-  // token) is assembled in the idle activation buffers and leaves in
-  // 16-byte stores, 512 contiguous bytes per token row; a token row's
-  // 16-byte chunk c sits at position c XOR 4 * ((row / 4) mod 2), so that
-  // the two lane halves (tokens four apart) write distinct banks.  kMidSave
+  // rows 8*(e/4) + 4*(l/32) + (e mod 4), e = 0..15.
+  if constexpr (!kBwd) {
+    if (gridDim.z > 1) {
+      // Split K: the fp32 partial of this tile over the workgroup's K steps,
+      // natural column order; splitk_reduce_kernel adds the partials and
+      // applies the mode's epilogue.
+      float *__restrict__ Ps = P + (size_t)blockIdx.z * T * N;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int n = wrow0 + 32 * j;
+        if (n >= N) continue;
+#pragma unroll
+        for (int i = 0; i < kTokBlocks; ++i)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int t = t0 + 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
+            if (t < T) Ps[(size_t)t * N + n] = acc[i][j][e];
+          }
+      }
+      return;
+    }
+  }
+  // A 16-bit output tile (kBM tokens x 256 columns, 512 bytes a token) is
+  // assembled in the idle activation buffers and leaves in 16-byte stores,
+  // 512 contiguous bytes per token row; a token row's 16-byte chunk c sits
+  // at position c XOR 4 * ((row / 4) mod 2), so that the two lane halves
+  // (tokens four apart) write distinct banks.  kMidSave
   // passes its second output V through the same buffer after C.
   float rs[2];
   int cpos[2];
@@ -720,6 +748,75 @@ __global__ __launch_bounds__(256) void bwd_finish_kernel(
   }
 }
 
+// The reduction of a split-K contraction (forward modes): C and its
+// companions from the S fp32 partials of the workgroups along K, added in
+// split order.  A thread takes 8 consecutive output positions of one token:
+// in pair order (kMid, kMidSave) positions 8u .. 8u+7 of a 32-column group
+// hold columns c0 .. c0+3 and c0+16 .. c0+19, interleaved.
+template <int kMode>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *__restrict__ P, int S,
+                                                            int T, int N,
+                                                            const uint16_t *__restrict__ rowscale,
+                                                            uint16_t *__restrict__ C,
+                                                            uint16_t *__restrict__ V,
+                                                            float *__restrict__ F) {
+  constexpr bool kPairOut = kMode == kMid || kMode == kMidSave;
+  const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int upr = N / 8;
+  if (u >= (int64_t)T * upr) return;
+  const int t = (int)(u / upr);
+  const int p = (int)(u % upr) * 8;  // first output position
+  int cl, ch;                        // columns of the two float4 runs
+  if (kPairOut) {
+    cl = (p & ~31) + ((p & 31) >> 1);
+    ch = cl + 16;
+  } else {
+    cl = p;
+    ch = p + 4;
+  }
+  float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
+  for (int sp = 0; sp < S; ++sp) {
+    const float *row = P + ((size_t)sp * T + t) * N;
+    const float4 a = *reinterpret_cast<const float4 *>(row + cl);
+    const float4 b = *reinterpret_cast<const float4 *>(row + ch);
+    lo.x += a.x; lo.y += a.y; lo.z += a.z; lo.w += a.w;
+    hi.x += b.x; hi.y += b.y; hi.z += b.z; hi.w += b.w;
+  }
+  // output k of the 8: pair order interleaves the runs, natural order
+  // concatenates them
+  const float l4[4] = {lo.x, lo.y, lo.z, lo.w}, h4[4] = {hi.x, hi.y, hi.z, hi.w};
+  float acc[8];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    acc[kPairOut ? 2 * k : k] = l4[k];
+    acc[kPairOut ? 2 * k + 1 : 4 + k] = h4[k];
+  }
+  uint32_t c[4], v[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    int col0, col1;
+    if (kPairOut) {
+      col0 = cl + k;
+      col1 = ch + k;
+    } else {
+      col0 = p + 2 * k;
+      col1 = p + 2 * k + 1;
+    }
+    const float r0 = f16_to_f32(rowscale[col0]), r1 = f16_to_f32(rowscale[col1]);
+    const float a0 = acc[2 * k] * r0, a1 = acc[2 * k + 1] * r1;
+    c[k] = kPairOut ? (uint32_t)f32_to_f16(a0) | ((uint32_t)f32_to_f16(a1) << 16)
+                    : (uint32_t)f32_to_bf16(a0) | ((uint32_t)f32_to_bf16(a1) << 16);
+    v[k] = (uint32_t)f32_to_f16(acc[2 * k]) | ((uint32_t)f32_to_f16(acc[2 * k + 1]) << 16);
+  }
+  const size_t o = (size_t)t * N + p;
+  *reinterpret_cast<uint4 *>(C + o) = make_uint4(c[0], c[1], c[2], c[3]);
+  if constexpr (kMode == kMidSave) *reinterpret_cast<uint4 *>(V + o) = make_uint4(v[0], v[1], v[2], v[3]);
+  if constexpr (kMode == kOutSave) {
+    *reinterpret_cast<float4 *>(F + o) = lo;
+    *reinterpret_cast<float4 *>(F + o + 4) = hi;
+  }
+}
+
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
 // Copy pipeline depth per token-tile height.
@@ -732,30 +829,85 @@ size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 constexpr int kStages128 = AF1_GEMM_STAGES_128;
 constexpr int kStages64 = AF1_GEMM_STAGES_64;
 
-// One contraction C[T, N] over K on the stream.  A grid of 128-token tiles
-// that gives each compute unit at most one workgroup (one wave per SIMD)
-// uses 64-token tiles instead: twice the workgroups, each expanding its
-// signs for half as many tokens.  Measured on 8192x8192 G1 (+2%); grids
-// between one and two workgroups per unit were slower with it.  *tile_tokens
-// receives the token-tile height used (the row count of F's per-tile sums).
+// How one contraction is launched.  A grid of 128-token tiles that gives
+// each compute unit at most one workgroup (one wave per SIMD) uses 64-token
+// tiles instead: twice the workgroups, each expanding its signs for half as
+// many tokens (measured on 8192x8192 G1: +2%; grids between one and two
+// workgroups per unit were slower with it).  A forward grid that still
+// leaves compute units idle (few tokens) may split its K steps over grid z
+// (at least kMinSplitSteps steps per split); splitk_reduce_kernel then adds
+// the fp32 partials in split order.  The split count minimises a simple
+// cost: K steps per workgroup times the waves of workgroups (two per unit),
+// plus, when split, the partials written and read back and one more launch.
+// The constants are measured: a K step of a workgroup with the unit nearly
+// to itself takes about 1.5 us at these grid sizes, partials move at about
+// 4 TB/s, and the reduction launch costs about 3 us.
+constexpr int kMinSplitSteps = 2;
+constexpr double kStepUs = 1.5, kPartialBytesPerUs = 4.0e6, kLaunchUs = 3.0;
+struct ContractionPlan {
+  int bm;                // token-tile height
+  unsigned gx, gy;       // weight-row tiles, token tiles
+  int splits, split_steps;
+};
+
+ContractionPlan plan_contraction(int64_t T, int64_t K, int64_t N, bool allow_split, int cus) {
+  ContractionPlan p;
+  p.gx = (unsigned)((N + BN - 1) / BN);
+  const int64_t tiles128 = (int64_t)p.gx * ((T + BM - 1) / BM);
+  p.bm = tiles128 <= (int64_t)cus && T > 64 ? 64 : BM;
+  p.gy = (unsigned)((T + p.bm - 1) / p.bm);
+  const int64_t nk = (K / 32 + kWords - 1) / kWords;
+  p.splits = 1;
+  p.split_steps = (int)nk;
+  const int64_t tiles = (int64_t)p.gx * p.gy;
+  if (allow_split && tiles < cus) {
+    auto cost = [&](int64_t sp) {
+      const int64_t steps = (nk + sp - 1) / sp;
+      const int64_t waves = (tiles * sp + 2 * cus - 1) / (2 * cus);
+      double us = (double)(steps * waves) * kStepUs;
+      if (sp > 1) us += 2.0 * (double)sp * T * N * 4 / kPartialBytesPerUs + kLaunchUs;
+      return us;
+    };
+    int64_t best = 1;
+    for (int64_t sp = 2; sp <= nk / kMinSplitSteps; ++sp)
+      if (cost(sp) < cost(best)) best = sp;
+    if (best > 1) {
+      p.split_steps = (int)((nk + best - 1) / best);
+      p.splits = (int)((nk + p.split_steps - 1) / p.split_steps);
+    }
+  }
+  return p;
+}
+
+size_t split_bytes(const ContractionPlan &p, int64_t T, int64_t N) {
+  return p.splits > 1 ? align256((size_t)p.splits * T * N * 4) : 0;
+}
+
+// One contraction C[T, N] over K on the stream.  P: fp32 workspace for a
+// split K (forward modes; nullptr never splits).  *tile_tokens receives the
+// token-tile height used (the row count of F's per-tile sums).
 template <int kMode>
 hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *W, int64_t N,
                        const uint16_t *rs, uint16_t *C, uint16_t *V, const uint16_t *S,
                        float *F, hipStream_t s, int *tile_tokens = nullptr,
-                       const float *gscale = nullptr) {
-  const int cus = device_cus();
-  const unsigned gx = (unsigned)((N + BN - 1) / BN);
-  const int64_t tiles128 = (int64_t)gx * ((T + BM - 1) / BM);
-  if (tiles128 <= (int64_t)cus && T > 64) {
-    dim3 g(gx, (unsigned)((T + 63) / 64));
+                       const float *gscale = nullptr, float *P = nullptr) {
+  const ContractionPlan p = plan_contraction(T, K, N, P != nullptr, device_cus());
+  const dim3 g(p.gx, p.gy, (unsigned)p.splits);
+  if (p.bm == 64)
     bingemm_kernel<kMode, 64, kStages64><<<g, kThreads, Lds<64, kStages64>::kBytes, s>>>(
-        A, (int)T, (int)K, W, (int)N, rs, C, V, S, F, gscale);
-    if (tile_tokens) *tile_tokens = 64;
-  } else {
-    dim3 g(gx, (unsigned)((T + BM - 1) / BM));
+        A, (int)T, (int)K, W, (int)N, rs, C, V, S, F, gscale, p.split_steps, P);
+  else
     bingemm_kernel<kMode, BM, kStages128><<<g, kThreads, Lds<BM, kStages128>::kBytes, s>>>(
-        A, (int)T, (int)K, W, (int)N, rs, C, V, S, F, gscale);
-    if (tile_tokens) *tile_tokens = BM;
+        A, (int)T, (int)K, W, (int)N, rs, C, V, S, F, gscale, p.split_steps, P);
+  if (tile_tokens) *tile_tokens = p.bm;
+  if (p.splits > 1) {
+    if constexpr (kMode == kMid || kMode == kMidSave || kMode == kOut || kMode == kOutSave) {
+      const int64_t units = T * (N / 8);
+      splitk_reduce_kernel<kMode><<<(unsigned)((units + 255) / 256), 256, 0, s>>>(
+          P, p.splits, (int)T, (int)N, rs, C, V, F);
+    } else {
+      return hipErrorInvalidValue;  // the backward modes never split
+    }
   }
   return hipGetLastError();
 }
@@ -770,14 +922,17 @@ hipError_t prepare_forward(int64_t n, const uint16_t *s_in, const uint16_t *x, i
 
 struct FwdWs {
   uint16_t *xp, *Z;
+  float *P;  // split-K partials of G1 or G2 (one at a time)
 };
 
-FwdWs forward_ws(void *ws, int64_t n, int64_t T) {
+FwdWs forward_ws(void *ws, int64_t n, int64_t r, int64_t T) {
   uint8_t *base = static_cast<uint8_t *>(ws);
   FwdWs w;
   w.xp = reinterpret_cast<uint16_t *>(base);
   base += align256((size_t)T * n * 2);
   w.Z = reinterpret_cast<uint16_t *>(base);
+  base += align256((size_t)T * r * 2);
+  w.P = reinterpret_cast<float *>(base);
   return w;
 }
 
@@ -817,9 +972,13 @@ size_t backward_ws_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
 }  // namespace
 
 size_t gemm_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
-  (void)m;
-  // fp16(s_in .* x) and the fp16 intermediate Z, both in pair order
-  return align256((size_t)T * (size_t)n * 2) + align256((size_t)T * (size_t)r * 2);
+  // fp16(s_in .* x) and the fp16 intermediate Z, both in pair order, and the
+  // fp32 partials of whichever contraction splits its K steps
+  const int cus = device_cus();
+  const size_t p1 = split_bytes(plan_contraction(T, n, r, true, cus), T, r);
+  const size_t p2 = split_bytes(plan_contraction(T, r, m, true, cus), T, m);
+  return align256((size_t)T * (size_t)n * 2) + align256((size_t)T * (size_t)r * 2) +
+         (p1 > p2 ? p1 : p2);
 }
 
 hipError_t launch_gemm(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
@@ -831,12 +990,14 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
   if (T * n * 2 > 0x7fffffff || T * r * 2 > 0x7fffffff || m * (r / 32) * 4 > 0x7fffffff ||
       r * (n / 32) * 4 > 0x7fffffff)
     return hipErrorInvalidValue;
-  const FwdWs w = forward_ws(ws, n, T);
+  const FwdWs w = forward_ws(ws, n, r, T);
   hipError_t e = prepare_forward(n, s_in, x, T, w.xp, s);
   if (e != hipSuccess) return e;
-  e = contraction<kMid>(w.xp, T, n, Bv, r, s_mid, w.Z, nullptr, nullptr, nullptr, s);
+  e = contraction<kMid>(w.xp, T, n, Bv, r, s_mid, w.Z, nullptr, nullptr, nullptr, s, nullptr,
+                        nullptr, w.P);
   if (e != hipSuccess) return e;
-  return contraction<kOut>(w.Z, T, r, Bu, m, s_out, y, nullptr, nullptr, nullptr, s);
+  return contraction<kOut>(w.Z, T, r, Bu, m, s_out, y, nullptr, nullptr, nullptr, s, nullptr,
+                           nullptr, w.P);
 }
 
 size_t train_saved_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
@@ -859,15 +1020,17 @@ hipError_t launch_forward_train(int64_t m, int64_t n, int64_t r, const uint32_t 
   if (T * n * 2 > 0x7fffffff || T * r * 2 > 0x7fffffff || m * (r / 32) * 4 > 0x7fffffff ||
       r * (n / 32) * 4 > 0x7fffffff)
     return hipErrorInvalidValue;
-  const FwdWs w = forward_ws(ws, n, T);
+  const FwdWs w = forward_ws(ws, n, r, T);
   uint16_t *v = static_cast<uint16_t *>(saved);
   float *z = reinterpret_cast<float *>(static_cast<uint8_t *>(saved) + align256((size_t)T * r * 2));
   hipError_t e = prepare_forward(n, s_in, x, T, w.xp, s);
   if (e != hipSuccess) return e;
   // the same G1 as the inference forward, which also keeps fp16(v)
-  e = contraction<kMidSave>(w.xp, T, n, Bv, r, s_mid, w.Z, v, nullptr, nullptr, s);
+  e = contraction<kMidSave>(w.xp, T, n, Bv, r, s_mid, w.Z, v, nullptr, nullptr, s, nullptr,
+                            nullptr, w.P);
   if (e != hipSuccess) return e;
-  return contraction<kOutSave>(w.Z, T, r, Bu, m, s_out, y, nullptr, nullptr, z, s);
+  return contraction<kOutSave>(w.Z, T, r, Bu, m, s_out, y, nullptr, nullptr, z, s, nullptr,
+                               nullptr, w.P);
 }
 
 hipError_t launch_backward(int64_t m, int64_t n, int64_t r, const uint32_t *BuT,

@@ -394,6 +394,24 @@ def test_gemm_full_size_sampled_tokens(oracle, name):
     assert err <= TOL
 
 
+@pytest.mark.parametrize("m,n,r,T", [(4096, 4096, 2016, 17), (4096, 4096, 2016, 100),
+                                     (4096, 14336, 3136, 33), (14336, 4096, 3136, 48),
+                                     (1056, 2080, 4064, 3)])
+def test_gemm_split_k_few_tokens(oracle, m, n, r, T):
+    """Token counts whose tile grid leaves most compute units idle: the
+    contractions split their K steps over several workgroups (partial last
+    step included: 2016/32 = 63 and 4064/32 = 127 words) and a second launch
+    adds the partials in split order.  Element-wise against the oracle, and
+    bit-identical on a repeat."""
+    lin = synth.make_linear(3000 + m + r + T, m, n, r, T)
+    y = gpu_gemm(lin)
+    ref = oracle_y(oracle, lin)
+    assert max_row_rel_l2(y, ref) <= TOL
+    ok, where = elementwise_ok(y, ref, rel=2 ** -6, abs_rms=6e-3)
+    assert ok, where
+    assert np.array_equal(y, gpu_gemm(lin))
+
+
 def test_gemm_matches_gemv_rows(oracle):
     lin = synth.make_linear(23, 4096, 4096, 2016, 16)
     a = gpu_gemm(lin)
