@@ -306,6 +306,27 @@ def bench_gemm(args, torch, stream):
     out["attn4096_r5120_2.5bpw"] = dict(m=m, n=n, r=r, T=T, us=ms * 1e3,
                                         tflops=2.0 * T * r * (m + n) / (ms * 1e-3) / 1e12)
     del L, x, y, ws
+    # Context: the prefill regime below 2048 tokens (chunked prefill), where
+    # the tile grid alone would leave compute units idle and the
+    # contractions split K; µs per call at 4096^2 and 8192^2.
+    sweep = {}
+    for name in ("attn4096", "sq8192"):
+        m, n, r = shape_of(name)
+        lin = synth.make_linear(57, m, n, r, 512)
+        L = DeviceLayer.from_host(lin)
+        for T in (32, 128, 512):
+            x = to_device(lin.x[:T])
+            y = torch.empty((T, m), dtype=torch.int16, device="cuda")
+            ws = torch.empty(af1.af1_gemm_workspace_bytes(m, n, r, T), dtype=torch.uint8,
+                             device="cuda")
+            fn = lambda i: L.gemm(x, y, ws, stream)
+            sustain(fn, stream, min(args.sustain, 0.1))
+            ms = time_events(fn, args.gemm_steps, stream) / args.gemm_steps
+            sweep[f"{name}_T{T}"] = dict(us=round(ms * 1e3, 1),
+                                         tflops=round(2.0 * T * r * (m + n) / (ms * 1e-3) / 1e12, 1))
+            del x, y, ws
+        del L
+    out["few_tokens"] = sweep
     # MFMA roofline of the prefill leg: algorithmic flops 2*T*r*(m+n) of the
     # three calls over their summed time, against the dense fp16 peak (the
     # contractions run on fp16 operands).

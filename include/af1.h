@@ -171,8 +171,11 @@ AF1_API af1_status af1_linear_gemv_multi(const af1_factorized_linear *Ls, int32_
  *        kernels address operands with 32-bit byte offsets); otherwise
  *        AF1_ERR_BATCH.  A sign matrix of 2 GiB or more is AF1_ERR_SHAPE.
  *   ws : device workspace of at least af1_gemm_workspace_bytes(m, n, r, T)
- *        bytes; holds the fp16 operand s_in .* x and the [T, r]
- *        intermediate.
+ *        bytes; holds the fp16 operand s_in .* x, the [T, r] intermediate
+ *        and, for token counts whose tile grid would leave compute units
+ *        idle, the fp32 partial sums of a contraction split along K (added
+ *        in a fixed order, so results repeat bit for bit).  The size depends
+ *        on the current device's compute-unit count.
  * Arithmetic: both products run on fp16 MFMA with fp32 accumulation against
  * exact +-1 sign operands; each scale vector is applied outside them.
  * s_in .* x is rounded once to fp16 (the bf16 x fp16 product is exact in
