@@ -37,15 +37,21 @@
 // with the LDS destination), double-buffered: a K step issues the copies of
 // the next step, runs its MFMAs, waits for its copies and meets one
 // barrier (a three-buffer variant, two steps ahead, is a template option;
-// it measured slower).  No staging registers are needed, which leaves room to read the
-// next MFMA step's operands from LDS while the current one runs.  An LDS
+// it measured slower).  No staging registers are needed, which leaves room
+// to read the next MFMA step's operands from LDS while the current one
+// runs.  An LDS
 // copy instruction writes 64 consecutive 16-byte chunks, one per lane, but
 // each lane chooses its source: the chunk of token row t holding columns
 // 8c .. 8c+7 of the step is stored at chunk position c XOR (t mod 16) of the
 // row, so that the MFMA operand reads (16 bytes per lane, consecutive
 // tokens) fall in distinct LDS banks.  Tiles are assigned so that the
 // workgroups of one XCD (blockIdx mod 8) work on a contiguous range of
-// tiles and share activation rows in their L2.
+// tiles and share activation rows in their L2.  The 16-bit output tile is
+// assembled in LDS and leaves in 16-byte rows.
+//
+// Few tokens.  When the tile grid leaves compute units idle, a forward
+// contraction splits its K steps over grid z and a reduction launch adds
+// the fp32 partials in split order (see plan_contraction).
 #include <utility>
 
 #include "af1_device.h"
