@@ -81,7 +81,9 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 //            du; C = bf16(rowscale * du) when C is given; F = per-tile token
 //            sums of du * S, S bf16 in natural order.
 // The backward's A operands also carry a power-of-two scale per 64-token
-// group (see bwd_prep_kernel).
+// group (see bwd_prep_kernel).  With a split K (grid z > 1, forward modes
+// only) a workgroup instead writes the fp32 partial of its K steps to P and
+// splitk_reduce_kernel produces the mode's outputs.
 enum Mode : int { kMid = 0, kMidSave = 1, kOut = 2, kOutSave = 3, kBwdMid = 4, kBwdIn = 5 };
 
 constexpr int BM = 128;          // tokens per tile
