@@ -130,6 +130,23 @@ def test_gemm_token_and_workspace_validation():
     assert gemm(L, T=2048, ws_bytes=need - 1) == af1.AF1_ERR_WORKSPACE
 
 
+def test_gemm_workspace_holds_split_partials_only_for_few_tokens():
+    """The GEMM workspace is fp16(s_in .* x) and Z (both 256-byte aligned),
+    plus fp32 partials when a contraction splits its K steps, which happens
+    only when the tile grid leaves compute units idle (here no GPU is
+    present and the library plans for 256 compute units)."""
+    a = lambda v: (v + 255) // 256 * 256
+    m = n = 4096
+    r = 2016
+    base = lambda T: a(T * n * 2) + a(T * r * 2)
+    assert af1.af1_gemm_workspace_bytes(m, n, r, 2048) == base(2048)
+    few = af1.af1_gemm_workspace_bytes(m, n, r, 64)
+    assert few > base(64)
+    # the partials: some number of splits of the larger of the two outputs
+    extra = few - base(64)
+    assert extra % 256 == 0 and extra <= 64 * (64 * max(r, m) * 4)
+
+
 def test_gemm_rejects_operands_beyond_32bit_offsets():
     """The GEMM kernels address operands with 32-bit byte offsets: T * max(n,
     r) * 2 must stay below 2^31 (a batch error), a sign matrix below 2 GiB (a
