@@ -308,7 +308,8 @@ def bench_gemm(args, torch, stream):
     del L, x, y, ws
     # Context: the prefill regime below 2048 tokens (chunked prefill), where
     # the tile grid alone would leave compute units idle and the
-    # contractions split K; µs per call at 4096^2 and 8192^2.
+    # contractions split K; µs per call at 4096^2 and 8192^2, eager and as a
+    # replayed HIP graph of 10 calls (up to five launches per call).
     sweep = {}
     for name in ("attn4096", "sq8192"):
         m, n, r = shape_of(name)
@@ -322,9 +323,21 @@ def bench_gemm(args, torch, stream):
             fn = lambda i: L.gemm(x, y, ws, stream)
             sustain(fn, stream, min(args.sustain, 0.1))
             ms = time_events(fn, args.gemm_steps, stream) / args.gemm_steps
-            sweep[f"{name}_T{T}"] = dict(us=round(ms * 1e3, 1),
-                                         tflops=round(2.0 * T * r * (m + n) / (ms * 1e-3) / 1e12, 1))
-            del x, y, ws
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                L.gemm(x, y, ws, None)
+            torch.cuda.current_stream().wait_stream(side)
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                for _ in range(10):
+                    L.gemm(x, y, ws, None)
+            time_events(lambda i: graph.replay(), 5, stream)
+            msg = time_events(lambda i: graph.replay(), 20, stream) / 200
+            flops = 2.0 * T * r * (m + n)
+            sweep[f"{name}_T{T}"] = dict(us=round(ms * 1e3, 1), us_graph=round(msg * 1e3, 1),
+                                         tflops_graph=round(flops / (msg * 1e-3) / 1e12, 1))
+            del graph, x, y, ws
         del L
     out["few_tokens"] = sweep
     # MFMA roofline of the prefill leg: algorithmic flops 2*T*r*(m+n) of the
