@@ -782,13 +782,28 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *__restr
     cl = p;
     ch = p + 4;
   }
+  // The loads of up to kReduceBatch splits are issued before any is added
+  // (one memory round trip per batch, not per split); adds stay in split
+  // order.
+  constexpr int kReduceBatch = 8;
   float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
-  for (int sp = 0; sp < S; ++sp) {
-    const float *row = P + ((size_t)sp * T + t) * N;
-    const float4 a = *reinterpret_cast<const float4 *>(row + cl);
-    const float4 b = *reinterpret_cast<const float4 *>(row + ch);
-    lo.x += a.x; lo.y += a.y; lo.z += a.z; lo.w += a.w;
-    hi.x += b.x; hi.y += b.y; hi.z += b.z; hi.w += b.w;
+  const size_t split_stride = (size_t)T * N;
+  const float *base = P + (size_t)t * N;
+  for (int s0 = 0; s0 < S; s0 += kReduceBatch) {
+    float4 a[kReduceBatch], b[kReduceBatch];
+#pragma unroll
+    for (int q = 0; q < kReduceBatch; ++q) {
+      const int sp = s0 + q < S ? s0 + q : S - 1;  // clamped: loaded, not added
+      const float *row = base + (size_t)sp * split_stride;
+      a[q] = *reinterpret_cast<const float4 *>(row + cl);
+      b[q] = *reinterpret_cast<const float4 *>(row + ch);
+    }
+#pragma unroll
+    for (int q = 0; q < kReduceBatch; ++q) {
+      if (s0 + q >= S) break;
+      lo.x += a[q].x; lo.y += a[q].y; lo.z += a[q].z; lo.w += a[q].w;
+      hi.x += b[q].x; hi.y += b[q].y; hi.z += b[q].z; hi.w += b[q].w;
+    }
   }
   // output k of the 8: pair order interleaves the runs, natural order
   // concatenates them
@@ -841,7 +856,9 @@ constexpr int kStages64 = AF1_GEMM_STAGES_64;
 // each compute unit at most one workgroup (one wave per SIMD) uses 64-token
 // tiles instead: twice the workgroups, each expanding its signs for half as
 // many tokens (measured on 8192x8192 G1: +2%; grids between one and two
-// workgroups per unit were slower with it).  A forward grid that still
+// workgroups per unit were slower with it; at 64 tokens or fewer the
+// shorter tile also computes fewer empty rows: 4096^2 G1 at T=32, 12.0 ->
+// 9.2 us).  A forward grid that still
 // leaves compute units idle (few tokens) may split its K steps over grid z
 // (at least kMinSplitSteps steps per split); splitk_reduce_kernel then adds
 // the fp32 partials in split order.  The split count minimises a simple
@@ -862,7 +879,7 @@ ContractionPlan plan_contraction(int64_t T, int64_t K, int64_t N, bool allow_spl
   ContractionPlan p;
   p.gx = (unsigned)((N + BN - 1) / BN);
   const int64_t tiles128 = (int64_t)p.gx * ((T + BM - 1) / BM);
-  p.bm = tiles128 <= (int64_t)cus && T > 64 ? 64 : BM;
+  p.bm = tiles128 <= (int64_t)cus ? 64 : BM;
   p.gy = (unsigned)((T + p.bm - 1) / p.bm);
   const int64_t nk = (K / 32 + kWords - 1) / kWords;
   p.splits = 1;
