@@ -81,9 +81,10 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 //            du; C = bf16(rowscale * du) when C is given; F = per-tile token
 //            sums of du * S, S bf16 in natural order.
 // The backward's A operands also carry a power-of-two scale per 64-token
-// group (see bwd_prep_kernel).  With a split K (grid z > 1, forward modes
-// only) a workgroup instead writes the fp32 partial of its K steps to P and
-// splitk_reduce_kernel produces the mode's outputs.
+// group (see bwd_prep_kernel).  With a split K (grid z > 1) a workgroup
+// instead writes the fp32 partial of its K steps to P and
+// splitk_reduce_kernel (forward modes) or splitk_bwd_reduce_kernel
+// produces the mode's outputs.
 enum Mode : int { kMid = 0, kMidSave = 1, kOut = 2, kOutSave = 3, kBwdMid = 4, kBwdIn = 5 };
 
 constexpr int BM = 128;          // tokens per tile
@@ -94,9 +95,10 @@ constexpr int kThreads = 256;
 constexpr int kARow = BK * 2;                // bytes of one token row of a K step
 constexpr int kATile = BM * kARow;           // 32 KiB
 constexpr int kWTile = BN * kWords * 4;      // 4 KiB
-// LDS map: A0 .. A(S-1) | W0 .. W(S-1) for S pipeline stages (the activation buffers first, so operand reads are immediate
-// offsets from one address), for a token tile of kBM rows (128, or 64 for
-// grids that would give each compute unit at most one workgroup).
+// LDS map: A0 .. A(S-1) | W0 .. W(S-1) for S pipeline stages (the
+// activation buffers first, so operand reads are immediate offsets from one
+// address), for a token tile of kBM rows (128, or 64 for grids that would
+// give each compute unit at most one workgroup).
 template <int kBM, int kStages>
 struct Lds {
   static constexpr int kATileT = kBM * kARow;
@@ -240,9 +242,8 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   const int n0 = (L % nN) * BN;
 
   const int kw = K / 32;                       // sign words per row
-  // K steps of this workgroup: all of them, or with a split K (grid z > 1,
-  // forward modes only) the range of split blockIdx.z; the last step of the
-  // row may be partial.
+  // K steps of this workgroup: all of them, or with a split K (grid z > 1)
+  // the range of split blockIdx.z; the last step of the row may be partial.
   const int nk_row = (kw + kWords - 1) / kWords;
   const int k0 = gridDim.z > 1 ? (int)blockIdx.z * split_steps : 0;
   const int nk = gridDim.z > 1 ? min(nk_row, k0 + split_steps) : nk_row;
@@ -387,10 +388,13 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
 
   // Epilogue.  32x32 accumulator layout: lane l holds column (l mod 32) and
   // rows 8*(e/4) + 4*(l/32) + (e mod 4), e = 0..15.
-  if constexpr (!kBwd) {
+  // (a split K only occurs with 64-token tiles: a grid of 128-token tiles
+  // that leaves compute units idle switches to 64-token tiles first, and
+  // the 128-token kernels carry no second epilogue)
+  if constexpr (kBM == 64) {
     if (gridDim.z > 1) {
       // Split K: the fp32 partial of this tile over the workgroup's K steps,
-      // natural column order; splitk_reduce_kernel adds the partials and
+      // natural column order; the reduction kernel adds the partials and
       // applies the mode's epilogue.
       float *__restrict__ Ps = P + (size_t)blockIdx.z * T * N;
 #pragma unroll
@@ -840,6 +844,107 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *__restr
   }
 }
 
+// The reduction of a split-K backward contraction.  A workgroup takes 64
+// tokens (one 64-token scale group) and 32 output positions: thread (tk, u)
+// adds the S partials of positions 8u .. 8u+7 of token tk in split order,
+// forms the mode's C values (scaled as in bingemm_kernel's epilogue), and
+// the workgroup adds gradient * S over its 64 tokens in token order for the
+// per-tile sums F (one row per 64 tokens).
+constexpr int kBwdReduceCols = 32;
+template <int kMode>
+__global__ __launch_bounds__(256) void splitk_bwd_reduce_kernel(
+    const float *__restrict__ P, int S, int T, int N, const uint16_t *__restrict__ rowscale,
+    const float *__restrict__ gscale, uint16_t *__restrict__ C, const uint16_t *__restrict__ Sv,
+    float *__restrict__ F) {
+  constexpr bool kPairOut = kMode == kBwdMid;
+  constexpr int kReduceBatch = 8;
+  __shared__ float red[64][kBwdReduceCols + 1];
+  const int u = threadIdx.x & 3, tk = threadIdx.x >> 2;
+  const int tile = blockIdx.y;
+  const int t = tile * 64 + tk;
+  const int p = blockIdx.x * kBwdReduceCols + 8 * u;  // first output position
+  int cl, ch;                                         // columns of the two float4 runs
+  if (kPairOut) {
+    cl = (p & ~31) + ((p & 31) >> 1);
+    ch = cl + 16;
+  } else {
+    cl = p;
+    ch = p + 4;
+  }
+  float g[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) g[k] = 0.f;
+  if (t < T && p < N) {
+    float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
+    const size_t split_stride = (size_t)T * N;
+    const float *base = P + (size_t)t * N;
+    for (int s0 = 0; s0 < S; s0 += kReduceBatch) {
+      float4 a[kReduceBatch], b[kReduceBatch];
+#pragma unroll
+      for (int q = 0; q < kReduceBatch; ++q) {
+        const int sp = s0 + q < S ? s0 + q : S - 1;  // clamped: loaded, not added
+        a[q] = *reinterpret_cast<const float4 *>(base + (size_t)sp * split_stride + cl);
+        b[q] = *reinterpret_cast<const float4 *>(base + (size_t)sp * split_stride + ch);
+      }
+#pragma unroll
+      for (int q = 0; q < kReduceBatch; ++q) {
+        if (s0 + q >= S) break;
+        lo.x += a[q].x; lo.y += a[q].y; lo.z += a[q].z; lo.w += a[q].w;
+        hi.x += b[q].x; hi.y += b[q].y; hi.z += b[q].z; hi.w += b[q].w;
+      }
+    }
+    const float2 gs = reinterpret_cast<const float2 *>(gscale)[t >> 6];
+    const float fg = kMode == kBwdMid ? gs.x : gs.x / gs.y;
+    const float l4[4] = {lo.x, lo.y, lo.z, lo.w}, h4[4] = {hi.x, hi.y, hi.z, hi.w};
+    float acc[8];
+    int col[8];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      acc[kPairOut ? 2 * k : k] = l4[k];
+      acc[kPairOut ? 2 * k + 1 : 4 + k] = h4[k];
+      col[kPairOut ? 2 * k : k] = cl + k;
+      col[kPairOut ? 2 * k + 1 : 4 + k] = ch + k;
+    }
+    // S is stored like C: fp16 in pair order (kBwdMid), bf16 natural (kBwdIn)
+    const uint4 sq = *reinterpret_cast<const uint4 *>(Sv + (size_t)t * N + p);
+    const uint32_t sw[4] = {sq.x, sq.y, sq.z, sq.w};
+    uint32_t c[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      float o[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int e = 2 * k + h;
+        const uint32_t sbits = h ? sw[k] >> 16 : sw[k] & 0xffffu;
+        const float sval = kMode == kBwdMid ? f16_to_f32((uint16_t)sbits) : bf16_to_f32(sbits);
+        g[e] = acc[e] * fg * sval;
+        const float rs = f16_to_f32(rowscale[col[e]]);
+        o[h] = kMode == kBwdMid ? acc[e] * rs * gs.y : acc[e] * fg * rs;
+      }
+      c[k] = kMode == kBwdMid
+                 ? (uint32_t)f32_to_f16(o[0]) | ((uint32_t)f32_to_f16(o[1]) << 16)
+                 : (uint32_t)f32_to_bf16(o[0]) | ((uint32_t)f32_to_bf16(o[1]) << 16);
+    }
+    if (C) *reinterpret_cast<uint4 *>(C + (size_t)t * N + p) = make_uint4(c[0], c[1], c[2], c[3]);
+  }
+  // token sums: red[token][position in block], then one thread per position
+  // adds the 64 tokens in order and writes the column's sum
+#pragma unroll
+  for (int k = 0; k < 8; ++k) red[tk][8 * u + k] = g[k];
+  __syncthreads();
+  if (threadIdx.x < kBwdReduceCols) {
+    const int pos = threadIdx.x;
+    const int pp = blockIdx.x * kBwdReduceCols + pos;
+    float sum = 0.f;
+    for (int k = 0; k < 64; ++k) sum += red[k][pos];
+    if (pp < N) {
+      // column of output position pp
+      const int n = kPairOut ? (pp & ~31) + ((pp & 31) >> 1) + 16 * (pp & 1) : pp;
+      F[(size_t)tile * N + n] = sum;
+    }
+  }
+}
+
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
 // Copy pipeline depth per token-tile height.
@@ -909,14 +1014,15 @@ size_t split_bytes(const ContractionPlan &p, int64_t T, int64_t N) {
 }
 
 // One contraction C[T, N] over K on the stream.  P: fp32 workspace for a
-// split K (forward modes; nullptr never splits).  *tile_tokens receives the
-// token-tile height used (the row count of F's per-tile sums).
+// split K (nullptr never splits).  *tile_tokens receives the token count
+// per row of F's per-tile sums (the token-tile height, or 64 when split).
 template <int kMode>
 hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *W, int64_t N,
                        const uint16_t *rs, uint16_t *C, uint16_t *V, const uint16_t *S,
                        float *F, hipStream_t s, int *tile_tokens = nullptr,
                        const float *gscale = nullptr, float *P = nullptr) {
   const ContractionPlan p = plan_contraction(T, K, N, P != nullptr, device_cus());
+  if (p.splits > 1 && p.bm != 64) return hipErrorInvalidValue;  // see bingemm_kernel
   const dim3 g(p.gx, p.gy, (unsigned)p.splits);
   if (p.bm == 64)
     bingemm_kernel<kMode, 64, kStages64><<<g, kThreads, Lds<64, kStages64>::kBytes, s>>>(
@@ -924,14 +1030,17 @@ hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *
   else
     bingemm_kernel<kMode, BM, kStages128><<<g, kThreads, Lds<BM, kStages128>::kBytes, s>>>(
         A, (int)T, (int)K, W, (int)N, rs, C, V, S, F, gscale, p.split_steps, P);
-  if (tile_tokens) *tile_tokens = p.bm;
+  if (tile_tokens) *tile_tokens = p.splits > 1 ? 64 : p.bm;
   if (p.splits > 1) {
-    if constexpr (kMode == kMid || kMode == kMidSave || kMode == kOut || kMode == kOutSave) {
+    if constexpr (kMode == kBwdMid || kMode == kBwdIn) {
+      const dim3 gr((unsigned)((N + kBwdReduceCols - 1) / kBwdReduceCols),
+                    (unsigned)((T + 63) / 64));
+      splitk_bwd_reduce_kernel<kMode><<<gr, 256, 0, s>>>(P, p.splits, (int)T, (int)N, rs,
+                                                          gscale, C, S, F);
+    } else {
       const int64_t units = T * (N / 8);
       splitk_reduce_kernel<kMode><<<(unsigned)((units + 255) / 256), 256, 0, s>>>(
           P, p.splits, (int)T, (int)N, rs, C, V, F);
-    } else {
-      return hipErrorInvalidValue;  // the backward modes never split
     }
   }
   return hipGetLastError();
@@ -965,7 +1074,7 @@ int64_t tiles64(int64_t T) { return (T + 63) / 64; }
 
 struct BwdWs {
   uint16_t *A1, *Zb;
-  float *p_out, *p_mid, *p_in, *tstat, *gscale;
+  float *p_out, *p_mid, *p_in, *tstat, *gscale, *P;
 };
 
 BwdWs backward_ws(void *ws, int64_t m, int64_t n, int64_t r, int64_t T) {
@@ -984,14 +1093,20 @@ BwdWs backward_ws(void *ws, int64_t m, int64_t n, int64_t r, int64_t T) {
   w.tstat = reinterpret_cast<float *>(base);
   base += align256((size_t)T * 8 + 4);
   w.gscale = reinterpret_cast<float *>(base);
+  base += align256((size_t)tiles64(T) * 8);
+  w.P = reinterpret_cast<float *>(base);
   return w;
 }
 
 size_t backward_ws_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
+  // ... and the fp32 partials of whichever backward contraction splits K
+  const int cus = device_cus();
+  const size_t p1 = split_bytes(plan_contraction(T, m, r, true, cus), T, r);
+  const size_t p2 = split_bytes(plan_contraction(T, r, n, true, cus), T, n);
   return align256((size_t)T * m * 2) + align256((size_t)T * r * 2) +
          align256((size_t)tiles64(T) * m * 4) + align256((size_t)tiles64(T) * r * 4) +
          align256((size_t)tiles64(T) * n * 4) + align256((size_t)T * 8 + 4) +
-         align256((size_t)tiles64(T) * 8);
+         align256((size_t)tiles64(T) * 8) + (p1 > p2 ? p1 : p2);
 }
 
 }  // namespace
@@ -1086,10 +1201,11 @@ hipError_t launch_backward(int64_t m, int64_t n, int64_t r, const uint32_t *BuT,
   // operand; sums dt .* v.
   int tm = 0, ti = 0;
   e = contraction<kBwdMid>(w.A1, T, m, BuT, r, s_mid, w.Zb, nullptr, v, w.p_mid, s, &tm,
-                           w.gscale);
+                           w.gscale, w.P);
   if (e != hipSuccess) return e;
   // du 2^(e - c) = Bv^T (s_mid .* dt 2^(e - c)): dx = s_in .* du; sums du .* x.
-  e = contraction<kBwdIn>(w.Zb, T, r, BvT, n, s_in, dx, nullptr, x, w.p_in, s, &ti, w.gscale);
+  e = contraction<kBwdIn>(w.Zb, T, r, BvT, n, s_in, dx, nullptr, x, w.p_in, s, &ti, w.gscale,
+                          w.P);
   if (e != hipSuccess) return e;
   const int total = (int)(m + r + n);
   bwd_finish_kernel<<<(unsigned)((total + kFinishCols - 1) / kFinishCols), 256, 0, s>>>(
