@@ -216,7 +216,7 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     const uint16_t *__restrict__ A, int T, int K, const uint32_t *__restrict__ W, int N,
     const uint16_t *__restrict__ rowscale, uint16_t *__restrict__ C, uint16_t *__restrict__ V,
     const uint16_t *__restrict__ S, float *__restrict__ F, const float *__restrict__ gscale,
-    int split_steps, float *__restrict__ P) {
+    int split_steps, float *__restrict__ P, int mix_full, int mix_splits, int mix_nN) {
   constexpr bool kPairOut = kMode == kMid || kMode == kMidSave || kMode == kBwdMid;
   constexpr bool kBwd = kMode == kBwdMid || kMode == kBwdIn;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
@@ -233,20 +233,44 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   // s_waitcnt leaves exactly the newest step's copies in flight).
   constexpr int kCopiesPerStep = kACopies + 4;
 
-  // Tile assignment: consecutive workgroups land on consecutive XCDs; give
-  // each XCD a contiguous range of tiles (weight-row tiles fastest).
-  const int nN = gridDim.x, nT = gridDim.y, total = nN * nT;
-  int L = blockIdx.y * nN + blockIdx.x;
-  if ((total & 7) == 0) L = (L & 7) * (total >> 3) + (L >> 3);
+  const int kw = K / 32;                       // sign words per row
+  const int nk_row = (kw + kWords - 1) / kWords;  // the last step may be partial
+  // Tile and K steps of this workgroup.
+  //  Plain grid: consecutive workgroups land on consecutive XCDs; each XCD
+  //  takes a contiguous range of tiles (weight-row tiles fastest); all K
+  //  steps, or with a split K (grid z > 1) the range of split blockIdx.z.
+  //  Mixed grid (mix_full > 0, forward modes, 1-D): workgroups below
+  //  mix_full take whole tiles (one per compute unit: workgroups are placed
+  //  one per unit before any unit gets a second), each remaining tile is cut
+  //  into mix_splits K ranges written as partials (pslot).
+  int nN, L, k0, nk, pslot = -1;
+  if (mix_full > 0) {
+    nN = mix_nN;
+    const int bid = (int)blockIdx.x;
+    if (bid < mix_full) {
+      L = bid;
+      if ((mix_full & 7) == 0) L = (L & 7) * (mix_full >> 3) + (L >> 3);
+      k0 = 0;
+      nk = nk_row;
+    } else {
+      pslot = bid - mix_full;
+      const int cut = (int)gridDim.x - mix_full;
+      if ((cut & 7) == 0) pslot = (pslot & 7) * (cut >> 3) + (pslot >> 3);
+      const int h = pslot / mix_splits;
+      L = mix_full + h;
+      k0 = (pslot - h * mix_splits) * split_steps;
+      nk = min(nk_row, k0 + split_steps);
+    }
+  } else {
+    nN = gridDim.x;
+    const int total = nN * gridDim.y;
+    L = blockIdx.y * nN + blockIdx.x;
+    if ((total & 7) == 0) L = (L & 7) * (total >> 3) + (L >> 3);
+    k0 = gridDim.z > 1 ? (int)blockIdx.z * split_steps : 0;
+    nk = gridDim.z > 1 ? min(nk_row, k0 + split_steps) : nk_row;
+  }
   const int t0 = (L / nN) * kBM;
   const int n0 = (L % nN) * BN;
-
-  const int kw = K / 32;                       // sign words per row
-  // K steps of this workgroup: all of them, or with a split K (grid z > 1)
-  // the range of split blockIdx.z; the last step of the row may be partial.
-  const int nk_row = (kw + kWords - 1) / kWords;
-  const int k0 = gridDim.z > 1 ? (int)blockIdx.z * split_steps : 0;
-  const int nk = gridDim.z > 1 ? min(nk_row, k0 + split_steps) : nk_row;
 
   // Copy roles, fixed per lane (a step only moves the resources' bases).
   //  Activations: wave w issues copies j = kACopies*w + jj, each covering
@@ -388,6 +412,23 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
 
   // Epilogue.  32x32 accumulator layout: lane l holds column (l mod 32) and
   // rows 8*(e/4) + 4*(l/32) + (e mod 4), e = 0..15.
+  if constexpr (!kBwd) {
+    if (pslot >= 0) {
+      // Mixed grid: the fp32 partial of this tile over the workgroup's K
+      // range, tile-local [token][column], for mixed_reduce_kernel.
+      float *__restrict__ Pt = P + (size_t)pslot * (kBM * BN);
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int nl = wrow_l + 32 * j;
+#pragma unroll
+        for (int i = 0; i < kTokBlocks; ++i)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            Pt[(32 * i + 8 * (e >> 2) + 4 * g + (e & 3)) * BN + nl] = acc[i][j][e];
+      }
+      return;
+    }
+  }
   // (a split K only occurs with 64-token tiles: a grid of 128-token tiles
   // that leaves compute units idle switches to 64-token tiles first, and
   // the 128-token kernels carry no second epilogue)
@@ -760,6 +801,50 @@ __global__ __launch_bounds__(256) void bwd_finish_kernel(
   }
 }
 
+// The forward modes' outputs for 8 consecutive output positions p .. p+7 of
+// token t from their fp32 sums: lo holds columns cl .. cl+3, hi columns
+// ch .. ch+3 (pair order interleaves the two runs, natural order
+// concatenates them).
+template <int kMode>
+__device__ __forceinline__ void finish8(const float4 &lo, const float4 &hi, int cl, int ch, int p,
+                                        int t, int N, const uint16_t *__restrict__ rowscale,
+                                        uint16_t *__restrict__ C, uint16_t *__restrict__ V,
+                                        float *__restrict__ F) {
+  constexpr bool kPairOut = kMode == kMid || kMode == kMidSave;
+  const float l4[4] = {lo.x, lo.y, lo.z, lo.w}, h4[4] = {hi.x, hi.y, hi.z, hi.w};
+  float acc[8];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    acc[kPairOut ? 2 * k : k] = l4[k];
+    acc[kPairOut ? 2 * k + 1 : 4 + k] = h4[k];
+  }
+  uint32_t c[4], v[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    int col0, col1;
+    if (kPairOut) {
+      col0 = cl + k;
+      col1 = ch + k;
+    } else {
+      col0 = p + 2 * k;
+      col1 = p + 2 * k + 1;
+    }
+    const float r0 = f16_to_f32(rowscale[col0]), r1 = f16_to_f32(rowscale[col1]);
+    const float a0 = acc[2 * k] * r0, a1 = acc[2 * k + 1] * r1;
+    c[k] = kPairOut ? (uint32_t)f32_to_f16(a0) | ((uint32_t)f32_to_f16(a1) << 16)
+                    : (uint32_t)f32_to_bf16(a0) | ((uint32_t)f32_to_bf16(a1) << 16);
+    v[k] = (uint32_t)f32_to_f16(acc[2 * k]) | ((uint32_t)f32_to_f16(acc[2 * k + 1]) << 16);
+  }
+  const size_t o = (size_t)t * N + p;
+  *reinterpret_cast<uint4 *>(C + o) = make_uint4(c[0], c[1], c[2], c[3]);
+  if constexpr (kMode == kMidSave)
+    *reinterpret_cast<uint4 *>(V + o) = make_uint4(v[0], v[1], v[2], v[3]);
+  if constexpr (kMode == kOutSave) {
+    *reinterpret_cast<float4 *>(F + o) = lo;
+    *reinterpret_cast<float4 *>(F + o + 4) = hi;
+  }
+}
+
 // The reduction of a split-K contraction (forward modes): C and its
 // companions from the S fp32 partials of the workgroups along K, added in
 // split order.  A thread takes 8 consecutive output positions of one token:
@@ -809,39 +894,53 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *__restr
       hi.x += b[q].x; hi.y += b[q].y; hi.z += b[q].z; hi.w += b[q].w;
     }
   }
-  // output k of the 8: pair order interleaves the runs, natural order
-  // concatenates them
-  const float l4[4] = {lo.x, lo.y, lo.z, lo.w}, h4[4] = {hi.x, hi.y, hi.z, hi.w};
-  float acc[8];
+  finish8<kMode>(lo, hi, cl, ch, p, t, N, rowscale, C, V, F);
+}
+
+// The reduction of a mixed grid (forward modes): for each tile cut into
+// S K ranges (tiles full .. full + H - 1), the partials of slots h S ..
+// h S + S - 1 (tile-local [token][column], fp32) added in range order, then
+// the mode's outputs.  16 workgroups per tile; a thread takes 8 consecutive
+// output positions of one token row of the tile.
+template <int kMode>
+__global__ __launch_bounds__(256) void mixed_reduce_kernel(const float *__restrict__ P, int S,
+                                                           int full, int nN, int T, int N,
+                                                           const uint16_t *__restrict__ rowscale,
+                                                           uint16_t *__restrict__ C,
+                                                           uint16_t *__restrict__ V,
+                                                           float *__restrict__ F) {
+  constexpr bool kPairOut = kMode == kMid || kMode == kMidSave;
+  const int h = blockIdx.x >> 4;
+  const int unit = ((blockIdx.x & 15) << 8) + threadIdx.x;  // 0 .. 4095
+  const int row = unit >> 5, pl = (unit & 31) * 8;          // token row, first position
+  const int L = full + h;
+  const int t = (L / nN) * BM + row;
+  const int n0 = (L % nN) * BN;
+  if (t >= T || n0 + pl >= N) return;
+  int cl, ch;  // tile-local columns of the two float4 runs
+  if (kPairOut) {
+    cl = (pl & ~31) + ((pl & 31) >> 1);
+    ch = cl + 16;
+  } else {
+    cl = pl;
+    ch = pl + 4;
+  }
+  float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
+  float4 a[4], b[4];
+  const float *base = P + (size_t)h * S * (BM * BN) + row * BN;
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    acc[kPairOut ? 2 * k : k] = l4[k];
-    acc[kPairOut ? 2 * k + 1 : 4 + k] = h4[k];
+  for (int q = 0; q < 4; ++q) {  // S <= 4
+    const int sp = q < S ? q : S - 1;
+    a[q] = *reinterpret_cast<const float4 *>(base + (size_t)sp * (BM * BN) + cl);
+    b[q] = *reinterpret_cast<const float4 *>(base + (size_t)sp * (BM * BN) + ch);
   }
-  uint32_t c[4], v[4];
 #pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    int col0, col1;
-    if (kPairOut) {
-      col0 = cl + k;
-      col1 = ch + k;
-    } else {
-      col0 = p + 2 * k;
-      col1 = p + 2 * k + 1;
-    }
-    const float r0 = f16_to_f32(rowscale[col0]), r1 = f16_to_f32(rowscale[col1]);
-    const float a0 = acc[2 * k] * r0, a1 = acc[2 * k + 1] * r1;
-    c[k] = kPairOut ? (uint32_t)f32_to_f16(a0) | ((uint32_t)f32_to_f16(a1) << 16)
-                    : (uint32_t)f32_to_bf16(a0) | ((uint32_t)f32_to_bf16(a1) << 16);
-    v[k] = (uint32_t)f32_to_f16(acc[2 * k]) | ((uint32_t)f32_to_f16(acc[2 * k + 1]) << 16);
+  for (int q = 0; q < 4; ++q) {
+    if (q >= S) break;
+    lo.x += a[q].x; lo.y += a[q].y; lo.z += a[q].z; lo.w += a[q].w;
+    hi.x += b[q].x; hi.y += b[q].y; hi.z += b[q].z; hi.w += b[q].w;
   }
-  const size_t o = (size_t)t * N + p;
-  *reinterpret_cast<uint4 *>(C + o) = make_uint4(c[0], c[1], c[2], c[3]);
-  if constexpr (kMode == kMidSave) *reinterpret_cast<uint4 *>(V + o) = make_uint4(v[0], v[1], v[2], v[3]);
-  if constexpr (kMode == kOutSave) {
-    *reinterpret_cast<float4 *>(F + o) = lo;
-    *reinterpret_cast<float4 *>(F + o + 4) = hi;
-  }
+  finish8<kMode>(lo, hi, n0 + cl, n0 + ch, n0 + pl, t, N, rowscale, C, V, F);
 }
 
 // The reduction of a split-K backward contraction.  A workgroup takes 64
@@ -978,10 +1077,24 @@ struct ContractionPlan {
   int bm;                // token-tile height
   unsigned gx, gy;       // weight-row tiles, token tiles
   int splits, split_steps;
+  int mix_full, mix_splits;  // mixed grid (mix_full > 0): whole tiles, K ranges per other tile
 };
 
-ContractionPlan plan_contraction(int64_t T, int64_t K, int64_t N, bool allow_split, int cus) {
+// A forward grid of 128-token tiles with between one and 1.75 tiles per
+// compute unit (28672x8192 and 8192x28672 G1 at T=2048: 400 tiles) leaves
+// the units that got one tile idle for the last part of the launch.  Mixed
+// grid: one whole tile per unit (the first workgroups, placed one per unit),
+// and the remaining tiles each cut into kMixSplits K ranges that run beside
+// them as partials; mixed_reduce_kernel adds them.  The busiest unit then
+// carries 1 + 2/3 tile instead of 2.  Only for K of at least kMixMinSteps
+// steps, where the partials' traffic is small against the kernel.
+constexpr int kMixSplits = 3;
+constexpr int kMixMinSteps = 24;
+
+ContractionPlan plan_contraction(int64_t T, int64_t K, int64_t N, bool allow_split, int cus,
+                                 bool allow_mixed = false) {
   ContractionPlan p;
+  p.mix_full = p.mix_splits = 0;
   p.gx = (unsigned)((N + BN - 1) / BN);
   const int64_t tiles128 = (int64_t)p.gx * ((T + BM - 1) / BM);
   p.bm = tiles128 <= (int64_t)cus ? 64 : BM;
@@ -1006,7 +1119,19 @@ ContractionPlan plan_contraction(int64_t T, int64_t K, int64_t N, bool allow_spl
       p.splits = (int)((nk + p.split_steps - 1) / p.split_steps);
     }
   }
+  if (allow_mixed && p.bm == BM && tiles > cus && tiles * 4 < (int64_t)cus * 7 &&
+      nk >= kMixMinSteps) {
+    p.mix_full = cus;
+    p.split_steps = (int)((nk + kMixSplits - 1) / kMixSplits);
+    p.mix_splits = (int)((nk + p.split_steps - 1) / p.split_steps);
+  }
   return p;
+}
+
+size_t mixed_bytes(const ContractionPlan &p, int64_t T, int64_t N) {
+  if (p.mix_full == 0) return 0;
+  const int64_t cut = (int64_t)p.gx * p.gy - p.mix_full;
+  return align256((size_t)cut * p.mix_splits * BM * BN * 4);
 }
 
 size_t split_bytes(const ContractionPlan &p, int64_t T, int64_t N) {
@@ -1021,16 +1146,31 @@ hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *
                        const uint16_t *rs, uint16_t *C, uint16_t *V, const uint16_t *S,
                        float *F, hipStream_t s, int *tile_tokens = nullptr,
                        const float *gscale = nullptr, float *P = nullptr) {
-  const ContractionPlan p = plan_contraction(T, K, N, P != nullptr, device_cus());
+  constexpr bool kFwd = kMode == kMid || kMode == kMidSave || kMode == kOut || kMode == kOutSave;
+  const ContractionPlan p = plan_contraction(T, K, N, P != nullptr, device_cus(), kFwd && P);
   if (p.splits > 1 && p.bm != 64) return hipErrorInvalidValue;  // see bingemm_kernel
-  const dim3 g(p.gx, p.gy, (unsigned)p.splits);
+  const int64_t tiles = (int64_t)p.gx * p.gy;
+  const dim3 g = p.mix_full > 0
+                     ? dim3((unsigned)(p.mix_full + (tiles - p.mix_full) * p.mix_splits))
+                     : dim3(p.gx, p.gy, (unsigned)p.splits);
   if (p.bm == 64)
     bingemm_kernel<kMode, 64, kStages64><<<g, kThreads, Lds<64, kStages64>::kBytes, s>>>(
-        A, (int)T, (int)K, W, (int)N, rs, C, V, S, F, gscale, p.split_steps, P);
+        A, (int)T, (int)K, W, (int)N, rs, C, V, S, F, gscale, p.split_steps, P, p.mix_full,
+        p.mix_splits, (int)p.gx);
   else
     bingemm_kernel<kMode, BM, kStages128><<<g, kThreads, Lds<BM, kStages128>::kBytes, s>>>(
-        A, (int)T, (int)K, W, (int)N, rs, C, V, S, F, gscale, p.split_steps, P);
+        A, (int)T, (int)K, W, (int)N, rs, C, V, S, F, gscale, p.split_steps, P, p.mix_full,
+        p.mix_splits, (int)p.gx);
   if (tile_tokens) *tile_tokens = p.splits > 1 ? 64 : p.bm;
+  if (p.mix_full > 0) {
+    if constexpr (kFwd) {
+      const unsigned blocks = (unsigned)((tiles - p.mix_full) * 16);
+      mixed_reduce_kernel<kMode><<<blocks, 256, 0, s>>>(P, p.mix_splits, p.mix_full, (int)p.gx,
+                                                         (int)T, (int)N, rs, C, V, F);
+    } else {
+      return hipErrorInvalidValue;  // planned for the forward modes only
+    }
+  }
   if (p.splits > 1) {
     if constexpr (kMode == kBwdMid || kMode == kBwdIn) {
       const dim3 gr((unsigned)((N + kBwdReduceCols - 1) / kBwdReduceCols),
@@ -1115,8 +1255,12 @@ size_t gemm_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
   // fp16(s_in .* x) and the fp16 intermediate Z, both in pair order, and the
   // fp32 partials of whichever contraction splits its K steps
   const int cus = device_cus();
-  const size_t p1 = split_bytes(plan_contraction(T, n, r, true, cus), T, r);
-  const size_t p2 = split_bytes(plan_contraction(T, r, m, true, cus), T, m);
+  const ContractionPlan g1 = plan_contraction(T, n, r, true, cus, true);
+  const ContractionPlan g2 = plan_contraction(T, r, m, true, cus, true);
+  const size_t p1 = split_bytes(g1, T, r) > mixed_bytes(g1, T, r) ? split_bytes(g1, T, r)
+                                                                   : mixed_bytes(g1, T, r);
+  const size_t p2 = split_bytes(g2, T, m) > mixed_bytes(g2, T, m) ? split_bytes(g2, T, m)
+                                                                   : mixed_bytes(g2, T, m);
   return align256((size_t)T * (size_t)n * 2) + align256((size_t)T * (size_t)r * 2) +
          (p1 > p2 ? p1 : p2);
 }

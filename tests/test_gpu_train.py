@@ -131,6 +131,25 @@ def test_forward_train_output_is_the_inference_output():
     assert torch.equal(y_inf, y_tr)
 
 
+def test_forward_train_output_is_the_inference_output_mixed_grid(oracle):
+    """28672x8192 at T = 2048: the first contraction's 400 tiles run as a
+    mixed grid (whole tiles beside K-range partials); the training forward's
+    y still equals the inference forward's, and sampled tokens match the
+    oracle."""
+    m, n, r = synth.SHAPES["mlp_up28672x8192"]
+    T = 2048
+    lin = synth.make_linear(43, m, n, r, T)
+    L = DeviceLayer.from_host(lin)
+    x = to_device(lin.x)
+    y_inf = L.gemm(x)
+    y_tr, _ = L.forward_train(x)
+    torch.cuda.synchronize()
+    assert torch.equal(y_inf, y_tr)
+    rows = [0, 511, 1024, 2047]
+    ref = oracle.forward(m, n, r, lin.Bu, lin.Bv, lin.s_out, lin.s_mid, lin.s_in, lin.x[rows])
+    assert max_row_rel_l2(bf16_bits_to_f64(y_tr)[rows], ref) <= TOL
+
+
 @pytest.mark.parametrize("name,T", [("attn4096", 64), ("sq8192", 64), ("mlp_up28672x8192", 32),
                                     ("mlp_down8192x28672", 32)])
 def test_backward_full_size_dims(oracle, name, T):
