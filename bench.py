@@ -155,10 +155,35 @@ def decode_time(args, torch, stream, m, n, r, b, seed, steps):
     replays = max(1, -(-steps // pool))
     time_events(lambda i: graph.replay(), max(1, args.warmup // pool), stream)
     ms_graph = time_events(lambda i: graph.replay(), replays, stream) / (replays * pool)
+    # spread: µs per layer of each replay (one pass over the pool), timed alone
+    per = sorted(time_events(lambda i: graph.replay(), 1, stream) * 1e3 / pool
+                 for _ in range(max(5, min(replays, 50))))
+    pct = lambda q: per[min(len(per) - 1, int(q * (len(per) - 1) + 0.5))]
     del graph, P
     return dict(m=m, n=n, r=r, b=b, pool=pool, pool_mb=pool * layer_bytes / 2 ** 20,
                 steps_timed=replays * pool, us_graph=ms_graph * 1e3, us_eager=ms_eager * 1e3,
+                us_graph_p10=pct(0.1), us_graph_p50=pct(0.5), us_graph_p90=pct(0.9),
                 alg_bytes=gemv_algorithmic_bytes(m, n, r, b))
+
+
+def launch_floor(torch, stream, count=256, replays=20):
+    """µs per launch of a one-workgroup kernel (torch's in-place add on one
+    element), `count` dependent launches in a replayed HIP graph: the floor
+    under any per-call time that takes one launch per stage."""
+    t = torch.zeros(1, device="cuda")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        t.add_(1.0)
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for _ in range(count):
+            t.add_(1.0)
+    time_events(lambda i: graph.replay(), 3, stream)
+    us = time_events(lambda i: graph.replay(), replays, stream) * 1e3 / (replays * count)
+    del graph
+    return round(us, 3)
 
 
 DECODE_TABLE = [("sq1024", 1), ("attn4096", 8), ("kv1024x4096", 1), ("mlp_up14336x4096", 1),
@@ -619,7 +644,11 @@ def main():
                                f"{g['pool']} distinct layers ({g['pool_mb']:.0f} MB)",
                    "m": g["m"], "n": g["n"], "r": g["r"], "batch": g["b"],
                    "timing": "hip graph of one pass over the weight pool, replayed",
-                   "us_per_layer_eager_launch": round(g["us_eager"], 3)},
+                   "us_per_layer_p10_p50_p90": [round(g["us_graph_p10"], 3),
+                                                round(g["us_graph_p50"], 3),
+                                                round(g["us_graph_p90"], 3)],
+                   "us_per_layer_eager_launch": round(g["us_eager"], 3),
+                   "us_per_launch_floor": launch_floor(torch, stream)},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 5),
                      "traffic": measured_gemv_traffic(),
