@@ -436,19 +436,33 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     if (gridDim.z > 1) {
       // Split K: the fp32 partial of this tile over the workgroup's K steps,
       // natural column order; the reduction kernel adds the partials and
-      // applies the mode's epilogue.
+      // applies the mode's epilogue.  Each half of the tile's columns (the
+      // j-th 32 of every wave's 64) is transposed through the idle LDS
+      // buffers and leaves in 16-byte stores along the columns: 16 stores
+      // a lane instead of 64 single floats, whose issue alone took ~2 us.
       float *__restrict__ Ps = P + (size_t)blockIdx.z * T * N;
+      constexpr int kRowF = 128 + 4;  // floats per staged token row
+      static_assert(kBM * kRowF * 4 <= kLdsBytes, "split partial staging fits the LDS");
+      float *stg = reinterpret_cast<float *>(lds);
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        const int n = wrow0 + 32 * j;
-        if (n >= N) continue;
+        if (j > 0) __syncthreads();  // the previous half has been read
 #pragma unroll
         for (int i = 0; i < kTokBlocks; ++i)
 #pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int t = t0 + 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
-            if (t < T) Ps[(size_t)t * N + n] = acc[i][j][e];
-          }
+          for (int e = 0; e < 16; ++e)
+            stg[(32 * i + 8 * (e >> 2) + 4 * g + (e & 3)) * kRowF + 32 * wave + (lane & 31)] =
+                acc[i][j][e];
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < kBM * 32 / kThreads; ++q) {
+          const int idx = q * kThreads + tid;
+          const int row = idx >> 5, c4 = idx & 31;  // token row, float4 of the half
+          const int n = n0 + 64 * (c4 >> 3) + 32 * j + 4 * (c4 & 7);
+          if (t0 + row < T && n < N)
+            *reinterpret_cast<float4 *>(Ps + (size_t)(t0 + row) * N + n) =
+                *reinterpret_cast<const float4 *>(stg + row * kRowF + 4 * c4);
+        }
       }
       return;
     }
