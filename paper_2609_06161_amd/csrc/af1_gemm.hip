@@ -429,6 +429,38 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       return;
     }
   }
+  // A fp32 [T][N] output of the whole tile (a split partial, or the saved
+  // pre-scale output z): each half of the tile's columns (the j-th 32 of
+  // every wave's 64) is transposed through the idle LDS buffers and leaves
+  // in 16-byte stores along the columns.  Stored from the accumulator
+  // layout (one column per lane) it took 64-128 single-float stores a lane,
+  // whose issue alone cost about 2 us per workgroup.  The LDS buffers must
+  // be idle on entry.
+  auto store_f32_tile = [&](float *__restrict__ dst) {
+    constexpr int kRowF = 128 + 4;  // floats per staged token row
+    static_assert(kBM * kRowF * 4 <= kLdsBytes, "fp32 staging fits the LDS");
+    float *stg = reinterpret_cast<float *>(lds);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      if (j > 0) __syncthreads();  // the previous half has been read
+#pragma unroll
+      for (int i = 0; i < kTokBlocks; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          stg[(32 * i + 8 * (e >> 2) + 4 * g + (e & 3)) * kRowF + 32 * wave + (lane & 31)] =
+              acc[i][j][e];
+      __syncthreads();
+#pragma unroll
+      for (int q = 0; q < kBM * 32 / kThreads; ++q) {
+        const int idx = q * kThreads + tid;
+        const int row = idx >> 5, c4 = idx & 31;  // token row, float4 of the half
+        const int n = n0 + 64 * (c4 >> 3) + 32 * j + 4 * (c4 & 7);
+        if (t0 + row < T && n < N)
+          *reinterpret_cast<float4 *>(dst + (size_t)(t0 + row) * N + n) =
+              *reinterpret_cast<const float4 *>(stg + row * kRowF + 4 * c4);
+      }
+    }
+  };
   // (a split K only occurs with 64-token tiles: a grid of 128-token tiles
   // that leaves compute units idle switches to 64-token tiles first, and
   // the 128-token kernels carry no second epilogue)
@@ -436,34 +468,8 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     if (gridDim.z > 1) {
       // Split K: the fp32 partial of this tile over the workgroup's K steps,
       // natural column order; the reduction kernel adds the partials and
-      // applies the mode's epilogue.  Each half of the tile's columns (the
-      // j-th 32 of every wave's 64) is transposed through the idle LDS
-      // buffers and leaves in 16-byte stores along the columns: 16 stores
-      // a lane instead of 64 single floats, whose issue alone took ~2 us.
-      float *__restrict__ Ps = P + (size_t)blockIdx.z * T * N;
-      constexpr int kRowF = 128 + 4;  // floats per staged token row
-      static_assert(kBM * kRowF * 4 <= kLdsBytes, "split partial staging fits the LDS");
-      float *stg = reinterpret_cast<float *>(lds);
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        if (j > 0) __syncthreads();  // the previous half has been read
-#pragma unroll
-        for (int i = 0; i < kTokBlocks; ++i)
-#pragma unroll
-          for (int e = 0; e < 16; ++e)
-            stg[(32 * i + 8 * (e >> 2) + 4 * g + (e & 3)) * kRowF + 32 * wave + (lane & 31)] =
-                acc[i][j][e];
-        __syncthreads();
-#pragma unroll
-        for (int q = 0; q < kBM * 32 / kThreads; ++q) {
-          const int idx = q * kThreads + tid;
-          const int row = idx >> 5, c4 = idx & 31;  // token row, float4 of the half
-          const int n = n0 + 64 * (c4 >> 3) + 32 * j + 4 * (c4 & 7);
-          if (t0 + row < T && n < N)
-            *reinterpret_cast<float4 *>(Ps + (size_t)(t0 + row) * N + n) =
-                *reinterpret_cast<const float4 *>(stg + row * kRowF + 4 * c4);
-        }
-      }
+      // applies the mode's epilogue.
+      store_f32_tile(P + (size_t)blockIdx.z * T * N);
       return;
     }
   }
@@ -576,18 +582,8 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     store_tile(V);
   }
   if constexpr (kMode == kOutSave) {
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int n = wrow0 + 32 * j;
-      if (n >= N) continue;
-#pragma unroll
-      for (int i = 0; i < kTokBlocks; ++i)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int t = t0 + 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
-          if (t < T) F[(size_t)t * N + n] = acc[i][j][e];
-        }
-    }
+    __syncthreads();  // every wave is done reading the staged C tile
+    store_f32_tile(F);
   }
 }
 
