@@ -313,57 +313,121 @@ __device__ __forceinline__ void stage_body(
     const bool two_parts = !kInX && in_parts > 1;
     const int bstride = row_stride(w_count);
     uint8_t *junk = xs + (size_t)b * bstride + (tid & 15) * kSlot;
-    // pass stride and this thread's first unit
-    const int stride = shared ? 2 * kThreads : 128;
-    const int first = shared ? tid : lane;
-    const int wave_first = shared ? 64 * wave : 0;
+    if (kHiLoCols && !shared && b == 1) {
+      // One batch row: the 64 lanes share a group's 16 units, a quarter
+      // unit each (columns c, c+1 and their partners c+16, c+17), so the
+      // conversion costs a quarter of the per-lane instructions of whole
+      // units.  Same values and layout as load_unit / store_unit.
+      const int rem = lane >> 2, qq = lane & 3;
+      u32x2 ra[kMaxGroups], rb[kMaxGroups], rc[kMaxGroups], rd[kMaxGroups];
+      int dst_off[kMaxGroups];
 #pragma unroll
-    for (int it = 0; it < kStageIters; ++it) {
-      const int base = it * stride;
-      if (base >= nunits) break;  // uniform
-      int slot_off[2], half[2], off[2], col[2];
-      bool has[2];
-#pragma unroll
-      for (int k = 0; k < 2; ++k) {
-        const int u = base + (stride >> 1) * k + first;
-        has[k] = base + (stride >> 1) * k + wave_first < nunits;  // wave-uniform
-        const bool ok = u < nunits;
-        // u / span for u < 2^12: a float estimate, corrected by one step
-        int q0 = (int)((float)u * inv_span);
-        q0 -= q0 * span > u;
-        q0 += (q0 + 1) * span <= u;
-        q0 = ok ? q0 : 0;
-        const int rem = u - q0 * span;
-        int bb, wl;
-        if (shared) {
-          bb = q0;
-          wl = rem >> 1;
-          half[k] = rem & 1;
+      for (int i = 0; i < kMaxGroups; ++i) {
+        if (i >= R.my_groups) break;  // uniform
+        const int wl = (R.cw + R.wpt * i) * kGroupWords + (rem >> 1);
+        const int col = (w_begin + wl) * 32 + 8 * (rem & 1) + 2 * qq;
+        const bool valid = wl < w_count;
+        dst_off[i] = valid ? wl * kSlot + 32 * (rem & 1) + 8 * qq : -1;
+        if constexpr (kInX) {
+          const int xo = valid ? col * 2 : kOob;
+          ra[i][0] = __builtin_amdgcn_raw_buffer_load_b32(xres, xo, 0, 0);
+          rb[i][0] = __builtin_amdgcn_raw_buffer_load_b32(xres, xo + 32, 0, 0);
+          rc[i][0] = __builtin_amdgcn_raw_buffer_load_b32(sres, xo, 0, 0);
+          rd[i][0] = __builtin_amdgcn_raw_buffer_load_b32(sres, xo + 32, 0, 0);
         } else {
-          // q0 = the wave's group index i, rem = (batch row, word, half)
-          bb = rem >> 4;
-          wl = (R.cw + R.wpt * q0) * kGroupWords + ((rem & 15) >> 1);
-          half[k] = rem & 1;
-        }
-        const bool valid = ok && wl < w_count;
-        col[k] = (w_begin + wl) * 32 + 8 * half[k];
-        off[k] = valid ? (int)(bb * K) + col[k] : kOob;
-        slot_off[k] = valid ? bb * bstride + wl * kSlot : -1;
-      }
-      UnitRaw raw[2], rawb[2];
-#pragma unroll
-      for (int k = 0; k < 2; ++k) {
-        if (has[k]) {
-          raw[k] = load_unit<kInX>(xres, sres, off[k], col[k]);
-          if (two_parts) rawb[k] = load_unit<kInX>(xres, sres, off[k], col[k], part_elems);
+          const int to = valid ? col * 4 : kOob;
+          ra[i] = __builtin_amdgcn_raw_buffer_load_b64(xres, to, 0, 0);
+          rb[i] = __builtin_amdgcn_raw_buffer_load_b64(xres, to + 64, 0, 0);
+          if (two_parts) {
+            const int to2 = valid ? (col + part_elems) * 4 : kOob;
+            rc[i] = __builtin_amdgcn_raw_buffer_load_b64(xres, to2, 0, 0);
+            rd[i] = __builtin_amdgcn_raw_buffer_load_b64(xres, to2 + 64, 0, 0);
+          }
         }
       }
 #pragma unroll
-      for (int k = 0; k < 2; ++k) {
-        if (has[k]) {
-          float v[16];
-          unit_values<kInX>(raw[k], v, two_parts ? &rawb[k] : nullptr);
-          store_unit(slot_off[k] >= 0 ? xs + slot_off[k] : junk, half[k], v);
+      for (int i = 0; i < kMaxGroups; ++i) {
+        if (i >= R.my_groups) break;  // uniform
+        float v[4];  // columns c, c+1, c+16, c+17
+        if constexpr (kInX) {
+          v[0] = bf16_to_f32(ra[i][0] & 0xffffu) * f16_to_f32((uint16_t)(rc[i][0] & 0xffffu));
+          v[1] = bf16_to_f32(ra[i][0] >> 16) * f16_to_f32((uint16_t)(rc[i][0] >> 16));
+          v[2] = bf16_to_f32(rb[i][0] & 0xffffu) * f16_to_f32((uint16_t)(rd[i][0] & 0xffffu));
+          v[3] = bf16_to_f32(rb[i][0] >> 16) * f16_to_f32((uint16_t)(rd[i][0] >> 16));
+        } else {
+          v[0] = __uint_as_float(ra[i][0]);
+          v[1] = __uint_as_float(ra[i][1]);
+          v[2] = __uint_as_float(rb[i][0]);
+          v[3] = __uint_as_float(rb[i][1]);
+          if (two_parts) {
+            v[0] += __uint_as_float(rc[i][0]);
+            v[1] += __uint_as_float(rc[i][1]);
+            v[2] += __uint_as_float(rd[i][0]);
+            v[3] += __uint_as_float(rd[i][1]);
+          }
+        }
+        const uint32_t h0 = pack_bf16x2(v[0], v[2]), h1 = pack_bf16x2(v[1], v[3]);
+        const uint32_t l0 =
+            pack_bf16x2(v[0] - bf16_to_f32(h0 & 0xffffu), v[2] - bf16_to_f32(h0 >> 16));
+        const uint32_t l1 =
+            pack_bf16x2(v[1] - bf16_to_f32(h1 & 0xffffu), v[3] - bf16_to_f32(h1 >> 16));
+        uint8_t *dst = dst_off[i] >= 0 ? xs + dst_off[i] : junk + 32 * (rem & 1) + 8 * qq;
+        *reinterpret_cast<uint2 *>(dst) = make_uint2(h0, h1);
+        *reinterpret_cast<uint2 *>(dst + 64) = make_uint2(l0, l1);
+      }
+    } else {
+      // pass stride and this thread's first unit
+      const int stride = shared ? 2 * kThreads : 128;
+      const int first = shared ? tid : lane;
+      const int wave_first = shared ? 64 * wave : 0;
+#pragma unroll
+      for (int it = 0; it < kStageIters; ++it) {
+        const int base = it * stride;
+        if (base >= nunits) break;  // uniform
+        int slot_off[2], half[2], off[2], col[2];
+        bool has[2];
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+          const int u = base + (stride >> 1) * k + first;
+          has[k] = base + (stride >> 1) * k + wave_first < nunits;  // wave-uniform
+          const bool ok = u < nunits;
+          // u / span for u < 2^12: a float estimate, corrected by one step
+          int q0 = (int)((float)u * inv_span);
+          q0 -= q0 * span > u;
+          q0 += (q0 + 1) * span <= u;
+          q0 = ok ? q0 : 0;
+          const int rem = u - q0 * span;
+          int bb, wl;
+          if (shared) {
+            bb = q0;
+            wl = rem >> 1;
+            half[k] = rem & 1;
+          } else {
+            // q0 = the wave's group index i, rem = (batch row, word, half)
+            bb = rem >> 4;
+            wl = (R.cw + R.wpt * q0) * kGroupWords + ((rem & 15) >> 1);
+            half[k] = rem & 1;
+          }
+          const bool valid = ok && wl < w_count;
+          col[k] = (w_begin + wl) * 32 + 8 * half[k];
+          off[k] = valid ? (int)(bb * K) + col[k] : kOob;
+          slot_off[k] = valid ? bb * bstride + wl * kSlot : -1;
+        }
+        UnitRaw raw[2], rawb[2];
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+          if (has[k]) {
+            raw[k] = load_unit<kInX>(xres, sres, off[k], col[k]);
+            if (two_parts) rawb[k] = load_unit<kInX>(xres, sres, off[k], col[k], part_elems);
+          }
+        }
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
+          if (has[k]) {
+            float v[16];
+            unit_values<kInX>(raw[k], v, two_parts ? &rawb[k] : nullptr);
+            store_unit(slot_off[k] >= 0 ? xs + slot_off[k] : junk, half[k], v);
+          }
         }
       }
     }
