@@ -34,8 +34,8 @@ POOL_BYTES = 512 << 20          # > 2 x 256 MB MALL
 # the source hash differs.
 GEMV_TRAFFIC = {"sources": ("paper_2609_06161_amd/csrc/af1_gemv.hip",
                             "paper_2609_06161_amd/csrc/af1_device.h"),
-                "sha256": "84510e39b3d02b600b6a3d66d3d70dea887fcb855bd4f954c6c9e3816992d642",
-                "bytes_per_call": 2704905}
+                "sha256": "586a740f16142e4b151767b32fc9639e304b9e36d228a960afe99cc3aba2d73c",
+                "bytes_per_call": 2783706}
 
 
 def measured_gemv_traffic():
