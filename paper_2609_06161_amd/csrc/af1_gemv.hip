@@ -258,31 +258,30 @@ __device__ __forceinline__ void stage_body(
   const int w_begin = R.w_begin;
   const int w_count = R.w_count;
 
-  // 1. Sign words of this wave's groups, issued before anything else as
-  //    unconditional buffer loads.  Lanes past the last row or the slab's
-  //    last word read data that never reaches a stored output: a ragged
-  //    group's tail meets the zero slot on the B side, and rows past `rows`
-  //    are not written.  Groups past my_groups use an out-of-range offset:
-  //    no branch, so the compiler has no join at which to wait for them.
-  //    One 8-byte load per lane; buffer range checking applies per dword,
-  //    so a pair whose second word lies past the buffer still returns its
-  //    first word (a second word past the row but inside the buffer is an
-  //    out-of-slab word and meets the zero slot).
+  // 1. Sign words of this wave's groups, issued before anything else, one
+  //    8-byte load per lane and group.  Lanes past the last row or the
+  //    slab's last word read data that never reaches a stored output: a
+  //    ragged group's tail meets the zero slot on the B side, and rows past
+  //    `rows` are not written.  Buffer range checking applies per dword, so
+  //    a pair whose second word lies past the buffer still returns its first
+  //    word (a second word past the row but inside the buffer is an
+  //    out-of-slab word and meets the zero slot).  Only the wave's own
+  //    groups are loaded, under a uniform branch: issuing out-of-range loads
+  //    for the other groups instead (to avoid the branch) still sent them
+  //    through the load path and cost 0.5 us of the 4096^2 layer at b=1.
   const int rho = lane & 15;
   const int q = lane >> 4;
   u32x2 wv[kMaxGroups];
   {
     const int64_t left = (int64_t)(rows - R.row0) * wpr * 4;
     const __amdgpu_buffer_rsrc_t mres = buffer_rsrc(M + (size_t)R.row0 * wpr, left);
-    // The group count lives in a vector register here so that the choice of
-    // offset is a select, not a branch around the load.
-    int my_groups_v = R.my_groups;
-    asm volatile("" : "+v"(my_groups_v));
 #pragma unroll
     for (int i = 0; i < kMaxGroups; ++i) {
-      const int wl = (R.cw + R.wpt * i) * kGroupWords + 2 * q;
-      const int off = i < my_groups_v ? (rho * wpr + w_begin + wl) * 4 : kOob;
-      wv[i] = __builtin_amdgcn_raw_buffer_load_b64(mres, off, 0, 0);
+      wv[i] = u32x2{0u, 0u};
+      if (i < R.my_groups) {  // uniform
+        const int wl = (R.cw + R.wpt * i) * kGroupWords + 2 * q;
+        wv[i] = __builtin_amdgcn_raw_buffer_load_b64(mres, (rho * wpr + w_begin + wl) * 4, 0, 0);
+      }
     }
   }
 
