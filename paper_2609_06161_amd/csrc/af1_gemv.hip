@@ -247,7 +247,8 @@ __device__ __forceinline__ void stage_body(
     const uint32_t *__restrict__ M, const void *__restrict__ in,
     const uint16_t *__restrict__ s_in, const uint16_t *__restrict__ row_scale, int rows,
     int wpr, int slab_words, int b, int rt_log2_arg, int nslabs, int mode, int in_parts,
-    void *__restrict__ out, float *__restrict__ part, uint32_t *__restrict__ cnt, int group) {
+    void *__restrict__ out, float *__restrict__ part, uint32_t *__restrict__ cnt, int group,
+    int red_off = 0) {
   const int rt_log2 = kMulti ? rt_log2_arg : 0;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   const int tid = threadIdx.x;
@@ -527,10 +528,13 @@ __device__ __forceinline__ void stage_body(
   // 4. Add the 16x16 tiles of the waves that share a row tile, through LDS
   //    (after every wave is done reading the staged input).  Accumulator
   //    layout: lane l holds rows 4*(l/16) + i (i = 0..3) of column l mod 16.
+  //    With red_off > 0 the tiles go to their own LDS region past the staged
+  //    input, and only one barrier is needed.
+  if (red_off == 0) __syncthreads();  // uniform
+  reinterpret_cast<float4 *>(lds + red_off)[wave * 64 + lane] =
+      make_float4(tot[0], tot[1], tot[2], tot[3]);
   __syncthreads();
-  reinterpret_cast<float4 *>(lds)[wave * 64 + lane] = make_float4(tot[0], tot[1], tot[2], tot[3]);
-  __syncthreads();
-  const float *redf = reinterpret_cast<const float *>(lds);
+  const float *redf = reinterpret_cast<const float *>(lds + red_off);
   float sum[kMaxOutPerThread];
 #pragma unroll
   for (int k = 0; k < kMaxOutPerThread; ++k) {
@@ -624,10 +628,10 @@ __global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
     const uint32_t *__restrict__ M, const void *__restrict__ in,
     const uint16_t *__restrict__ s_in, const uint16_t *__restrict__ row_scale, int rows,
     int wpr, int slab_words, int b, int rt_log2, int nslabs, int mode, int in_parts,
-    void *__restrict__ out, float *__restrict__ part, uint32_t *__restrict__ cnt) {
+    void *__restrict__ out, float *__restrict__ part, uint32_t *__restrict__ cnt, int red_off) {
   stage_body<kInX, kOutY, kHiLoCols, kMulti>(M, in, s_in, row_scale, rows, wpr, slab_words, b,
                                              rt_log2, nslabs, mode, in_parts, out, part, cnt,
-                                             (int)blockIdx.x);
+                                             (int)blockIdx.x, red_off);
 }
 
 // One stage of several layers that share the input width (the segments):
@@ -663,9 +667,13 @@ __global__ __launch_bounds__(kThreads) void gemv_segs_kernel(const Segs segs, in
       slab_words, b, rt_log2, 1, mode, in_parts, segs.out[sg], nullptr, nullptr, g - g0);
 }
 
-size_t lds_bytes_for(int64_t b, int slab_words) {
+size_t lds_stage_bytes(int64_t b, int slab_words) {
   // zero slot, staged slots, 16 scratch slots for lanes without a unit
-  const size_t stage = (size_t)kSlot * 17 + (size_t)b * row_stride(slab_words);
+  return (size_t)kSlot * 17 + (size_t)b * row_stride(slab_words);
+}
+
+size_t lds_bytes_for(int64_t b, int slab_words) {
+  const size_t stage = lds_stage_bytes(b, slab_words);
   return stage > (size_t)kRedBytes ? stage : (size_t)kRedBytes;
 }
 
@@ -781,13 +789,24 @@ hipError_t launch_stage(const StageArgs &a, const StagePlan &p, hipStream_t s) {
   const int rows_wg = kTileRows << p.rt_log2;
   if ((int64_t)rows_wg * a.b > (int64_t)kThreads * kMaxOutPerThread) return hipErrorInvalidValue;
   dim3 grid((unsigned)((a.rows + rows_wg - 1) / rows_wg), (unsigned)p.nslabs);
-  const size_t lds = lds_bytes_for(a.b, p.slab_words < a.wpr ? p.slab_words : a.wpr);
+  const bool multi = p.rt_log2 > 0;
+  size_t lds = lds_bytes_for(a.b, p.slab_words < a.wpr ? p.slab_words : a.wpr);
+  // One row tile per workgroup: the cross-wave sums get their own LDS region
+  // past the staged input when it fits (one barrier instead of two).
+  int red_off = 0;
+  if (!multi) {
+    const size_t stage = (lds_stage_bytes(a.b, p.slab_words < a.wpr ? p.slab_words : a.wpr) + 15) &
+                         ~(size_t)15;
+    if (stage + kRedBytes <= (size_t)kLdsBudget) {
+      red_off = (int)stage;
+      lds = stage + kRedBytes;
+    }
+  }
   auto go = [&](auto kernel) {
     kernel<<<grid, kThreads, lds, s>>>(a.M, a.in, a.s_in, a.row_scale, a.rows, a.wpr,
                                        p.slab_words, a.b, p.rt_log2, p.nslabs, p.mode,
-                                       a.in_parts, a.out, a.part, a.cnt);
+                                       a.in_parts, a.out, a.part, a.cnt, red_off);
   };
-  const bool multi = p.rt_log2 > 0;
   if (a.b <= 8) {
     if (multi)
       go(gemv_stage_kernel<kInX, kOutY, true, true>);
