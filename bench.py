@@ -34,8 +34,8 @@ POOL_BYTES = 512 << 20          # > 2 x 256 MB MALL
 # the source hash differs.
 GEMV_TRAFFIC = {"sources": ("paper_2609_06161_amd/csrc/af1_gemv.hip",
                             "paper_2609_06161_amd/csrc/af1_device.h"),
-                "sha256": "1d7ad872a1a8e4093e0fe83f0d993e656c983816b8354d7b8085b5bd77e4941c",
-                "bytes_per_call": 2799057}
+                "sha256": "4d444f6c6528d26dd01e7dedab272ac03fbf52066bb524e759818d0f07e6a3d8",
+                "bytes_per_call": 2784727}
 
 
 def measured_gemv_traffic():
