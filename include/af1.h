@@ -181,8 +181,15 @@ AF1_API af1_status af1_linear_gemv_multi(const af1_factorized_linear *Ls, int32_
  * s_in .* x is rounded once to fp16 (the bf16 x fp16 product is exact in
  * fp32), the intermediate s_mid .* (Bv (s_in .* x)) is rounded once to fp16
  * before the second product, s_out is applied in fp32 and y is rounded to
- * bfloat16.  Both fp16 operands must stay below 65504 in magnitude; values
- * below 2^-14 keep fewer significant bits.
+ * bfloat16.  Range: each token's two fp16 operands carry a power of two
+ * chosen from that token alone (its largest |s_in .* x| for the first, the
+ * bound sum_j |s_in_j x_j| * max|s_mid| on the intermediate for the
+ * second), undone in fp32 before s_out, so no fp16 operand overflows or
+ * goes subnormal for any finite bf16 x: the GEMM is defined on the same
+ * inputs as the GEMV.  Entries below 2^-27 of their token's largest one
+ * keep fewer digits, as in any fp16 rounding.
+ * Defining passage: App. A.2.1 (Diag form, label eq:double_factor_equiv)
+ * and Sec. 4.1 (label eq:final_reconstruction), as for af1_linear_gemv.
  */
 AF1_API size_t af1_gemm_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T);
 AF1_API af1_status af1_linear_gemm(const af1_factorized_linear *L, const uint16_t *x,
@@ -217,8 +224,9 @@ AF1_API af1_status af1_pack_transpose(const uint32_t *src, int64_t rows, int64_t
  * af1_linear_forward_train -- y as af1_linear_gemm computes it (same
  * kernels and rounding, bit-identical y), and in `saved` the two pre-scale
  * intermediates the gradients need: v = Bv (s_in .* x) ([T, r], rounded to
- * fp16, in a layout private to the library) and z = Bu (s_mid .* v)
- * ([T, m], fp32, the second product's accumulator).
+ * fp16 at a per-token power-of-two scale, in a layout private to the
+ * library), z = Bu (s_mid .* v) ([T, m], fp32, the second product's
+ * accumulator, unscaled) and the per-token scale record.
  *   saved : device, at least af1_train_saved_bytes(m, n, r, T) bytes,
  *           written; hand it unchanged to af1_linear_backward with the same
  *           layer, x and T.

@@ -171,43 +171,267 @@ __device__ __forceinline__ int pair_pos(int c) {
   return (c & ~31) + 2 * (c & 15) + ((c >> 4) & 1);
 }
 
-// x (bf16, [T][K]) and s (fp16, [K]) -> xp = fp16(x .* s) ([T][K], pair
-// order).  The product of a bf16 and an fp16 value is exact in fp32, so
-// each entry is rounded once.  One thread per 16 columns: 8 columns
-// c .. c+7 and their partners c+16 .. c+23 become the pair dwords
+// Range guard of the forward's fp16 operands, per token t (one row of x).
+// The layer is defined for any input (App. A.2.1), but fp16 holds only
+// 2^-24 .. 65504, so both fp16 operands carry a power-of-two scale that is
+// undone in fp32:
+//   xp[t]  = fp16(s_in .* x[t] * 2^e_t), e_t putting the row's largest entry
+//            in [2^13, 2^14);
+//   Z[t]   = fp16(s_mid .* (Bv xp[t]) * 2^-c_t), where L_t = sum_j |s_in_j
+//            x_tj| 2^e_t bounds every |(Bv xp[t])_k| (the signs are +-1),
+//            and c_t makes L_t * max|s_mid| * 2^-c_t < 2^14;
+//   y[t]   = bf16(s_out .* (Bu Z[t]) * 2^(c_t - e_t)).
+// Each rounding to fp16 is therefore a plain 2^-11 relative rounding with no
+// overflow, whatever the magnitude of x (entries far below a row's largest
+// one, under 2^-27 of it, keep fewer digits, as in any fp16 rounding).
+// Scaling by a power of two is exact, so for inputs inside fp16's range the
+// results differ from unscaled operands only where they would have been
+// subnormal.  The per-token record is
+//   tinfo[2t] = L_t (fp32),  tinfo[2t + 1] = e_t (int32 bits),
+//   tinfo[2T] = max_k |s_mid_k|.
+// `tinfo_floats(T)` floats hold it.
+__host__ __device__ constexpr int64_t tinfo_floats(int64_t T) { return 2 * T + 4; }
+
+// Exponent c_t of the intermediate's scale: 2^-c_t L_t smax' < 2^14, with
+// smax' = max|s_mid| (1 when every s_mid is zero).  0 for an all-zero row.
+__device__ __forceinline__ int mid_exp(float L, float smax) {
+  const float b = L * (smax > 0.f ? smax : 1.f);
+  if (!(b > 0.f) || !__builtin_isfinite(b)) return 0;
+  int k;
+  frexpf(b, &k);  // b = f 2^k, f in [0.5, 1): b < 2^k
+  return k - 14;
+}
+
+// Exponent of max|s_mid|: smax' < 2^es (so 2^(es - c_t) L_t < 2^15).
+__device__ __forceinline__ int smax_exp(float smax) {
+  int k;
+  frexpf(smax > 0.f && __builtin_isfinite(smax) ? smax : 1.f, &k);
+  return k;
+}
+
+// The token's shift of the forward output before its row scale: the first
+// product's accumulator (kMid modes) is scaled by 2^-c_t, the second's (kOut
+// modes) by 2^(c_t - e_t), which leaves the unscaled value.
+template <bool kFirst>
+__device__ __forceinline__ int fwd_shift(const float *__restrict__ tinfo, int T, int t) {
+  const float2 ti = reinterpret_cast<const float2 *>(tinfo)[t];
+  const int c = mid_exp(ti.x, tinfo[2 * T]);
+  return kFirst ? -c : c - __float_as_int(ti.y);
+}
+
+// The training forward saves V = fp16(v 2^(e_t - c_t + es)) (v = Bv (s_in
+// .* x), es = smax_exp); v = V 2^shift with this shift.
+__device__ __forceinline__ int saved_v_shift(const float *__restrict__ tinfo, int T, int t) {
+  const float2 ti = reinterpret_cast<const float2 *>(tinfo)[t];
+  return mid_exp(ti.x, tinfo[2 * T]) - smax_exp(tinfo[2 * T]) - __float_as_int(ti.y);
+}
+
+// One token row per workgroup: x (bf16, [T][K]) and s (fp16, [K]) ->
+// xp = fp16(x .* s 2^e_t) ([T][K], pair order) and the token's record.
+// Three steps, each ending in a reduction over the workgroup:
+//  1. the largest |x| (bf16 magnitudes compare as integers), whose binary
+//     exponent gives a first shift e1 with |x 2^e1| < 1 (so x 2^e1 s_in is
+//     finite and exact for any bf16 x and fp16 s_in);
+//  2. p = x 2^e1 s_in: the largest |p| and sum |p|, which give e2;
+//  3. xp = fp16(p 2^e2), e_t = e1 + e2.
+// Rows of up to 2048 units (1024 threads, two units each) are loaded once
+// (x and s_in together) and kept in registers through the three steps;
+// wider rows are read again.
+// Block T stores max |s_mid| instead.  A unit is 16 columns: 8 columns
+// c .. c+7 and their partners c+16 .. c+23, which become the pair dwords
 // 8h .. 8h+7 of their group.
-__device__ __forceinline__ void pair_order_unit(const uint16_t *__restrict__ x,
-                                                const uint16_t *__restrict__ sc,
-                                                uint16_t *__restrict__ xp, int K, int64_t u) {
-  const int units_per_row = K / 16;
-  const int t = (int)(u / units_per_row);
-  const int ur = (int)(u % units_per_row);
-  const int c = (ur >> 1) * 32 + 8 * (ur & 1);
-  const uint16_t *src = x + (size_t)t * K + c;
-  const u32x4 lo = *reinterpret_cast<const u32x4 *>(src);
-  const u32x4 hi = *reinterpret_cast<const u32x4 *>(src + 16);
-  const u32x4 slo = *reinterpret_cast<const u32x4 *>(sc + c);
-  const u32x4 shi = *reinterpret_cast<const u32x4 *>(sc + c + 16);
+__device__ __forceinline__ void load_x_unit(const uint16_t *__restrict__ row, int c, u32x4 &lo,
+                                            u32x4 &hi) {
+  lo = *reinterpret_cast<const u32x4 *>(row + c);
+  hi = *reinterpret_cast<const u32x4 *>(row + c + 16);
+}
+
+__device__ __forceinline__ int unit_col(int u) { return (u >> 1) * 32 + 8 * (u & 1); }
+
+// Sum and maximum over the workgroup (fixed order: lanes by butterfly, then
+// the waves in order), every thread receives both.  red holds 32 floats.
+__device__ __forceinline__ void block_sum_max(float &sum, float &mx, float *red) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int waves = blockDim.x >> 6;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    sum += __shfl_xor(sum, off, 64);
+    mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+  }
+  __syncthreads();  // red may still be read from a previous call
+  if (lane == 0) {
+    red[wave] = sum;
+    red[16 + wave] = mx;
+  }
+  __syncthreads();
+  sum = red[0];
+  mx = red[16];
+  for (int w = 1; w < waves; ++w) {
+    sum += red[w];
+    mx = fmaxf(mx, red[16 + w]);
+  }
+}
+
+// Block T: max |s_mid| into tinfo[2T].
+__device__ __forceinline__ void prep_smax(const uint16_t *__restrict__ s_mid, int r, int T,
+                                          float *__restrict__ tinfo, float *red) {
+  float sum = 0.f, mx = 0.f;
+  for (int k = threadIdx.x; k < r; k += blockDim.x) mx = fmaxf(mx, fabsf(f16_to_f32(s_mid[k])));
+  block_sum_max(sum, mx, red);
+  if (threadIdx.x == 0) tinfo[2 * T] = mx;
+}
+
+// e1 from the row's largest bf16 magnitude pattern: |x 2^e1| < 1.
+__device__ __forceinline__ int prep_e1(uint32_t mb) {
+  const float xmax = bf16_to_f32(mb);
+  int e1 = 0;
+  if (xmax > 0.f && __builtin_isfinite(xmax)) {
+    frexpf(xmax, &e1);  // xmax < 2^e1
+    e1 = -e1;
+  }
+  return e1;
+}
+
+// e2 from the largest |p|: pmax 2^e2 in [2^13, 2^14).
+__device__ __forceinline__ int prep_e2(float pmax) {
+  int e2 = 0;
+  if (pmax > 0.f && __builtin_isfinite(pmax)) {
+    frexpf(pmax, &e2);  // pmax = f 2^k, f in [0.5, 1)
+    e2 = 14 - e2;
+  }
+  return e2;
+}
+
+// Pair-order dwords of one unit from its 16 values (v[d] = column c + d,
+// v[8 + d] = column c + 16 + d), stored at the unit's place in xp.
+__device__ __forceinline__ void prep_store(uint16_t *__restrict__ xp, int t, int K, int c,
+                                           const float (&v)[16], int e2) {
   uint32_t d[8];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const uint32_t sl = slo[e], sh = shi[e];
-    d[2 * e] = pack_f16x2(__uint_as_float(lo[e] << 16) * f16_lo(sl),
-                          __uint_as_float(hi[e] << 16) * f16_lo(sh));
-    d[2 * e + 1] = pack_f16x2(__uint_as_float(lo[e] & 0xffff0000u) * f16_hi(sl),
-                              __uint_as_float(hi[e] & 0xffff0000u) * f16_hi(sh));
-  }
+  for (int k = 0; k < 8; ++k) d[k] = pack_f16x2(ldexpf(v[k], e2), ldexpf(v[8 + k], e2));
   uint4 *dst = reinterpret_cast<uint4 *>(xp + (size_t)t * K + (c & ~31) + 2 * (c & 15));
   dst[0] = make_uint4(d[0], d[1], d[2], d[3]);
   dst[1] = make_uint4(d[4], d[5], d[6], d[7]);
 }
 
-// The A operand of G1: fp16(s_in .* x) in pair order.
-__global__ __launch_bounds__(256) void prep_kernel(const uint16_t *__restrict__ x,
-                                                   const uint16_t *__restrict__ s_in,
-                                                   uint16_t *__restrict__ xp, int T, int n) {
-  const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (u < (int64_t)T * (n / 16)) pair_order_unit(x, s_in, xp, n, u);
+// p values of one unit: x 2^e1 s_in, v[d] = column c + d, v[8 + d] = c + 16 + d.
+__device__ __forceinline__ void prep_values(const u32x4 &lo, const u32x4 &hi, const u32x4 &slo,
+                                            const u32x4 &shi, int e1, float (&v)[16]) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    v[2 * e] = ldexpf(__uint_as_float(lo[e] << 16), e1) * f16_lo(slo[e]);
+    v[2 * e + 1] = ldexpf(__uint_as_float(lo[e] & 0xffff0000u), e1) * f16_hi(slo[e]);
+    v[8 + 2 * e] = ldexpf(__uint_as_float(hi[e] << 16), e1) * f16_lo(shi[e]);
+    v[8 + 2 * e + 1] = ldexpf(__uint_as_float(hi[e] & 0xffff0000u), e1) * f16_hi(shi[e]);
+  }
+}
+
+__device__ __forceinline__ uint32_t unit_maxbits(const u32x4 &lo, const u32x4 &hi) {
+  uint32_t mb = 0;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    mb = max(mb, max(lo[e] & 0x7fffu, (lo[e] >> 16) & 0x7fffu));
+    mb = max(mb, max(hi[e] & 0x7fffu, (hi[e] >> 16) & 0x7fffu));
+  }
+  return mb;
+}
+
+// kU > 0: the row's units (at most kU per thread) stay in registers, and x
+// and s_in are loaded once, together, before the first reduction.  kU = 0:
+// any width, three passes over the row (the second and third hit the caches).
+template <int kU, int kThreads>
+__global__ __launch_bounds__(kThreads) void prep_kernel(
+    const uint16_t *__restrict__ x, const uint16_t *__restrict__ s_in,
+    uint16_t *__restrict__ xp, int T, int K, float *__restrict__ tinfo,
+    const uint16_t *__restrict__ s_mid, int r) {
+  __shared__ float red[32];
+  const int t = blockIdx.x;
+  if (t == T) {
+    prep_smax(s_mid, r, T, tinfo, red);
+    return;
+  }
+  const int units = K / 16;
+  const uint16_t *row = x + (size_t)t * K;
+  float l1 = 0.f, pmax = 0.f;
+  int e1, e2;
+  if constexpr (kU > 0) {
+    u32x4 xl[kU], xh[kU], sl[kU], sh[kU];
+#pragma unroll
+    for (int i = 0; i < kU; ++i) {
+      const int u = threadIdx.x + kThreads * i;
+      if (u < units) {
+        const int c = unit_col(u);
+        load_x_unit(row, c, xl[i], xh[i]);
+        sl[i] = *reinterpret_cast<const u32x4 *>(s_in + c);
+        sh[i] = *reinterpret_cast<const u32x4 *>(s_in + c + 16);
+      } else {
+        xl[i] = xh[i] = sl[i] = sh[i] = u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+    uint32_t mb = 0;
+#pragma unroll
+    for (int i = 0; i < kU; ++i) mb = max(mb, unit_maxbits(xl[i], xh[i]));
+    {
+      float sum = 0.f, mx = __uint_as_float(mb);  // a non-negative pattern orders as its value
+      block_sum_max(sum, mx, red);
+      e1 = prep_e1(__float_as_uint(mx));
+    }
+    float v[kU][16];
+#pragma unroll
+    for (int i = 0; i < kU; ++i) {
+      prep_values(xl[i], xh[i], sl[i], sh[i], e1, v[i]);
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        pmax = fmaxf(pmax, fabsf(v[i][k]));
+        l1 += fabsf(v[i][k]);
+      }
+    }
+    block_sum_max(l1, pmax, red);
+    e2 = prep_e2(pmax);
+#pragma unroll
+    for (int i = 0; i < kU; ++i) {
+      const int u = threadIdx.x + kThreads * i;
+      if (u < units) prep_store(xp, t, K, unit_col(u), v[i], e2);
+    }
+  } else {
+    uint32_t mb = 0;
+    for (int u = threadIdx.x; u < units; u += kThreads) {
+      u32x4 lo, hi;
+      load_x_unit(row, unit_col(u), lo, hi);
+      mb = max(mb, unit_maxbits(lo, hi));
+    }
+    {
+      float sum = 0.f, mx = __uint_as_float(mb);
+      block_sum_max(sum, mx, red);
+      e1 = prep_e1(__float_as_uint(mx));
+    }
+    for (int u = threadIdx.x; u < units; u += kThreads) {
+      const int c = unit_col(u);
+      u32x4 lo, hi;
+      load_x_unit(row, c, lo, hi);
+      float v[16];
+      prep_values(lo, hi, *reinterpret_cast<const u32x4 *>(s_in + c),
+                  *reinterpret_cast<const u32x4 *>(s_in + c + 16), e1, v);
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        pmax = fmaxf(pmax, fabsf(v[k]));
+        l1 += fabsf(v[k]);
+      }
+    }
+    block_sum_max(l1, pmax, red);
+    e2 = prep_e2(pmax);
+    for (int u = threadIdx.x; u < units; u += kThreads) {
+      const int c = unit_col(u);
+      u32x4 lo, hi;
+      load_x_unit(row, c, lo, hi);
+      float v[16];
+      prep_values(lo, hi, *reinterpret_cast<const u32x4 *>(s_in + c),
+                  *reinterpret_cast<const u32x4 *>(s_in + c + 16), e1, v);
+      prep_store(xp, t, K, c, v, e2);
+    }
+  }
+  if (threadIdx.x == 0)
+    reinterpret_cast<float2 *>(tinfo)[t] = make_float2(ldexpf(l1, e2), __int_as_float(e1 + e2));
 }
 
 // C = rowscale * (A_pairorder x sign(W)^T), in the forms listed under Mode.
@@ -216,7 +440,8 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     const uint16_t *__restrict__ A, int T, int K, const uint32_t *__restrict__ W, int N,
     const uint16_t *__restrict__ rowscale, uint16_t *__restrict__ C, uint16_t *__restrict__ V,
     const uint16_t *__restrict__ S, float *__restrict__ F, const float *__restrict__ gscale,
-    int split_steps, float *__restrict__ P, int mix_full, int mix_splits, int mix_nN) {
+    int split_steps, float *__restrict__ P, int mix_full, int mix_splits, int mix_nN,
+    const float *__restrict__ tinfo) {
   constexpr bool kPairOut = kMode == kMid || kMode == kMidSave || kMode == kBwdMid;
   constexpr bool kBwd = kMode == kBwdMid || kMode == kBwdIn;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
@@ -487,6 +712,28 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     rs[j] = n < N ? (rowscale ? f16_to_f32(rowscale[n]) : 1.0f) : 0.f;
     cpos[j] = (kPairOut ? pair_pos(n) : n) - n0;
   }
+  // The forward's per-token range-guard shifts (see prep_kernel), applied to
+  // the accumulators before any rounding: a table of the tile's tokens in
+  // the idle sign buffers, read four consecutive tokens at a time (the rows
+  // 4(l/32) + (e mod 4) of an accumulator block).
+  if constexpr (!kBwd) {
+    int *shl = reinterpret_cast<int *>(lds + kW0);
+    for (int q = tid; q < kBM; q += kThreads)
+      shl[q] = t0 + q < T ? fwd_shift<kMode == kMid || kMode == kMidSave>(tinfo, T, t0 + q) : 0;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kTokBlocks; ++i)
+#pragma unroll
+      for (int e4 = 0; e4 < 4; ++e4) {
+        const int4 s4 = *reinterpret_cast<const int4 *>(shl + 32 * i + 8 * e4 + 4 * g);
+        const int sv[4] = {s4.x, s4.y, s4.z, s4.w};
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int e3 = 0; e3 < 4; ++e3)
+            acc[i][j][4 * e4 + e3] = ldexpf(acc[i][j][4 * e4 + e3], sv[e3]);
+      }
+  }
   auto stage_tile = [&](auto value) {
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
@@ -527,6 +774,13 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       const int off = t0 + row < T ? (t0 + row) * N * 2 + n0 * 2 + 16 * chunk : kOob;
       copy16(srs, lds + (kSCopies * wave + jj) * 1024, off);
     }
+    // kBwdMid: S is the saved intermediate, stored with the forward's
+    // per-token scale; vsl holds each token's shift back to v (idle sign
+    // buffers).
+    int *vsl = reinterpret_cast<int *>(lds + kW0);
+    if constexpr (kMode == kBwdMid) {
+      for (int q = tid; q < kBM; q += kThreads) vsl[q] = t0 + q < T ? saved_v_shift(tinfo, T, t0 + q) : 0;
+    }
     wait_copies();
     __syncthreads();
     // The 32-token block i lies in 64-token group (t0 + 32 i) / 64; its
@@ -556,7 +810,10 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
           const int row = 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
           const int pos = ((lpos >> 3) ^ (((row >> 2) & 1) << 2)) * 16 + cbyte;
           const uint16_t sv = *reinterpret_cast<const uint16_t *>(lds + row * 512 + pos);
-          part += acc[i][j][e] * fg[i] * (kMode == kBwdMid ? f16_to_f32(sv) : bf16_to_f32(sv));
+          if constexpr (kMode == kBwdMid)
+            part += ldexpf(acc[i][j][e] * fg[i] * f16_to_f32(sv), vsl[row]);
+          else
+            part += acc[i][j][e] * fg[i] * bf16_to_f32(sv);
         }
       part += __shfl_xor(part, 32, 64);
       if (g == 0 && n < N) F[(size_t)(t0 / kBM) * N + n] = part;
@@ -578,7 +835,8 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   store_tile(C);
   if constexpr (kMode == kMidSave) {
     __syncthreads();
-    stage_tile([&](int i, int j, int e) { return f32_to_f16(acc[i][j][e]); });
+    const int es = smax_exp(tinfo[2 * T]);
+    stage_tile([&](int i, int j, int e) { return f32_to_f16(ldexpf(acc[i][j][e], es)); });
     store_tile(V);
   }
   if constexpr (kMode == kOutSave) {
@@ -817,11 +1075,15 @@ __global__ __launch_bounds__(256) void bwd_finish_kernel(
 // concatenates them).
 template <int kMode>
 __device__ __forceinline__ void finish8(const float4 &lo, const float4 &hi, int cl, int ch, int p,
-                                        int t, int N, const uint16_t *__restrict__ rowscale,
+                                        int t, int T, int N, const uint16_t *__restrict__ rowscale,
                                         uint16_t *__restrict__ C, uint16_t *__restrict__ V,
-                                        float *__restrict__ F) {
+                                        float *__restrict__ F, const float *__restrict__ tinfo) {
   constexpr bool kPairOut = kMode == kMid || kMode == kMidSave;
-  const float l4[4] = {lo.x, lo.y, lo.z, lo.w}, h4[4] = {hi.x, hi.y, hi.z, hi.w};
+  // the token's range-guard shift (see prep_kernel) before any rounding
+  const int sh = fwd_shift<kPairOut>(tinfo, T, t);
+  const int es = kMode == kMidSave ? smax_exp(tinfo[2 * T]) : 0;
+  const float l4[4] = {ldexpf(lo.x, sh), ldexpf(lo.y, sh), ldexpf(lo.z, sh), ldexpf(lo.w, sh)};
+  const float h4[4] = {ldexpf(hi.x, sh), ldexpf(hi.y, sh), ldexpf(hi.z, sh), ldexpf(hi.w, sh)};
   float acc[8];
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
@@ -843,15 +1105,16 @@ __device__ __forceinline__ void finish8(const float4 &lo, const float4 &hi, int 
     const float a0 = acc[2 * k] * r0, a1 = acc[2 * k + 1] * r1;
     c[k] = kPairOut ? (uint32_t)f32_to_f16(a0) | ((uint32_t)f32_to_f16(a1) << 16)
                     : (uint32_t)f32_to_bf16(a0) | ((uint32_t)f32_to_bf16(a1) << 16);
-    v[k] = (uint32_t)f32_to_f16(acc[2 * k]) | ((uint32_t)f32_to_f16(acc[2 * k + 1]) << 16);
+    v[k] = (uint32_t)f32_to_f16(ldexpf(acc[2 * k], es)) |
+           ((uint32_t)f32_to_f16(ldexpf(acc[2 * k + 1], es)) << 16);
   }
   const size_t o = (size_t)t * N + p;
   *reinterpret_cast<uint4 *>(C + o) = make_uint4(c[0], c[1], c[2], c[3]);
   if constexpr (kMode == kMidSave)
     *reinterpret_cast<uint4 *>(V + o) = make_uint4(v[0], v[1], v[2], v[3]);
   if constexpr (kMode == kOutSave) {
-    *reinterpret_cast<float4 *>(F + o) = lo;
-    *reinterpret_cast<float4 *>(F + o + 4) = hi;
+    *reinterpret_cast<float4 *>(F + o) = make_float4(l4[0], l4[1], l4[2], l4[3]);
+    *reinterpret_cast<float4 *>(F + o + 4) = make_float4(h4[0], h4[1], h4[2], h4[3]);
   }
 }
 
@@ -866,7 +1129,8 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *__restr
                                                             const uint16_t *__restrict__ rowscale,
                                                             uint16_t *__restrict__ C,
                                                             uint16_t *__restrict__ V,
-                                                            float *__restrict__ F) {
+                                                            float *__restrict__ F,
+                                                            const float *__restrict__ tinfo) {
   constexpr bool kPairOut = kMode == kMid || kMode == kMidSave;
   const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int upr = N / 8;
@@ -904,7 +1168,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *__restr
       hi.x += b[q].x; hi.y += b[q].y; hi.z += b[q].z; hi.w += b[q].w;
     }
   }
-  finish8<kMode>(lo, hi, cl, ch, p, t, N, rowscale, C, V, F);
+  finish8<kMode>(lo, hi, cl, ch, p, t, T, N, rowscale, C, V, F, tinfo);
 }
 
 // The reduction of a mixed grid (forward modes): for each tile cut into
@@ -918,7 +1182,8 @@ __global__ __launch_bounds__(256) void mixed_reduce_kernel(const float *__restri
                                                            const uint16_t *__restrict__ rowscale,
                                                            uint16_t *__restrict__ C,
                                                            uint16_t *__restrict__ V,
-                                                           float *__restrict__ F) {
+                                                           float *__restrict__ F,
+                                                           const float *__restrict__ tinfo) {
   constexpr bool kPairOut = kMode == kMid || kMode == kMidSave;
   const int h = blockIdx.x >> 4;
   const int unit = ((blockIdx.x & 15) << 8) + threadIdx.x;  // 0 .. 4095
@@ -950,7 +1215,7 @@ __global__ __launch_bounds__(256) void mixed_reduce_kernel(const float *__restri
     lo.x += a[q].x; lo.y += a[q].y; lo.z += a[q].z; lo.w += a[q].w;
     hi.x += b[q].x; hi.y += b[q].y; hi.z += b[q].z; hi.w += b[q].w;
   }
-  finish8<kMode>(lo, hi, n0 + cl, n0 + ch, n0 + pl, t, N, rowscale, C, V, F);
+  finish8<kMode>(lo, hi, n0 + cl, n0 + ch, n0 + pl, t, T, N, rowscale, C, V, F, tinfo);
 }
 
 // The reduction of a split-K backward contraction.  A workgroup takes 64
@@ -964,7 +1229,7 @@ template <int kMode>
 __global__ __launch_bounds__(256) void splitk_bwd_reduce_kernel(
     const float *__restrict__ P, int S, int T, int N, const uint16_t *__restrict__ rowscale,
     const float *__restrict__ gscale, uint16_t *__restrict__ C, const uint16_t *__restrict__ Sv,
-    float *__restrict__ F) {
+    float *__restrict__ F, const float *__restrict__ tinfo) {
   constexpr bool kPairOut = kMode == kBwdMid;
   constexpr int kReduceBatch = 8;
   __shared__ float red[64][kBwdReduceCols + 1];
@@ -1004,6 +1269,8 @@ __global__ __launch_bounds__(256) void splitk_bwd_reduce_kernel(
     }
     const float2 gs = reinterpret_cast<const float2 *>(gscale)[t >> 6];
     const float fg = kMode == kBwdMid ? gs.x : gs.x / gs.y;
+    // kBwdMid: S is the saved intermediate at the forward's per-token scale
+    const int vsh = kMode == kBwdMid ? saved_v_shift(tinfo, T, t) : 0;
     const float l4[4] = {lo.x, lo.y, lo.z, lo.w}, h4[4] = {hi.x, hi.y, hi.z, hi.w};
     float acc[8];
     int col[8];
@@ -1026,7 +1293,7 @@ __global__ __launch_bounds__(256) void splitk_bwd_reduce_kernel(
         const int e = 2 * k + h;
         const uint32_t sbits = h ? sw[k] >> 16 : sw[k] & 0xffffu;
         const float sval = kMode == kBwdMid ? f16_to_f32((uint16_t)sbits) : bf16_to_f32(sbits);
-        g[e] = acc[e] * fg * sval;
+        g[e] = kMode == kBwdMid ? ldexpf(acc[e] * fg * sval, vsh) : acc[e] * fg * sval;
         const float rs = f16_to_f32(rowscale[col[e]]);
         o[h] = kMode == kBwdMid ? acc[e] * rs * gs.y : acc[e] * fg * rs;
       }
@@ -1155,7 +1422,8 @@ template <int kMode>
 hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *W, int64_t N,
                        const uint16_t *rs, uint16_t *C, uint16_t *V, const uint16_t *S,
                        float *F, hipStream_t s, int *tile_tokens = nullptr,
-                       const float *gscale = nullptr, float *P = nullptr) {
+                       const float *gscale = nullptr, float *P = nullptr,
+                       const float *tinfo = nullptr) {
   constexpr bool kFwd = kMode == kMid || kMode == kMidSave || kMode == kOut || kMode == kOutSave;
   const ContractionPlan p = plan_contraction(T, K, N, P != nullptr, device_cus(), kFwd && P);
   if (p.splits > 1 && p.bm != 64) return hipErrorInvalidValue;  // see bingemm_kernel
@@ -1166,17 +1434,17 @@ hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *
   if (p.bm == 64)
     bingemm_kernel<kMode, 64, kStages64><<<g, kThreads, Lds<64, kStages64>::kBytes, s>>>(
         A, (int)T, (int)K, W, (int)N, rs, C, V, S, F, gscale, p.split_steps, P, p.mix_full,
-        p.mix_splits, (int)p.gx);
+        p.mix_splits, (int)p.gx, tinfo);
   else
     bingemm_kernel<kMode, BM, kStages128><<<g, kThreads, Lds<BM, kStages128>::kBytes, s>>>(
         A, (int)T, (int)K, W, (int)N, rs, C, V, S, F, gscale, p.split_steps, P, p.mix_full,
-        p.mix_splits, (int)p.gx);
+        p.mix_splits, (int)p.gx, tinfo);
   if (tile_tokens) *tile_tokens = p.splits > 1 ? 64 : p.bm;
   if (p.mix_full > 0) {
     if constexpr (kFwd) {
       const unsigned blocks = (unsigned)((tiles - p.mix_full) * 16);
       mixed_reduce_kernel<kMode><<<blocks, 256, 0, s>>>(P, p.mix_splits, p.mix_full, (int)p.gx,
-                                                         (int)T, (int)N, rs, C, V, F);
+                                                         (int)T, (int)N, rs, C, V, F, tinfo);
     } else {
       return hipErrorInvalidValue;  // planned for the forward modes only
     }
@@ -1186,7 +1454,7 @@ hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *
       const dim3 gr((unsigned)((N + kBwdReduceCols - 1) / kBwdReduceCols),
                     (unsigned)((T + 63) / 64));
       splitk_bwd_reduce_kernel<kMode><<<gr, 256, 0, s>>>(P, p.splits, (int)T, (int)N, rs,
-                                                          gscale, C, S, F);
+                                                          gscale, C, S, F, tinfo);
     } else {
       // A reduction that would occupy at most half the compute units with
       // 256-thread blocks runs 64-thread blocks: the partial loads of a few
@@ -1195,23 +1463,39 @@ hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *
       const int64_t units = T * (N / 8);
       const int rt = (units + 255) / 256 <= device_cus() / 2 ? 64 : 256;
       splitk_reduce_kernel<kMode><<<(unsigned)((units + rt - 1) / rt), rt, 0, s>>>(
-          P, p.splits, (int)T, (int)N, rs, C, V, F);
+          P, p.splits, (int)T, (int)N, rs, C, V, F, tinfo);
     }
   }
   return hipGetLastError();
 }
 
-// fp16(s_in .* x) in pair order, the A operand of G1.
+// fp16(s_in .* x 2^e_t) in pair order, the A operand of G1, and the
+// per-token range-guard record (see prep_kernel).
 hipError_t prepare_forward(int64_t n, const uint16_t *s_in, const uint16_t *x, int64_t T,
-                           uint16_t *xp, hipStream_t s) {
-  const int64_t units = T * (n / 16);
-  prep_kernel<<<(unsigned)((units + 255) / 256), 256, 0, s>>>(x, s_in, xp, (int)T, (int)n);
+                           uint16_t *xp, float *tinfo, const uint16_t *s_mid, int64_t r,
+                           hipStream_t s) {
+  // a row in registers: at most two units a thread, 256 to 1024 threads
+  const int64_t units = n / 16;
+  const dim3 g((unsigned)(T + 1));
+  if (units <= 256)
+    prep_kernel<1, 256><<<g, 256, 0, s>>>(x, s_in, xp, (int)T, (int)n, tinfo, s_mid, (int)r);
+  else if (units <= 512)
+    prep_kernel<2, 256><<<g, 256, 0, s>>>(x, s_in, xp, (int)T, (int)n, tinfo, s_mid, (int)r);
+  else if (units <= 1024)
+    prep_kernel<2, 512><<<g, 512, 0, s>>>(x, s_in, xp, (int)T, (int)n, tinfo, s_mid, (int)r);
+  else if (units <= 2048)
+    prep_kernel<2, 1024><<<g, 1024, 0, s>>>(x, s_in, xp, (int)T, (int)n, tinfo, s_mid, (int)r);
+  else
+    prep_kernel<0, 256><<<g, 256, 0, s>>>(x, s_in, xp, (int)T, (int)n, tinfo, s_mid, (int)r);
   return hipGetLastError();
 }
 
+size_t tinfo_bytes(int64_t T) { return align256((size_t)tinfo_floats(T) * 4); }
+
 struct FwdWs {
   uint16_t *xp, *Z;
-  float *P;  // split-K partials of G1 or G2 (one at a time)
+  float *tinfo;  // the per-token range-guard record
+  float *P;      // split-K partials of G1 or G2 (one at a time)
 };
 
 FwdWs forward_ws(void *ws, int64_t n, int64_t r, int64_t T) {
@@ -1221,6 +1505,8 @@ FwdWs forward_ws(void *ws, int64_t n, int64_t r, int64_t T) {
   base += align256((size_t)T * n * 2);
   w.Z = reinterpret_cast<uint16_t *>(base);
   base += align256((size_t)T * r * 2);
+  w.tinfo = reinterpret_cast<float *>(base);
+  base += tinfo_bytes(T);
   w.P = reinterpret_cast<float *>(base);
   return w;
 }
@@ -1277,7 +1563,7 @@ size_t gemm_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
   const size_t p2 = split_bytes(g2, T, m) > mixed_bytes(g2, T, m) ? split_bytes(g2, T, m)
                                                                    : mixed_bytes(g2, T, m);
   return align256((size_t)T * (size_t)n * 2) + align256((size_t)T * (size_t)r * 2) +
-         (p1 > p2 ? p1 : p2);
+         tinfo_bytes(T) + (p1 > p2 ? p1 : p2);
 }
 
 hipError_t launch_gemm(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
@@ -1290,20 +1576,21 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
       r * (n / 32) * 4 > 0x7fffffff)
     return hipErrorInvalidValue;
   const FwdWs w = forward_ws(ws, n, r, T);
-  hipError_t e = prepare_forward(n, s_in, x, T, w.xp, s);
+  hipError_t e = prepare_forward(n, s_in, x, T, w.xp, w.tinfo, s_mid, r, s);
   if (e != hipSuccess) return e;
   e = contraction<kMid>(w.xp, T, n, Bv, r, s_mid, w.Z, nullptr, nullptr, nullptr, s, nullptr,
-                        nullptr, w.P);
+                        nullptr, w.P, w.tinfo);
   if (e != hipSuccess) return e;
   return contraction<kOut>(w.Z, T, r, Bu, m, s_out, y, nullptr, nullptr, nullptr, s, nullptr,
-                           nullptr, w.P);
+                           nullptr, w.P, w.tinfo);
 }
 
 size_t train_saved_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
   (void)n;
-  // the pre-scale intermediate v = Bv (s_in .* x), fp16 in pair order, and
-  // the pre-scale output z = Bu (s_mid .* v), fp32
-  return align256((size_t)T * r * 2) + align256((size_t)T * m * 4);
+  // the pre-scale intermediate v = Bv (s_in .* x), fp16 in pair order at a
+  // per-token scale, the pre-scale output z = Bu (s_mid .* v), fp32, and the
+  // per-token range-guard record that gives v's scale
+  return align256((size_t)T * r * 2) + align256((size_t)T * m * 4) + tinfo_bytes(T);
 }
 
 size_t train_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
@@ -1322,14 +1609,18 @@ hipError_t launch_forward_train(int64_t m, int64_t n, int64_t r, const uint32_t 
   const FwdWs w = forward_ws(ws, n, r, T);
   uint16_t *v = static_cast<uint16_t *>(saved);
   float *z = reinterpret_cast<float *>(static_cast<uint8_t *>(saved) + align256((size_t)T * r * 2));
-  hipError_t e = prepare_forward(n, s_in, x, T, w.xp, s);
+  float *tinfo = reinterpret_cast<float *>(static_cast<uint8_t *>(saved) +
+                                           align256((size_t)T * r * 2) +
+                                           align256((size_t)T * m * 4));
+  hipError_t e = prepare_forward(n, s_in, x, T, w.xp, tinfo, s_mid, r, s);
   if (e != hipSuccess) return e;
-  // the same G1 as the inference forward, which also keeps fp16(v)
+  // the same G1 as the inference forward, which also keeps fp16(v) at the
+  // token's scale
   e = contraction<kMidSave>(w.xp, T, n, Bv, r, s_mid, w.Z, v, nullptr, nullptr, s, nullptr,
-                            nullptr, w.P);
+                            nullptr, w.P, tinfo);
   if (e != hipSuccess) return e;
   return contraction<kOutSave>(w.Z, T, r, Bu, m, s_out, y, nullptr, nullptr, z, s, nullptr,
-                               nullptr, w.P);
+                               nullptr, w.P, tinfo);
 }
 
 hipError_t launch_backward(int64_t m, int64_t n, int64_t r, const uint32_t *BuT,
@@ -1345,6 +1636,9 @@ hipError_t launch_backward(int64_t m, int64_t n, int64_t r, const uint32_t *BuT,
   const uint16_t *v = static_cast<const uint16_t *>(saved);
   const float *z = reinterpret_cast<const float *>(static_cast<const uint8_t *>(saved) +
                                                    align256((size_t)T * r * 2));
+  const float *tinfo = reinterpret_cast<const float *>(
+      static_cast<const uint8_t *>(saved) + align256((size_t)T * r * 2) +
+      align256((size_t)T * m * 4));
   // per-token statistics of dy * s_out, and the largest |s_mid|
   bwd_rowstat_kernel<<<(unsigned)(T + 1), 256, 0, s>>>(dy, s_out, (int)T, (int)m, w.tstat, s_mid,
                                                        (int)r);
@@ -1360,7 +1654,7 @@ hipError_t launch_backward(int64_t m, int64_t n, int64_t r, const uint32_t *BuT,
   // operand; sums dt .* v.
   int tm = 0, ti = 0;
   e = contraction<kBwdMid>(w.A1, T, m, BuT, r, s_mid, w.Zb, nullptr, v, w.p_mid, s, &tm,
-                           w.gscale, w.P);
+                           w.gscale, w.P, tinfo);
   if (e != hipSuccess) return e;
   // du 2^(e - c) = Bv^T (s_mid .* dt 2^(e - c)): dx = s_in .* du; sums du .* x.
   e = contraction<kBwdIn>(w.Zb, T, r, BvT, n, s_in, dx, nullptr, x, w.p_in, s, &ti, w.gscale,

@@ -291,7 +291,8 @@ __device__ __forceinline__ void stage_body(
   //    batch row and for the tail of a ragged group.  A unit is 8 columns
   //    (and their partners 16 on) of one batch row.  With one row tile per
   //    workgroup every wave stages exactly the columns of its own groups
-  //    (and reads only what it wrote, so no barrier is needed); with
+  //    (and reads only what it wrote, the zero slot included, so no
+  //    barrier is needed); with
   //    several, the waves of different tiles share columns and the
   //    workgroup stages the slab once, then meets a barrier.  A wave with
   //    no unit in a pass issues no load (out-of-range loads still occupy the
@@ -299,7 +300,11 @@ __device__ __forceinline__ void stage_body(
   //    scratch slot instead of branching, so that no load is moved behind
   //    another unit's wait.
   uint8_t *xs = lds + kSlot;
-  if (tid < kSlot / 16) reinterpret_cast<uint4 *>(lds)[tid] = make_uint4(0u, 0u, 0u, 0u);
+  // Every wave writes the zero slot itself: with one tile per workgroup no
+  // barrier separates staging from the products, and a wave whose ragged
+  // group tail points at the slot must see zeros written in its own program
+  // order (the stores of other waves carry the same zeros).
+  if (lane < kSlot / 16) reinterpret_cast<uint4 *>(lds)[lane] = make_uint4(0u, 0u, 0u, 0u);
   {
     constexpr bool shared = kMulti;
     const int per_group = b * kGroupWords * 2;  // units of one group
