@@ -191,14 +191,17 @@ DECODE_TABLE = [("sq1024", 1), ("attn4096", 8), ("kv1024x4096", 1), ("mlp_up1433
                 ("mlp_down4096x14336", 4), ("mlp_down4096x14336", 16),
                 ("attn4096_r5120_2.5bpw", 1), ("attn4096_r5120_2.5bpw", 8)]
 
-# The paper's other budget (2.5 bits per weight): rank round(2.5 mn / (m + n)),
-# above min(m, n), so the second sign matrix is the larger one.
-EXTRA_SHAPES = {"attn4096_r5120_2.5bpw": (4096, 4096, 5120)}
+# The paper's other budget (2.5 bits per weight) at 4096x4096: its own rank
+# rule round(2.5 mn / (m + n)) (af1_paper_rank, 5120), above min(m, n), so
+# the second sign matrix is the larger one.
+def paper_25bpw_shape():
+    from paper_2609_06161_amd import af1
+    return (4096, 4096, af1.af1_paper_rank(4096, 4096, 2.5))
 
 
 def shape_of(name):
     from paper_2609_06161_amd import synth
-    return EXTRA_SHAPES[name] if name in EXTRA_SHAPES else synth.SHAPES[name]
+    return paper_25bpw_shape() if name == "attn4096_r5120_2.5bpw" else synth.SHAPES[name]
 
 
 STACK_LINEARS = [("q", 4096, 4096, 2016), ("k", 1024, 4096, 800), ("v", 1024, 4096, 800),
@@ -319,7 +322,7 @@ def bench_gemm(args, torch, stream):
         del xd, wd
     out["all3_tflops"] = total_flops / (total_ms * 1e-3) / 1e12
     # the 2.5-BPW setting at 4096^2 (context; not in the three-shape total)
-    m, n, r = EXTRA_SHAPES["attn4096_r5120_2.5bpw"]
+    m, n, r = paper_25bpw_shape()
     lin = synth.make_linear(56, m, n, r, T)
     L = DeviceLayer.from_host(lin)
     x = to_device(lin.x)

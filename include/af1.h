@@ -124,7 +124,11 @@ AF1_API af1_status af1_unpack(const uint32_t *words, int64_t rows, int64_t cols,
  *        workspace's first use, and every call that
  *        completes leaves the counters at zero again, so one workspace
  *        serves any sequence of calls, of any shapes, on one stream.  Calls
- *        that may overlap in time need distinct workspaces.
+ *        that may overlap in time need distinct workspaces.  Recovery: a
+ *        call that did not run to completion (a launch error reported by
+ *        a later call, a killed stream) may leave counters non-zero, after
+ *        which results are wrong; zero-fill the header again before reusing
+ *        such a workspace.
  * Arithmetic: s_in .* x in fp32 (exact), both sign products accumulated in
  * fp32, the rank-r intermediate kept in fp32, scales applied in fp32, y
  * rounded to bfloat16 (round to nearest even).  y must not overlap x, the
@@ -134,6 +138,7 @@ AF1_API size_t af1_gemv_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t
 AF1_API af1_status af1_linear_gemv(const af1_factorized_linear *L, const uint16_t *x,
                            int64_t b, uint16_t *y, void *ws, size_t ws_bytes,
                            void *stream);
+
 
 /*
  * af1_linear_gemv_multi -- decode forward of several layers that read the
@@ -290,10 +295,20 @@ AF1_API af1_status af1_linear_backward(const af1_factorized_linear *L, const uin
  * label eq:app_af1_memory).  Returns -1 for negative arguments. */
 AF1_API int64_t af1_storage_bits(int64_t m, int64_t n, int64_t r);
 
-/* Largest multiple of 32 rank whose storage bits do not exceed m*n (a
- * strict 1.0 effective-BPW budget for this layer alone, App. A.3).  Returns
- * 0 when no positive rank fits or an argument is not positive. */
-AF1_API int64_t af1_budget_rank(int64_t m, int64_t n);
+/* Largest rank r, a multiple of `multiple`, whose storage bits
+ * r*(m+n) + 16*(m+n+r) do not exceed floor(bpw * m * n): the layer at an
+ * effective budget of bpw bits per weight with its scales counted (App. A.3,
+ * labels eq:app_af1_memory and eq:app_af1_bpw); bpw = 1, multiple = 32 is
+ * the strict 1.0-BPW rank.  Returns 0 when no positive rank fits or an
+ * argument is out of range (m, n in 1..AF1_MAX_DIM, 0 < bpw <= 64,
+ * multiple >= 1). */
+AF1_API int64_t af1_budget_rank(int64_t m, int64_t n, double bpw, int64_t multiple);
+
+/* The paper's own budget-to-rank rule (App. A.1.3): round(bpw * m * n /
+ * (m + n)), counting the sign bits only (so a layer at this rank exceeds
+ * bpw once its scales are counted); 2.5 BPW at 4096 x 4096 gives 5120.
+ * Rounding half away from zero; 0 for arguments out of the range above. */
+AF1_API int64_t af1_paper_rank(int64_t m, int64_t n, double bpw);
 
 /* Static, NUL-terminated description of a status code. */
 AF1_API const char *af1_status_string(int32_t status);

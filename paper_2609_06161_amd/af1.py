@@ -75,8 +75,10 @@ def lib():
                                       SZ, P, P, P, P, I32, P, SZ, P]
     L.af1_storage_bits.argtypes = [I64, I64, I64]
     L.af1_storage_bits.restype = I64
-    L.af1_budget_rank.argtypes = [I64, I64]
+    L.af1_budget_rank.argtypes = [I64, I64, ctypes.c_double, I64]
     L.af1_budget_rank.restype = I64
+    L.af1_paper_rank.argtypes = [I64, I64, ctypes.c_double]
+    L.af1_paper_rank.restype = I64
     L.af1_status_string.argtypes = [I32]
     L.af1_status_string.restype = ctypes.c_char_p
     L.af1_version.restype = ctypes.c_char_p
@@ -229,5 +231,9 @@ def af1_storage_bits(m, n, r) -> int:
     return int(lib().af1_storage_bits(m, n, r))
 
 
-def af1_budget_rank(m, n) -> int:
-    return int(lib().af1_budget_rank(m, n))
+def af1_budget_rank(m, n, bpw=1.0, multiple=32) -> int:
+    return int(lib().af1_budget_rank(m, n, float(bpw), multiple))
+
+
+def af1_paper_rank(m, n, bpw) -> int:
+    return int(lib().af1_paper_rank(m, n, float(bpw)))

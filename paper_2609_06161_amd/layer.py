@@ -1,6 +1,8 @@
 """Device-resident factorized layer: the packed signs and fp16 scales held as
 torch CUDA tensors (plumbing only), plus the C descriptor that points at them.
 """
+import contextlib
+
 import numpy as np
 import torch
 
@@ -16,6 +18,18 @@ def to_device(a: np.ndarray, device="cuda") -> torch.Tensor:
     patterns travel as signed views of the same bits)."""
     a = np.ascontiguousarray(a)
     return torch.from_numpy(a.view(_VIEW[a.dtype])).to(device)
+
+
+def on_stream(stream):
+    """Context in which the helpers below allocate their outputs and
+    workspaces: the stream the kernels are launched on (torch's current one
+    when stream is None), so a zero-fill is ordered before the kernels and
+    the caching allocator does not hand the memory to other work while they
+    may still use it."""
+    if stream is None or isinstance(stream, int):
+        # an integer stream handle: the caller owns ordering and lifetimes
+        return contextlib.nullcontext()
+    return torch.cuda.stream(stream)
 
 
 def bf16_bits_to_f64(t: torch.Tensor) -> np.ndarray:
@@ -44,23 +58,25 @@ class DeviceLayer:
 
     def gemv(self, x: torch.Tensor, y: torch.Tensor = None, ws: torch.Tensor = None, stream=None):
         b = x.shape[0]
-        if y is None:
-            y = torch.empty((b, self.m), dtype=torch.int16, device=x.device)
-        need = af1.af1_gemv_workspace_bytes(self.m, self.n, self.r, b)
-        if ws is None:
-            # zero-filled: the decode path keeps arrival counters here
-            ws = torch.zeros(max(need, 256), dtype=torch.uint8, device=x.device)
-        af1.af1_linear_gemv(self.desc, x, b, y, ws, ws.numel(), stream)
+        with on_stream(stream):
+            if y is None:
+                y = torch.empty((b, self.m), dtype=torch.int16, device=x.device)
+            need = af1.af1_gemv_workspace_bytes(self.m, self.n, self.r, b)
+            if ws is None:
+                # zero-filled: the decode path keeps arrival counters here
+                ws = torch.zeros(max(need, 256), dtype=torch.uint8, device=x.device)
+            af1.af1_linear_gemv(self.desc, x, b, y, ws, ws.numel(), stream)
         return y
 
     def gemm(self, x: torch.Tensor, y: torch.Tensor = None, ws: torch.Tensor = None, stream=None):
         T = x.shape[0]
-        if y is None:
-            y = torch.empty((T, self.m), dtype=torch.int16, device=x.device)
-        need = af1.af1_gemm_workspace_bytes(self.m, self.n, self.r, T)
-        if ws is None:
-            ws = torch.empty(max(need, 256), dtype=torch.uint8, device=x.device)
-        af1.af1_linear_gemm(self.desc, x, T, y, ws, ws.numel(), stream)
+        with on_stream(stream):
+            if y is None:
+                y = torch.empty((T, self.m), dtype=torch.int16, device=x.device)
+            need = af1.af1_gemm_workspace_bytes(self.m, self.n, self.r, T)
+            if ws is None:
+                ws = torch.empty(max(need, 256), dtype=torch.uint8, device=x.device)
+            af1.af1_linear_gemm(self.desc, x, T, y, ws, ws.numel(), stream)
         return y
 
     # -- scale-only reconstruction: signs frozen, scales trained -----------
@@ -77,16 +93,17 @@ class DeviceLayer:
 
     def forward_train(self, x, y=None, saved=None, ws=None, stream=None):
         T = x.shape[0]
-        if y is None:
-            y = torch.empty((T, self.m), dtype=torch.int16, device=x.device)
-        if saved is None:
-            saved = torch.empty(af1.af1_train_saved_bytes(self.m, self.n, self.r, T),
-                                dtype=torch.uint8, device=x.device)
-        if ws is None:
-            ws = torch.empty(af1.af1_train_workspace_bytes(self.m, self.n, self.r, T),
-                             dtype=torch.uint8, device=x.device)
-        af1.af1_linear_forward_train(self.desc, x, T, y, saved, saved.numel(), ws, ws.numel(),
-                                     stream)
+        with on_stream(stream):
+            if y is None:
+                y = torch.empty((T, self.m), dtype=torch.int16, device=x.device)
+            if saved is None:
+                saved = torch.empty(af1.af1_train_saved_bytes(self.m, self.n, self.r, T),
+                                    dtype=torch.uint8, device=x.device)
+            if ws is None:
+                ws = torch.empty(af1.af1_train_workspace_bytes(self.m, self.n, self.r, T),
+                                 dtype=torch.uint8, device=x.device)
+            af1.af1_linear_forward_train(self.desc, x, T, y, saved, saved.numel(), ws,
+                                         ws.numel(), stream)
         return y, saved
 
     def backward(self, x, dy, saved, dx=None, grads=None, accumulate=False, ws=None,
@@ -94,29 +111,31 @@ class DeviceLayer:
         """dx ([T, n] bf16 patterns, or None) and the fp32 scale gradients
         (ds_out, ds_mid, ds_in)."""
         T = x.shape[0]
-        BuT, BvT = self.transposed(stream)
-        if dx is None and want_dx:
-            dx = torch.empty((T, self.n), dtype=torch.int16, device=x.device)
-        if grads is None:
-            grads = tuple(torch.empty(k, dtype=torch.float32, device=x.device)
-                          for k in (self.m, self.r, self.n))
-        if ws is None:
-            ws = torch.empty(af1.af1_train_workspace_bytes(self.m, self.n, self.r, T),
-                             dtype=torch.uint8, device=x.device)
-        af1.af1_linear_backward(self.desc, BuT, BvT, x, dy, T, saved, saved.numel(), dx,
-                                grads[0], grads[1], grads[2], int(bool(accumulate)), ws,
-                                ws.numel(), stream)
+        with on_stream(stream):
+            BuT, BvT = self.transposed(stream)
+            if dx is None and want_dx:
+                dx = torch.empty((T, self.n), dtype=torch.int16, device=x.device)
+            if grads is None:
+                grads = tuple(torch.empty(k, dtype=torch.float32, device=x.device)
+                              for k in (self.m, self.r, self.n))
+            if ws is None:
+                ws = torch.empty(af1.af1_train_workspace_bytes(self.m, self.n, self.r, T),
+                                 dtype=torch.uint8, device=x.device)
+            af1.af1_linear_backward(self.desc, BuT, BvT, x, dy, T, saved, saved.numel(), dx,
+                                    grads[0], grads[1], grads[2], int(bool(accumulate)), ws,
+                                    ws.numel(), stream)
         return dx, grads
 
 
 def gemv_multi(layers, x: torch.Tensor, ys=None, ws: torch.Tensor = None, stream=None):
     """One decode step of several layers that read the same x (same n)."""
     b = x.shape[0]
-    if ys is None:
-        ys = [torch.empty((b, L.m), dtype=torch.int16, device=x.device) for L in layers]
-    descs = [L.desc for L in layers]
-    need = af1.af1_gemv_multi_workspace_bytes(descs, b)
-    if ws is None:
-        ws = torch.zeros(max(need, 256), dtype=torch.uint8, device=x.device)
-    af1.af1_linear_gemv_multi(descs, x, b, ys, ws, ws.numel(), stream)
+    with on_stream(stream):
+        if ys is None:
+            ys = [torch.empty((b, L.m), dtype=torch.int16, device=x.device) for L in layers]
+        descs = [L.desc for L in layers]
+        need = af1.af1_gemv_multi_workspace_bytes(descs, b)
+        if ws is None:
+            ws = torch.zeros(max(need, 256), dtype=torch.uint8, device=x.device)
+        af1.af1_linear_gemv_multi(descs, x, b, ys, ws, ws.numel(), stream)
     return ys

@@ -63,6 +63,36 @@ def test_budget_rank_matches_oracle(oracle):
     assert af1.af1_budget_rank(32, 32) == 0      # scales alone exceed the budget
 
 
+def test_budget_rank_other_budgets(oracle):
+    """Any budget: the rank's storage (oracle.storage_bits, pinned to the
+    paper's count) fits floor(bpw m n) bits and one more multiple does not."""
+    rng = np.random.default_rng(2)
+    for _ in range(300):
+        m, n = (int(v) for v in rng.integers(32, 40000, size=2))
+        bpw = float(rng.choice([0.55, 1.0, 1.5, 2.0, 2.5, 3.3]))
+        mult = int(rng.choice([1, 16, 32, 64]))
+        r = af1.af1_budget_rank(m, n, bpw, mult)
+        budget = int(np.floor(bpw * m * n))
+        assert r % mult == 0
+        if r > 0:
+            assert oracle.storage_bits(m, n, r) <= budget, (m, n, bpw, mult)
+        assert oracle.storage_bits(m, n, r + mult) > budget, (m, n, bpw, mult)
+    assert af1.af1_budget_rank(4096, 4096, 2.5, 32) == 5088   # scales counted
+    assert af1.af1_budget_rank(4096, 4096, 0.0, 32) == 0
+    assert af1.af1_budget_rank(4096, 4096, 1.0, 0) == 0
+
+
+def test_paper_rank_matches_oracle(oracle):
+    """The paper's sign-bits-only rank rule (App. A.1.3) through the ABI."""
+    assert af1.af1_paper_rank(4096, 4096, 2.5) == 5120
+    rng = np.random.default_rng(3)
+    for _ in range(200):
+        m, n = (int(v) for v in rng.integers(1, 40000, size=2))
+        bpw = float(rng.uniform(0.1, 4.0))
+        assert af1.af1_paper_rank(m, n, bpw) == oracle.paper_rank(bpw, m, n), (m, n, bpw)
+    assert af1.af1_paper_rank(0, 5, 1.0) == 0
+
+
 # --------------------------------------------------------------------------
 # argument validation (no launch happens on any of these paths)
 # --------------------------------------------------------------------------
