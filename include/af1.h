@@ -138,6 +138,27 @@ AF1_API size_t af1_gemv_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t
 AF1_API af1_status af1_linear_gemv(const af1_factorized_linear *L, const uint16_t *x,
                            int64_t b, uint16_t *y, void *ws, size_t ws_bytes,
                            void *stream);
+/*
+ * af1_linear_gemv_noalloc -- af1_linear_gemv for callers that cannot
+ * allocate device memory or hand over a workspace: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * kernels, arithmetic and results as af1_linear_gemv (bit for bit); the
+ * workspace is a library-owned device array of AF1_GEMV_SCRATCH_BYTES bytes
+ * that each GPU the library runs on holds from load until the process
+ * ends.  The call allocates nothing and calls no allocating routine.
+ *   x, b, y : as af1_linear_gemv (the caller still owns x and y).
+ * Errors: as af1_linear_gemv; AF1_ERR_WORKSPACE when the shape and batch
+ * need more than AF1_GEMV_SCRATCH_BYTES (af1_gemv_workspace_bytes tells);
+ * AF1_ERR_HIP when the device array's address cannot be obtained.
+ * Concurrency: every call on one GPU uses that GPU's one array, so calls
+ * that overlap in time on one GPU (other streams, other threads) race and
+ * give wrong results; serialise them.  The array keeps the last call's
+ * contents; each call first clears the arrival counters it uses (with a
+ * kernel, no memset), so a previous call cannot corrupt it.
+ */
+#define AF1_GEMV_SCRATCH_BYTES (4 << 20)
+AF1_API af1_status af1_linear_gemv_noalloc(const af1_factorized_linear *L, const uint16_t *x,
+                                           int64_t b, uint16_t *y, void *stream);
 
 
 /*

@@ -24,6 +24,7 @@ AF1_ERR_DTYPE = 8
 AF1_SRC_F32, AF1_SRC_BF16, AF1_SRC_F16, AF1_SRC_I8 = 0, 1, 2, 3
 AF1_GEMV_MAX_BATCH = 16
 AF1_GEMV_MULTI_MAX = 4
+AF1_GEMV_SCRATCH_BYTES = 4 << 20
 AF1_MAX_DIM = 1 << 20
 
 _lib = None
@@ -79,10 +80,12 @@ def lib():
     L.af1_budget_rank.restype = I64
     L.af1_paper_rank.argtypes = [I64, I64, ctypes.c_double]
     L.af1_paper_rank.restype = I64
+    L.af1_linear_gemv_noalloc.argtypes = [ctypes.POINTER(af1_factorized_linear), P, I64, P, P]
     L.af1_status_string.argtypes = [I32]
     L.af1_status_string.restype = ctypes.c_char_p
     L.af1_version.restype = ctypes.c_char_p
-    for fn in ("af1_pack", "af1_unpack", "af1_linear_gemv", "af1_linear_gemv_multi",
+    for fn in ("af1_pack", "af1_unpack", "af1_linear_gemv", "af1_linear_gemv_noalloc",
+               "af1_linear_gemv_multi",
                "af1_linear_gemm", "af1_pack_transpose", "af1_linear_forward_train",
                "af1_linear_backward"):
         getattr(L, fn).restype = I32
@@ -150,6 +153,14 @@ def af1_linear_gemv(layer, x, b: int, y, ws, ws_bytes: int, stream=None, check=T
     st = lib().af1_linear_gemv(ref, _addr(x), b, _addr(y), _addr(ws), ws_bytes, _stream(stream))
     if check:
         _check(st, "af1_linear_gemv")
+    return st
+
+
+def af1_linear_gemv_noalloc(layer, x, b: int, y, stream=None, check=True) -> int:
+    ref = ctypes.byref(layer) if layer is not None else None
+    st = lib().af1_linear_gemv_noalloc(ref, _addr(x), b, _addr(y), _stream(stream))
+    if check:
+        _check(st, "af1_linear_gemv_noalloc")
     return st
 
 

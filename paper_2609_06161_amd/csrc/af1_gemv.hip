@@ -962,6 +962,32 @@ hipError_t launch_gemv_multi(int count, const int64_t *m, const int64_t *r, int6
   return launch_segs<false, true>(s2, L.p2, (int)b, wpr2, tparts, s);
 }
 
+namespace {
+__global__ void zero_words_kernel(uint32_t *__restrict__ p, int count) {
+  const int i = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+  if (i < count) p[i] = 0u;
+}
+}  // namespace
+
+hipError_t launch_gemv_clear_counters(int64_t m, int64_t n, int64_t r, int64_t b, void *ws,
+                                      hipStream_t s) {
+  const WsLayout L = ws_layout(m, n, r, b, device_cus());
+  uint8_t *base = static_cast<uint8_t *>(ws);
+  const StagePlan *plans[2] = {&L.p1, &L.p2};
+  const size_t offs[2] = {L.cnt1, L.cnt2};
+  const int64_t rows[2] = {r, m};
+  for (int k = 0; k < 2; ++k) {
+    if (plans[k]->mode != kModeLastSlab) continue;
+    const int64_t rows_wg = (int64_t)kTileRows << plans[k]->rt_log2;
+    const int groups = (int)((rows[k] + rows_wg - 1) / rows_wg);
+    zero_words_kernel<<<(unsigned)((groups + 255) / 256), 256, 0, s>>>(
+        reinterpret_cast<uint32_t *>(base + offs[k]), groups);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 hipError_t launch_gemv(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
                        const uint32_t *Bv, const uint16_t *s_out,
                        const uint16_t *s_mid, const uint16_t *s_in,

@@ -29,6 +29,11 @@ hipError_t launch_gemv(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
                        const uint16_t *x, int64_t b, uint16_t *y, void *ws,
                        hipStream_t s);
 
+// Zero the arrival counters that launch_gemv uses for this shape and batch
+// (none when no stage splits its columns); a fill kernel, no memset node.
+hipError_t launch_gemv_clear_counters(int64_t m, int64_t n, int64_t r, int64_t b, void *ws,
+                                      hipStream_t s);
+
 // Several layers that share n (count <= 4): two launches for all of them
 // when the plan allows, else one call per layer on the same workspace.
 size_t gemv_multi_workspace_bytes(const int64_t *m, const int64_t *r, int count, int64_t n,
