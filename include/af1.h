@@ -62,7 +62,8 @@ typedef enum af1_status {
     AF1_ERR_WORKSPACE = 5,   /* workspace missing or smaller than the query returns */
     AF1_ERR_ALIAS = 6,       /* an output buffer overlaps an input or the workspace */
     AF1_ERR_HIP = 7,         /* the HIP runtime rejected a launch */
-    AF1_ERR_DTYPE = 8        /* unknown source element type */
+    AF1_ERR_DTYPE = 8,       /* unknown source element type */
+    AF1_ERR_PLAN = 9         /* a stream plan that this library did not build */
 } af1_status;
 
 /* Element type of the dense matrix handed to af1_pack. */
@@ -189,6 +190,62 @@ AF1_API size_t af1_gemv_multi_workspace_bytes(const af1_factorized_linear *Ls, i
 AF1_API af1_status af1_linear_gemv_multi(const af1_factorized_linear *Ls, int32_t count,
                                          const uint16_t *x, int64_t b, uint16_t *const *ys,
                                          void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Layer stream -- the decode forward of a sequence of factorized layers in
+ * one persistent launch (the decode setting of Sec. 5.4: batch 1, one
+ * decoder step through every linear of the model; heterogeneous ranks as in
+ * App. A.3, label eq:app_af1_bpw).  Each item computes what
+ * af1_linear_gemv computes for its layer (same arithmetic); items run in
+ * order, and an item with `wait` set starts only after every earlier item
+ * of the call has written its output, so it may read those outputs (x of a
+ * later item may be y of an earlier one).  Items without `wait` may run
+ * concurrently with the item group before them: q, k and v, or gate and
+ * up, are one group.  The launch replaces a kernel boundary per product by
+ * a grid-wide barrier between phases.
+ *
+ * Use: af1_stream_workspace_bytes for the workspace size (zero-fill it
+ * before its first use, like the GEMV workspace: it holds arrival words
+ * and counters that every completed call leaves consistent);
+ * af1_stream_plan_bytes and af1_stream_plan to build the plan on the host,
+ * bound to the items' buffers and to that workspace; copy the plan's bytes
+ * to device memory; then af1_linear_stream once per decode step.  Rebuild
+ * the plan when any buffer changes.
+ *
+ * af1_stream_item fields:
+ *   L    : the layer (device arrays as for af1_linear_gemv).
+ *   x    : device, [b, L.n] bfloat16.       y : device, [b, L.m] bfloat16.
+ *   wait : non-zero to start after all earlier items have finished.
+ *
+ * af1_stream_plan errors: AF1_ERR_NULL (items, plan, ws or an item's
+ * pointer), AF1_ERR_SHAPE (count outside 1..AF1_STREAM_MAX_ITEMS or a bad
+ * layer), AF1_ERR_BATCH (b outside 1..AF1_GEMV_MAX_BATCH), AF1_ERR_ALIGN,
+ * AF1_ERR_WORKSPACE (ws or plan too small), AF1_ERR_ALIAS (an output
+ * overlaps any layer's arrays, another output, the workspace, or the input
+ * of an item that does not wait for it).
+ * af1_linear_stream: `plan` is the host plan, `plan_dev` a device copy of
+ * its bytes (16-byte aligned).  AF1_ERR_PLAN when the host plan is not a
+ * plan of this library, AF1_ERR_HIP when the launch fails or the device
+ * cannot hold every workgroup at once.  If a barrier ever timed out (a
+ * workgroup that never arrived; only a device fault causes it) the kernel
+ * ends early and leaves word 1 of the workspace non-zero; outputs are then
+ * invalid and the workspace header must be zero-filled again.  Calls on
+ * one workspace must not overlap in time.
+ */
+#define AF1_STREAM_MAX_ITEMS 4096
+typedef struct af1_stream_item {
+    af1_factorized_linear L;
+    const uint16_t *x;
+    uint16_t *y;
+    int32_t wait;
+    int32_t reserved;   /* set to 0 */
+} af1_stream_item;
+
+AF1_API size_t af1_stream_workspace_bytes(const af1_stream_item *items, int32_t count, int64_t b);
+AF1_API size_t af1_stream_plan_bytes(const af1_stream_item *items, int32_t count, int64_t b);
+AF1_API af1_status af1_stream_plan(const af1_stream_item *items, int32_t count, int64_t b,
+                                   void *ws, size_t ws_bytes, void *plan, size_t plan_bytes);
+AF1_API af1_status af1_linear_stream(const void *plan, const void *plan_dev, void *stream);
 
 /*
  * af1_linear_gemm -- prefill-regime forward for T tokens on the matrix cores.

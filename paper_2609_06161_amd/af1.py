@@ -20,12 +20,15 @@ AF1_ERR_WORKSPACE = 5
 AF1_ERR_ALIAS = 6
 AF1_ERR_HIP = 7
 AF1_ERR_DTYPE = 8
+AF1_ERR_PLAN = 9
 
 AF1_SRC_F32, AF1_SRC_BF16, AF1_SRC_F16, AF1_SRC_I8 = 0, 1, 2, 3
 AF1_GEMV_MAX_BATCH = 16
 AF1_GEMV_MULTI_MAX = 4
 AF1_GEMV_SCRATCH_BYTES = 4 << 20
 AF1_MAX_DIM = 1 << 20
+
+AF1_STREAM_MAX_ITEMS = 4096
 
 _lib = None
 
@@ -41,6 +44,11 @@ class af1_factorized_linear(ctypes.Structure):
                 ("Bu", ctypes.c_void_p), ("Bv", ctypes.c_void_p),
                 ("s_out", ctypes.c_void_p), ("s_mid", ctypes.c_void_p),
                 ("s_in", ctypes.c_void_p)]
+
+
+class af1_stream_item(ctypes.Structure):
+    _fields_ = [("L", af1_factorized_linear), ("x", ctypes.c_void_p), ("y", ctypes.c_void_p),
+                ("wait", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
 def lib():
@@ -74,6 +82,13 @@ def lib():
                                            SZ, P, SZ, P]
     L.af1_linear_backward.argtypes = [ctypes.POINTER(af1_factorized_linear), P, P, P, P, I64, P,
                                       SZ, P, P, P, P, I32, P, SZ, P]
+    SI = ctypes.POINTER(af1_stream_item)
+    L.af1_stream_workspace_bytes.argtypes = [SI, I32, I64]
+    L.af1_stream_workspace_bytes.restype = SZ
+    L.af1_stream_plan_bytes.argtypes = [SI, I32, I64]
+    L.af1_stream_plan_bytes.restype = SZ
+    L.af1_stream_plan.argtypes = [SI, I32, I64, P, SZ, P, SZ]
+    L.af1_linear_stream.argtypes = [P, P, P]
     L.af1_storage_bits.argtypes = [I64, I64, I64]
     L.af1_storage_bits.restype = I64
     L.af1_budget_rank.argtypes = [I64, I64, ctypes.c_double, I64]
@@ -87,7 +102,7 @@ def lib():
     for fn in ("af1_pack", "af1_unpack", "af1_linear_gemv", "af1_linear_gemv_noalloc",
                "af1_linear_gemv_multi",
                "af1_linear_gemm", "af1_pack_transpose", "af1_linear_forward_train",
-               "af1_linear_backward"):
+               "af1_linear_backward", "af1_stream_plan", "af1_linear_stream"):
         getattr(L, fn).restype = I32
     _lib = L
     return L
@@ -235,6 +250,44 @@ def af1_linear_backward(layer, BuT, BvT, x, dy, T: int, saved, saved_bytes: int,
                                    ws_bytes, _stream(stream))
     if check:
         _check(st, "af1_linear_backward")
+    return st
+
+
+def stream_items(entries):
+    """A ctypes array of af1_stream_item from (layer descriptor, x, y, wait)
+    tuples (x and y tensors or addresses)."""
+    arr = (af1_stream_item * len(entries))()
+    for i, (desc, x, y, wait) in enumerate(entries):
+        arr[i] = af1_stream_item(desc, _addr(x), _addr(y), int(bool(wait)), 0)
+    return arr
+
+
+def af1_stream_workspace_bytes(items, b) -> int:
+    return int(lib().af1_stream_workspace_bytes(items, len(items), b))
+
+
+def af1_stream_plan_bytes(items, b) -> int:
+    return int(lib().af1_stream_plan_bytes(items, len(items), b))
+
+
+def af1_stream_plan(items, b: int, ws, ws_bytes: int, plan, plan_bytes: int, count=None,
+                    check=True) -> int:
+    """plan: a host buffer (an int address, or a numpy uint8 array)."""
+    addr = plan if isinstance(plan, int) or plan is None else plan.ctypes.data
+    n = len(items) if count is None else count
+    st = lib().af1_stream_plan(items, n, b, _addr(ws), ws_bytes, addr, plan_bytes)
+    if check:
+        _check(st, "af1_stream_plan")
+    return st
+
+
+def af1_linear_stream(plan, plan_dev, stream=None, check=True) -> int:
+    """plan: the host plan (numpy uint8 array or address); plan_dev: its
+    device copy."""
+    addr = plan if isinstance(plan, int) or plan is None else plan.ctypes.data
+    st = lib().af1_linear_stream(addr, _addr(plan_dev), _stream(stream))
+    if check:
+        _check(st, "af1_linear_stream")
     return st
 
 

@@ -7,6 +7,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "af1.h"
 #include "af1_check.h"
 #include "af1_internal.h"
@@ -118,6 +120,100 @@ af1_status af1_linear_gemv_multi(const af1_factorized_linear *Ls, int32_t count,
   return hip_status(af1::launch_gemv_multi(count, m, r, Ls[0].n, Bu, Bv, so, sm, si, x, b, ys, ws,
                                            as_stream(stream)));
 }
+
+}  // extern "C"
+
+namespace {
+
+// Arguments of a layer stream, checked before any plan is made.
+af1_status check_stream(const af1_stream_item *items, int32_t count, int64_t b) {
+  if (!items) return AF1_ERR_NULL;
+  if (count < 1 || count > AF1_STREAM_MAX_ITEMS) return AF1_ERR_SHAPE;
+  if (b < 1 || b > AF1_GEMV_MAX_BATCH) return AF1_ERR_BATCH;
+  for (int i = 0; i < count; ++i) {
+    const af1_status st =
+        check_forward(&items[i].L, items[i].x, b, AF1_GEMV_MAX_BATCH, items[i].y, nullptr, 0, 0);
+    if (st != AF1_OK) return st;
+  }
+  // outputs against every layer's arrays, each other, and the inputs of
+  // items that run before them or in their group
+  std::vector<int> group_start(count);
+  for (int i = 0; i < count; ++i)
+    group_start[i] = (i == 0 || items[i].wait) ? i : group_start[i - 1];
+  for (int i = 0; i < count; ++i) {
+    const af1_factorized_linear &Li = items[i].L;
+    const Span yi = span(items[i].y, (uint64_t)b * Li.m * 2);
+    for (int j = 0; j < count; ++j) {
+      const af1_factorized_linear &Lj = items[j].L;
+      const Span arrays[] = {span(Lj.Bu, (uint64_t)Lj.m * Lj.r / 8),
+                             span(Lj.Bv, (uint64_t)Lj.r * Lj.n / 8),
+                             span(Lj.s_out, (uint64_t)Lj.m * 2), span(Lj.s_mid, (uint64_t)Lj.r * 2),
+                             span(Lj.s_in, (uint64_t)Lj.n * 2)};
+      for (const Span &a : arrays)
+        if (overlap(yi, a)) return AF1_ERR_ALIAS;
+      if (j != i && overlap(yi, span(items[j].y, (uint64_t)b * Lj.m * 2))) return AF1_ERR_ALIAS;
+      // item j may read y_i only from a later group that waits (a group
+      // that does not wait shares a phase with the group before it)
+      const bool ordered = j > i && group_start[j] > i && items[group_start[j]].wait &&
+                           group_start[group_start[j]] == group_start[j];
+      if (!ordered && overlap(yi, span(items[j].x, (uint64_t)b * Lj.n * 2))) return AF1_ERR_ALIAS;
+    }
+  }
+  return AF1_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t af1_stream_workspace_bytes(const af1_stream_item *items, int32_t count, int64_t b) {
+  if (check_stream(items, count, b) != AF1_OK) return 0;
+  size_t plan = 0, ws = 0;
+  af1::stream_plan_impl(items, count, b, nullptr, nullptr, &plan, &ws);
+  return ws;
+}
+
+size_t af1_stream_plan_bytes(const af1_stream_item *items, int32_t count, int64_t b) {
+  if (check_stream(items, count, b) != AF1_OK) return 0;
+  size_t plan = 0, ws = 0;
+  af1::stream_plan_impl(items, count, b, nullptr, nullptr, &plan, &ws);
+  return plan;
+}
+
+af1_status af1_stream_plan(const af1_stream_item *items, int32_t count, int64_t b, void *ws,
+                           size_t ws_bytes, void *plan, size_t plan_bytes) {
+  const af1_status st = check_stream(items, count, b);
+  if (st != AF1_OK) return st;
+  if (!ws || !plan) return AF1_ERR_NULL;
+  if (!aligned16(ws) || !aligned16(plan)) return AF1_ERR_ALIGN;
+  size_t need_plan = 0, need_ws = 0;
+  af1::stream_plan_impl(items, count, b, nullptr, nullptr, &need_plan, &need_ws);
+  if (ws_bytes < need_ws || plan_bytes < need_plan) return AF1_ERR_WORKSPACE;
+  const Span sws = span(ws, need_ws);
+  for (int i = 0; i < count; ++i) {
+    const af1_factorized_linear &L = items[i].L;
+    const Span arrays[] = {span(items[i].x, (uint64_t)b * L.n * 2),
+                           span(items[i].y, (uint64_t)b * L.m * 2),
+                           span(L.Bu, (uint64_t)L.m * L.r / 8), span(L.Bv, (uint64_t)L.r * L.n / 8),
+                           span(L.s_out, (uint64_t)L.m * 2), span(L.s_mid, (uint64_t)L.r * 2),
+                           span(L.s_in, (uint64_t)L.n * 2)};
+    for (const Span &a : arrays)
+      if (overlap(sws, a)) return AF1_ERR_ALIAS;
+  }
+  af1::stream_plan_impl(items, count, b, ws, plan, &need_plan, &need_ws);
+  return AF1_OK;
+}
+
+af1_status af1_linear_stream(const void *plan, const void *plan_dev, void *stream) {
+  if (!plan || !plan_dev) return AF1_ERR_NULL;
+  if (!aligned16(plan_dev)) return AF1_ERR_ALIGN;
+  if (af1::stream_plan_check(plan, (size_t)1 << 40) != 0) return AF1_ERR_PLAN;
+  return hip_status(af1::launch_stream(plan_dev, plan, as_stream(stream)));
+}
+
+}  // extern "C"
+
+extern "C" {
 
 size_t af1_gemm_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
   if (!dim_ok(m) || !dim_ok(n) || !dim_ok(r) || T < 1 || T > AF1_GEMM_MAX_TOKENS) return 0;
@@ -294,6 +390,7 @@ const char *af1_status_string(int32_t status) {
     case AF1_ERR_ALIAS: return "an output overlaps an input or the workspace";
     case AF1_ERR_HIP: return "the HIP runtime rejected a launch";
     case AF1_ERR_DTYPE: return "unknown source element type";
+    case AF1_ERR_PLAN: return "not a layer-stream plan of this library";
     default: return "unknown status";
   }
 }

@@ -40,7 +40,9 @@
 // a row group to finish (atomic counter) adds the partials in slab order,
 // so the result is deterministic.
 #include <atomic>
+#include <cstring>
 #include <utility>
+#include <vector>
 
 #include "af1_device.h"
 #include "af1_internal.h"
@@ -95,6 +97,10 @@ __device__ __forceinline__ void store_device(float *p, float v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+__device__ __forceinline__ void store_device_u16(uint16_t *p, uint16_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Calls f(std::integral_constant<int, I>) for I = 0 .. N-1, fully unrolled,
 // so that register arrays indexed by I stay in registers.
 template <typename F, int... I>
@@ -126,7 +132,7 @@ struct UnitRaw {
 // Raw data of one staging unit: columns c0 .. c0+7 and c0+16 .. c0+23 of one
 // batch row (x and s_in for the first stage, fp32 t for the second).  `off`
 // is the element offset of column c0 in the input, kOob for no unit.
-template <bool kInX>
+template <bool kInX, int kAux>
 __device__ __forceinline__ UnitRaw load_unit(__amdgpu_buffer_rsrc_t xres,
                                              __amdgpu_buffer_rsrc_t sres, int off, int col,
                                              int part_off = 0) {
@@ -134,16 +140,16 @@ __device__ __forceinline__ UnitRaw load_unit(__amdgpu_buffer_rsrc_t xres,
   if constexpr (kInX) {
     const int xo = off == kOob ? kOob : off * 2;
     const int so = off == kOob ? kOob : col * 2;
-    r.a = __builtin_amdgcn_raw_buffer_load_b128(xres, xo, 0, 0);
-    r.b = __builtin_amdgcn_raw_buffer_load_b128(xres, xo + 32, 0, 0);
+    r.a = __builtin_amdgcn_raw_buffer_load_b128(xres, xo, 0, kAux);
+    r.b = __builtin_amdgcn_raw_buffer_load_b128(xres, xo + 32, 0, kAux);
     r.c = __builtin_amdgcn_raw_buffer_load_b128(sres, so, 0, 0);
     r.d = __builtin_amdgcn_raw_buffer_load_b128(sres, so + 32, 0, 0);
   } else {
     const int to = off == kOob ? kOob : (off + part_off) * 4;
-    r.a = __builtin_amdgcn_raw_buffer_load_b128(xres, to, 0, 0);
-    r.b = __builtin_amdgcn_raw_buffer_load_b128(xres, to + 16, 0, 0);
-    r.c = __builtin_amdgcn_raw_buffer_load_b128(xres, to + 64, 0, 0);
-    r.d = __builtin_amdgcn_raw_buffer_load_b128(xres, to + 80, 0, 0);
+    r.a = __builtin_amdgcn_raw_buffer_load_b128(xres, to, 0, kAux);
+    r.b = __builtin_amdgcn_raw_buffer_load_b128(xres, to + 16, 0, kAux);
+    r.c = __builtin_amdgcn_raw_buffer_load_b128(xres, to + 64, 0, kAux);
+    r.d = __builtin_amdgcn_raw_buffer_load_b128(xres, to + 80, 0, kAux);
   }
   return r;
 }
@@ -214,7 +220,7 @@ struct Role {
   int my_groups;
 };
 
-__device__ __forceinline__ Role make_role(int wave, int group, int rt_log2, int wpr,
+__device__ __forceinline__ Role make_role(int wave, int group, int slab, int rt_log2, int wpr,
                                          int slab_words) {
   Role r;
   r.rt_log2 = rt_log2;
@@ -223,7 +229,7 @@ __device__ __forceinline__ Role make_role(int wave, int group, int rt_log2, int 
   r.cw = wave & (r.wpt - 1);
   r.tile = (group << rt_log2) + r.rt;
   r.row0 = r.tile * kTileRows;
-  r.w_begin = (int)blockIdx.y * slab_words;
+  r.w_begin = slab * slab_words;
   r.w_count = min(slab_words, wpr - r.w_begin);
   const int ngroups = (r.w_count + kGroupWords - 1) / kGroupWords;
   r.my_groups = ngroups > r.cw ? (ngroups - r.cw + r.wpt - 1) >> (3 - rt_log2) : 0;
@@ -242,25 +248,91 @@ __device__ __forceinline__ Role make_role(int wave, int group, int rt_log2, int 
 //
 // kMulti: several row tiles per workgroup (rt_log2 > 0, staging shared by
 // the workgroup); otherwise one tile, and rt_log2 is ignored.
-template <bool kInX, bool kOutY, bool kHiLoCols, bool kMulti>
+//
+// kCoherent: the input may have been written by other workgroups of the
+// same launch and the output may be read by them (the persistent stream
+// kernel): input loads and output stores then use device scope, coherent
+// across the XCDs' L2 caches.
+// Row scales of the outputs thread tid writes at the end of a stage:
+// outputs o = tid + kThreads * k, row (o mod rows_wg) of the workgroup's
+// rows, batch row o / rows_wg.
+__device__ __forceinline__ void load_row_scales(uint32_t (&rs)[kMaxOutPerThread],
+                                                const uint16_t *__restrict__ row_scale, int rows,
+                                                int group, int rt_log2, int b, int nk_out) {
+  const int rows_wg = 16 << rt_log2;
+  const int row_wg0 = group * rows_wg;
+  const int nout = rows_wg * b;
+  const __amdgpu_buffer_rsrc_t rres = buffer_rsrc(row_scale, (int64_t)rows * 2);
+#pragma unroll
+  for (int k = 0; k < kMaxOutPerThread; ++k) {
+    // the first load is unconditional (and so is its use below): a load
+    // whose only use sits in a branch is moved there, behind every wait
+    rs[k] = 0u;
+    if (k > 0 && k >= nk_out) break;
+    const int o = (int)threadIdx.x + kThreads * k;
+    const int orow = row_wg0 + (o & (rows_wg - 1));
+    rs[k] = __builtin_amdgcn_raw_buffer_load_b16(rres, o < nout ? orow * 2 : kOob, 0, 0);
+  }
+}
+
+// Sign words of one wave's groups (step 1 below) and the row scales of a
+// stage, loaded ahead of the rest by the stream kernel.
+struct SignRegs {
+  u32x2 wv[kMaxGroups];
+  uint32_t rs[kMaxOutPerThread];
+};
+
+__device__ __forceinline__ void stage_signs(SignRegs &sg, const uint32_t *__restrict__ M, int rows,
+                                            int wpr, int slab_words, int rt_log2, int group,
+                                            int slab, const uint16_t *__restrict__ row_scale,
+                                            int b) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const Role R = make_role(wave, group, slab, rt_log2, wpr, slab_words);
+  const int nout = (16 << rt_log2) * b;
+  load_row_scales(sg.rs, row_scale, rows, group, rt_log2, b,
+                  rt_log2 > 0 ? (nout + kThreads - 1) / kThreads : 1);
+  const int64_t left = (int64_t)(rows - R.row0) * wpr * 4;
+  const __amdgpu_buffer_rsrc_t mres = buffer_rsrc(M + (size_t)R.row0 * wpr, left);
+#pragma unroll
+  for (int i = 0; i < kMaxGroups; ++i) {
+    sg.wv[i] = u32x2{0u, 0u};
+    if (i < R.my_groups) {  // uniform
+      const int wl = (R.cw + R.wpt * i) * kGroupWords + 2 * (lane >> 4);
+      sg.wv[i] = __builtin_amdgcn_raw_buffer_load_b64(
+          mres, ((lane & 15) * wpr + R.w_begin + wl) * 4, 0, 0);
+    }
+  }
+}
+
+// kLoop: a wave may own more than kMaxGroups groups; they are taken in
+// chunks of kMaxGroups, the next chunk's sign words loading while the
+// current chunk's products run (the stream kernel, whose persistent
+// workgroups cover long rows without splitting them into slabs).
+template <bool kInX, bool kOutY, bool kHiLoCols, bool kMulti, bool kCoherent = false,
+          bool kLoop = false>
 __device__ __forceinline__ void stage_body(
     const uint32_t *__restrict__ M, const void *__restrict__ in,
     const uint16_t *__restrict__ s_in, const uint16_t *__restrict__ row_scale, int rows,
     int wpr, int slab_words, int b, int rt_log2_arg, int nslabs, int mode, int in_parts,
     void *__restrict__ out, float *__restrict__ part, uint32_t *__restrict__ cnt, int group,
-    int red_off = 0) {
+    int slab, int red_off = 0, const SignRegs *pre = nullptr) {
+  constexpr int kInAux = kCoherent ? kDeviceScope : 0;
   const int rt_log2 = kMulti ? rt_log2_arg : 0;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // scalar: wave-uniform
-  const Role R = make_role(wave, group, rt_log2, wpr, slab_words);
+  const Role R = make_role(wave, group, slab, rt_log2, wpr, slab_words);
   const size_t K = (size_t)wpr * 32;
   const int w_begin = R.w_begin;
   const int w_count = R.w_count;
 
-  // 1. Sign words of this wave's groups, issued before anything else, one
-  //    8-byte load per lane and group.  Lanes past the last row or the
+  // 1. Sign words of this wave's groups, one 8-byte load per lane and
+  //    group, issued right after the input loads of step 2 (which mostly hit
+  //    the caches; loads complete in order, so the conversion of the input
+  //    need not wait for the signs to arrive from HBM), or first when the
+  //    input is staged pass by pass.  Lanes past the last row or the
   //    slab's last word read data that never reaches a stored output: a
   //    ragged group's tail meets the zero slot on the B side, and rows past
   //    `rows` are not written.  Buffer range checking applies per dword, so
@@ -273,18 +345,27 @@ __device__ __forceinline__ void stage_body(
   const int rho = lane & 15;
   const int q = lane >> 4;
   u32x2 wv[kMaxGroups];
-  {
+  // sign words of groups c0 .. c0 + kMaxGroups - 1 into dst
+  auto load_chunk = [&](u32x2 (&dst)[kMaxGroups], int c0) {
     const int64_t left = (int64_t)(rows - R.row0) * wpr * 4;
     const __amdgpu_buffer_rsrc_t mres = buffer_rsrc(M + (size_t)R.row0 * wpr, left);
 #pragma unroll
     for (int i = 0; i < kMaxGroups; ++i) {
-      wv[i] = u32x2{0u, 0u};
-      if (i < R.my_groups) {  // uniform
-        const int wl = (R.cw + R.wpt * i) * kGroupWords + 2 * q;
-        wv[i] = __builtin_amdgcn_raw_buffer_load_b64(mres, (rho * wpr + w_begin + wl) * 4, 0, 0);
+      dst[i] = u32x2{0u, 0u};
+      if (c0 + i < R.my_groups) {  // uniform
+        const int wl = (R.cw + R.wpt * (c0 + i)) * kGroupWords + 2 * q;
+        dst[i] = __builtin_amdgcn_raw_buffer_load_b64(mres, (rho * wpr + w_begin + wl) * 4, 0, 0);
       }
     }
-  }
+  };
+  auto load_signs = [&]() {
+    if (pre) {  // loaded ahead (same addresses as load_chunk(wv, 0))
+#pragma unroll
+      for (int i = 0; i < kMaxGroups; ++i) wv[i] = pre->wv[i];
+      return;
+    }
+    load_chunk(wv, 0);
+  };
 
   // 2. Stage the input columns as bf16 hi/lo (p, p+16) pairs, one 144-byte
   //    slot per (batch row, word); slot 0 holds zeros for lanes with no
@@ -324,35 +405,38 @@ __device__ __forceinline__ void stage_body(
       // conversion costs a quarter of the per-lane instructions of whole
       // units.  Same values and layout as load_unit / store_unit.
       const int rem = lane >> 2, qq = lane & 3;
+      const int qgroups = kLoop ? R.my_groups : kMaxGroups;
+      for (int c0 = 0; c0 < qgroups; c0 += kMaxGroups) {
       u32x2 ra[kMaxGroups], rb[kMaxGroups], rc[kMaxGroups], rd[kMaxGroups];
       int dst_off[kMaxGroups];
 #pragma unroll
       for (int i = 0; i < kMaxGroups; ++i) {
-        if (i >= R.my_groups) break;  // uniform
-        const int wl = (R.cw + R.wpt * i) * kGroupWords + (rem >> 1);
+        if (c0 + i >= R.my_groups) break;  // uniform
+        const int wl = (R.cw + R.wpt * (c0 + i)) * kGroupWords + (rem >> 1);
         const int col = (w_begin + wl) * 32 + 8 * (rem & 1) + 2 * qq;
         const bool valid = wl < w_count;
         dst_off[i] = valid ? wl * kSlot + 32 * (rem & 1) + 8 * qq : -1;
         if constexpr (kInX) {
           const int xo = valid ? col * 2 : kOob;
-          ra[i][0] = __builtin_amdgcn_raw_buffer_load_b32(xres, xo, 0, 0);
-          rb[i][0] = __builtin_amdgcn_raw_buffer_load_b32(xres, xo + 32, 0, 0);
+          ra[i][0] = __builtin_amdgcn_raw_buffer_load_b32(xres, xo, 0, kInAux);
+          rb[i][0] = __builtin_amdgcn_raw_buffer_load_b32(xres, xo + 32, 0, kInAux);
           rc[i][0] = __builtin_amdgcn_raw_buffer_load_b32(sres, xo, 0, 0);
           rd[i][0] = __builtin_amdgcn_raw_buffer_load_b32(sres, xo + 32, 0, 0);
         } else {
           const int to = valid ? col * 4 : kOob;
-          ra[i] = __builtin_amdgcn_raw_buffer_load_b64(xres, to, 0, 0);
-          rb[i] = __builtin_amdgcn_raw_buffer_load_b64(xres, to + 64, 0, 0);
+          ra[i] = __builtin_amdgcn_raw_buffer_load_b64(xres, to, 0, kInAux);
+          rb[i] = __builtin_amdgcn_raw_buffer_load_b64(xres, to + 64, 0, kInAux);
           if (two_parts) {
             const int to2 = valid ? (col + part_elems) * 4 : kOob;
-            rc[i] = __builtin_amdgcn_raw_buffer_load_b64(xres, to2, 0, 0);
-            rd[i] = __builtin_amdgcn_raw_buffer_load_b64(xres, to2 + 64, 0, 0);
+            rc[i] = __builtin_amdgcn_raw_buffer_load_b64(xres, to2, 0, kInAux);
+            rd[i] = __builtin_amdgcn_raw_buffer_load_b64(xres, to2 + 64, 0, kInAux);
           }
         }
       }
+      if (c0 == 0) load_signs();
 #pragma unroll
       for (int i = 0; i < kMaxGroups; ++i) {
-        if (i >= R.my_groups) break;  // uniform
+        if (c0 + i >= R.my_groups) break;  // uniform
         float v[4];  // columns c, c+1, c+16, c+17
         if constexpr (kInX) {
           v[0] = bf16_to_f32(ra[i][0] & 0xffffu) * f16_to_f32((uint16_t)(rc[i][0] & 0xffffu));
@@ -380,13 +464,15 @@ __device__ __forceinline__ void stage_body(
         *reinterpret_cast<uint2 *>(dst) = make_uint2(h0, h1);
         *reinterpret_cast<uint2 *>(dst + 64) = make_uint2(l0, l1);
       }
+      }
     } else {
+      load_signs();
       // pass stride and this thread's first unit
       const int stride = shared ? 2 * kThreads : 128;
       const int first = shared ? tid : lane;
       const int wave_first = shared ? 64 * wave : 0;
 #pragma unroll
-      for (int it = 0; it < kStageIters; ++it) {
+      for (int it = 0; it < (kLoop ? 1 << 20 : kStageIters); ++it) {
         const int base = it * stride;
         if (base >= nunits) break;  // uniform
         int slot_off[2], half[2], off[2], col[2];
@@ -422,8 +508,9 @@ __device__ __forceinline__ void stage_body(
 #pragma unroll
         for (int k = 0; k < 2; ++k) {
           if (has[k]) {
-            raw[k] = load_unit<kInX>(xres, sres, off[k], col[k]);
-            if (two_parts) rawb[k] = load_unit<kInX>(xres, sres, off[k], col[k], part_elems);
+            raw[k] = load_unit<kInX, kInAux>(xres, sres, off[k], col[k]);
+            if (two_parts)
+              rawb[k] = load_unit<kInX, kInAux>(xres, sres, off[k], col[k], part_elems);
           }
         }
 #pragma unroll
@@ -448,17 +535,11 @@ __device__ __forceinline__ void stage_body(
   // uniform, <= kMaxOutPerThread (one tile: 16 b <= 256 outputs)
   const int nk_out = kMulti ? (nout + kThreads - 1) / kThreads : 1;
   uint32_t rscale_bits[kMaxOutPerThread];
-  {
-    const __amdgpu_buffer_rsrc_t rres = buffer_rsrc(row_scale, (int64_t)rows * 2);
+  if (pre) {
 #pragma unroll
-    for (int k = 0; k < kMaxOutPerThread; ++k) {
-      // the first load is unconditional (and so is its use below): a load
-      // whose only use sits in a branch is moved there, behind every wait
-      if (k > 0 && k >= nk_out) break;
-      const int o = tid + kThreads * k;
-      const int orow = row_wg0 + (o & (rows_wg - 1));
-      rscale_bits[k] = __builtin_amdgcn_raw_buffer_load_b16(rres, o < nout ? orow * 2 : kOob, 0, 0);
-    }
+    for (int k = 0; k < kMaxOutPerThread; ++k) rscale_bits[k] = pre->rs[k];
+  } else {
+    load_row_scales(rscale_bits, row_scale, rows, group, rt_log2, b, nk_out);
   }
   if constexpr (kMulti)
     __syncthreads();  // the staged slab is complete
@@ -483,46 +564,64 @@ __device__ __forceinline__ void stage_body(
   for (int t = 0; t < 4; ++t)
 #pragma unroll
     for (int hl = 0; hl < kChains; ++hl) acc[t][hl] = floatx4{0.f, 0.f, 0.f, 0.f};
-  const int nsteps = R.my_groups * 2;
   const bool b_lane = beta < b;
-  auto b_ptr = [&](int st) -> const uint8_t * {
-    const int wl = (R.cw + R.wpt * (st >> 1)) * kGroupWords + 2 * q + (st & 1);
-    return wl < w_count ? xs + (size_t)beta * row_stride(w_count) + wl * kSlot + 64 * hl_col : lds;
-  };
-  uint4 bop[2][kReads];
+  // the products of the wave's groups c0 .. c0 + kMaxGroups - 1 (sign words w)
+  auto products = [&](const u32x2 (&w)[kMaxGroups], int c0, int nsteps) {
+    auto b_ptr = [&](int st) -> const uint8_t * {
+      const int wl = (R.cw + R.wpt * (c0 + (st >> 1))) * kGroupWords + 2 * q + (st & 1);
+      return wl < w_count ? xs + (size_t)beta * row_stride(w_count) + wl * kSlot + 64 * hl_col
+                          : lds;
+    };
+    uint4 bop[2][kReads];
 #pragma unroll
-  for (int k = 0; k < kReads; ++k) bop[0][k] = bop[1][k] = make_uint4(0u, 0u, 0u, 0u);
-  if (nsteps > 0 && b_lane) {
-    const uint8_t *bs = b_ptr(0);
+    for (int k = 0; k < kReads; ++k) bop[0][k] = bop[1][k] = make_uint4(0u, 0u, 0u, 0u);
+    if (nsteps > 0 && b_lane) {
+      const uint8_t *bs = b_ptr(0);
 #pragma unroll
-    for (int k = 0; k < kReads; ++k) bop[0][k] = *reinterpret_cast<const uint4 *>(bs + 16 * k);
-  }
-  static_for<kMaxGroups * 2>([&](auto ST) {
-    constexpr int st = decltype(ST)::value;
-    constexpr int cur = st & 1;
-    if (st < nsteps) {  // wave-uniform
-      if (st + 1 < nsteps && b_lane) {
-        const uint8_t *bs = b_ptr(st + 1);
+      for (int k = 0; k < kReads; ++k) bop[0][k] = *reinterpret_cast<const uint4 *>(bs + 16 * k);
+    }
+    static_for<kMaxGroups * 2>([&](auto ST) {
+      constexpr int st = decltype(ST)::value;
+      constexpr int cur = st & 1;
+      if (st < nsteps) {  // wave-uniform
+        if (st + 1 < nsteps && b_lane) {
+          const uint8_t *bs = b_ptr(st + 1);
 #pragma unroll
-        for (int k = 0; k < kReads; ++k)
-          bop[cur ^ 1][k] = *reinterpret_cast<const uint4 *>(bs + 16 * k);
+          for (int k = 0; k < kReads; ++k)
+            bop[cur ^ 1][k] = *reinterpret_cast<const uint4 *>(bs + 16 * k);
+        }
+        const uint32_t wd = w[st >> 1][st & 1];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          uint4 a;
+          a.x = ((wd << (15 - (4 * t + 0))) & kSignMask) | (kOne & ~kSignMask);
+          a.y = ((wd << (15 - (4 * t + 1))) & kSignMask) | (kOne & ~kSignMask);
+          a.z = ((wd << (15 - (4 * t + 2))) & kSignMask) | (kOne & ~kSignMask);
+          a.w = ((wd << (15 - (4 * t + 3))) & kSignMask) | (kOne & ~kSignMask);
+          const bf16x8 av = __builtin_bit_cast(bf16x8, a);
+#pragma unroll
+          for (int hl = 0; hl < kChains; ++hl)
+            acc[t][hl] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                av, __builtin_bit_cast(bf16x8, bop[cur][4 * hl + t]), acc[t][hl], 0, 0, 0);
+        }
       }
-      const uint32_t w = wv[st >> 1][st & 1];
+    });
+  };
+  if constexpr (kLoop) {
+    const int nchunks = (R.my_groups + kMaxGroups - 1) / kMaxGroups;
+    for (int chunk = 0; chunk < nchunks; ++chunk) {
+      const int c0 = chunk * kMaxGroups;
+      u32x2 wnext[kMaxGroups];
+      if (chunk + 1 < nchunks) load_chunk(wnext, c0 + kMaxGroups);
+      products(wv, c0, min(R.my_groups - c0, kMaxGroups) * 2);
+      if (chunk + 1 < nchunks) {
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        uint4 a;
-        a.x = ((w << (15 - (4 * t + 0))) & kSignMask) | (kOne & ~kSignMask);
-        a.y = ((w << (15 - (4 * t + 1))) & kSignMask) | (kOne & ~kSignMask);
-        a.z = ((w << (15 - (4 * t + 2))) & kSignMask) | (kOne & ~kSignMask);
-        a.w = ((w << (15 - (4 * t + 3))) & kSignMask) | (kOne & ~kSignMask);
-        const bf16x8 av = __builtin_bit_cast(bf16x8, a);
-#pragma unroll
-        for (int hl = 0; hl < kChains; ++hl)
-          acc[t][hl] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              av, __builtin_bit_cast(bf16x8, bop[cur][4 * hl + t]), acc[t][hl], 0, 0, 0);
+        for (int i = 0; i < kMaxGroups; ++i) wv[i] = wnext[i];
       }
     }
-  });
+  } else {
+    products(wv, 0, R.my_groups * 2);
+  }
   floatx4 tot = acc[0][0];
 #pragma unroll
   for (int t = 0; t < 4; ++t)
@@ -571,7 +670,7 @@ __device__ __forceinline__ void stage_body(
       const int o = tid + kThreads * k;
       const int orow = row_wg0 + (o & (rows_wg - 1));
       if (o < nout && orow < rows)
-        store_device(&part[((size_t)blockIdx.y * b + (o >> rows_log2)) * rows + orow], sum[k]);
+        store_device(&part[((size_t)slab * b + (o >> rows_log2)) * rows + orow], sum[k]);
     }
     wait_memory();
     __syncthreads();
@@ -616,11 +715,18 @@ __device__ __forceinline__ void stage_body(
     const float v = sum[k] * f16_to_f32((uint16_t)rscale_bits[k]);
     if (o < nout && orow < rows) {
       size_t oi = (size_t)(o >> rows_log2) * rows + orow;
-      if (mode == kModePartial) oi += (size_t)blockIdx.y * b * rows;
-      if constexpr (kOutY)
-        static_cast<uint16_t *>(out)[oi] = f32_to_bf16(v);
-      else
-        static_cast<float *>(out)[oi] = v;
+      if (mode == kModePartial) oi += (size_t)slab * b * rows;
+      if constexpr (kCoherent) {
+        if constexpr (kOutY)
+          store_device_u16(static_cast<uint16_t *>(out) + oi, f32_to_bf16(v));
+        else
+          store_device(static_cast<float *>(out) + oi, v);
+      } else {
+        if constexpr (kOutY)
+          static_cast<uint16_t *>(out)[oi] = f32_to_bf16(v);
+        else
+          static_cast<float *>(out)[oi] = v;
+      }
     }
   }
 }
@@ -636,7 +742,7 @@ __global__ __launch_bounds__(kThreads) void gemv_stage_kernel(
     void *__restrict__ out, float *__restrict__ part, uint32_t *__restrict__ cnt, int red_off) {
   stage_body<kInX, kOutY, kHiLoCols, kMulti>(M, in, s_in, row_scale, rows, wpr, slab_words, b,
                                              rt_log2, nslabs, mode, in_parts, out, part, cnt,
-                                             (int)blockIdx.x, red_off);
+                                             (int)blockIdx.x, (int)blockIdx.y, red_off);
 }
 
 // One stage of several layers that share the input width (the segments):
@@ -669,7 +775,8 @@ __global__ __launch_bounds__(kThreads) void gemv_segs_kernel(const Segs segs, in
   const int g0 = sg > 0 ? segs.group_end[sg - 1] : 0;
   stage_body<kInX, kOutY, kHiLoCols, kMulti>(
       segs.M[sg], segs.in[sg], segs.s_in[sg], segs.row_scale[sg], segs.rows[sg], segs.wpr[sg],
-      slab_words, b, rt_log2, 1, mode, in_parts, segs.out[sg], nullptr, nullptr, g - g0);
+      slab_words, b, rt_log2, 1, mode, in_parts, segs.out[sg], nullptr, nullptr, g - g0,
+      (int)blockIdx.y);
 }
 
 size_t lds_stage_bytes(int64_t b, int slab_words) {
@@ -704,6 +811,8 @@ int max_slab_words(int64_t b, int rt_log2) {
   return (int)(w - w % kGroupWords);
 }
 
+StagePlan plan_slabs(int64_t rows, int64_t wpr, int64_t b, int rt, bool allow_partial, int cus);
+
 StagePlan plan_stage(int64_t rows, int64_t wpr, int64_t b, bool allow_partial, int cus) {
   const int64_t tiles = (rows + kTileRows - 1) / kTileRows;
   // Preferred tiles per workgroup for this batch (input shared over more
@@ -720,6 +829,12 @@ StagePlan plan_stage(int64_t rows, int64_t wpr, int64_t b, bool allow_partial, i
   while (rt < 3 && (((tiles + (1 << rt) - 1) >> rt) > 2 * cus)) ++rt;
   while (rt < want && wgs(rt + 1) >= cus / 2) ++rt;
   while (((int64_t)kTileRows << rt) * b > (int64_t)kThreads * kMaxOutPerThread) --rt;
+  return plan_slabs(rows, wpr, b, rt, allow_partial, cus);
+}
+
+// The column split of a stage whose workgroups own 16 << rt rows.
+StagePlan plan_slabs(int64_t rows, int64_t wpr, int64_t b, int rt, bool allow_partial, int cus) {
+  const int64_t tiles = (rows + kTileRows - 1) / kTileRows;
   StagePlan p{rt, 0, 0, kModeFinal};
   int sw = max_slab_words(b, rt);
   if (rt == 0) {
@@ -1006,6 +1121,508 @@ hipError_t launch_gemv(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
                      reinterpret_cast<float *>(base + L.part2),
                      reinterpret_cast<uint32_t *>(base + L.cnt2)};
   return launch_stage<false, true>(s2, L.p2, s);
+}
+
+// ---------------------------------------------------------------------------
+// Layer stream: the decode forward of a sequence of layers in one persistent
+// launch.  A decoder step at batch 1 runs dozens of small, dependent
+// products; as separate launches each pays a kernel boundary (about 1.6 us
+// in a replayed graph) and a cold start.  Here one grid of workgroups (one
+// 512-thread workgroup per compute unit, all resident) walks a precomputed
+// plan of phases.  A phase is a set of stage segments (the first or second product
+// of one layer) whose row groups are spread over the workgroups; phases are
+// separated by a grid barrier: every workgroup writes its arrival word and
+// polls all of them, with device-scope stores and loads and no atomic
+// read-modify-write, so no arrival waits for another (an uncontended
+// hand-off between compute units measured about 0.3 us within an XCD and
+// 0.4 us across XCDs).  Outputs that later phases read are written and read
+// at device scope.  Layers marked `wait` start after every earlier layer of
+// the call has finished (they may read those layers' outputs); the first
+// product of a layer that does not wait shares a phase with the second
+// product of the layer group before it.
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr uint32_t kStreamMagic = 0xAF15EA01u;
+constexpr int kStreamThreads = kThreads;
+constexpr int kStreamMaxGroupItems = 8;  // layers per group (a phase holds up to two groups)
+constexpr int kStreamMaxGrid = 512;     // workgroups (one per compute unit)
+constexpr int kSpinLimit = 1 << 20;      // polls per barrier before giving up
+// workspace header (uint32 words): epoch, error, arrival words
+constexpr int kSyncEpoch = 0, kSyncError = 1, kSyncFlags = 64;
+constexpr size_t kStreamHeaderBytes = (size_t)(kSyncFlags + 8 * kStreamMaxGrid) * 4;
+
+struct StreamSeg {
+  const uint32_t *M;
+  const void *in;
+  const uint16_t *s_in;
+  const uint16_t *row_scale;
+  void *out;
+  float *part;
+  uint32_t *cnt;
+  int32_t kind;  // 0: first product (x in, t out); 1: second (t in, y out)
+  int32_t rows, wpr, slab_words, rt_log2, nslabs, mode, in_parts, red_off;
+  int32_t groups;                // row groups (workgroup tasks per slab)
+  int32_t task_begin, task_end;  // this segment's tasks within its phase
+};
+
+struct StreamPhase {
+  int32_t seg_begin, seg_end, tasks, pad;
+};
+
+struct StreamHeader {
+  uint32_t magic, version;
+  int32_t nphases, nsegs, b, lds_bytes;
+  int32_t max_tasks, pad;
+  uint64_t plan_bytes, ws_bytes;
+  void *ws;  // the workspace the plan's pointers lie in
+};
+
+size_t stream_plan_size(int nphases, int nsegs) {
+  return sizeof(StreamHeader) + (size_t)nphases * sizeof(StreamPhase) +
+         (size_t)nsegs * sizeof(StreamSeg);
+}
+
+__device__ __forceinline__ uint32_t load_device_u32(const uint32_t *p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_device_u32(uint32_t *p, uint32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Grid barrier number `target`, in two halves so that a workgroup can issue
+// the next phase's weight loads while it waits.  Arrival words only grow, so
+// a word at or past the target has arrived.  Each workgroup writes its word
+// into kFlagReplicas copies and polls one copy (workgroup w polls copy w mod
+// kFlagReplicas), so the pollers spread over several memory lines instead
+// of all reading the same ones; two polls are kept in flight.
+constexpr int kFlagReplicas = 8;
+static_assert(kStreamHeaderBytes >= (size_t)(kSyncFlags + kFlagReplicas * kStreamMaxGrid) * 4,
+              "arrival words fit the header");
+
+// Every wave first waits for its own memory operations, so the phase's
+// stores are complete before the arrival word is written.
+__device__ __forceinline__ void barrier_arrive(uint32_t *sync, uint32_t target) {
+  wait_memory();
+  __syncthreads();
+  if (threadIdx.x < kFlagReplicas)
+    store_device_u32(sync + kSyncFlags + threadIdx.x * kStreamMaxGrid + blockIdx.x, target);
+}
+
+// Returns false when the error word is set (a wait timed out here or
+// elsewhere); every wave then leaves the phase loop.
+__device__ bool barrier_wait(uint32_t *sync, uint32_t target) {
+  __shared__ uint32_t s_ok;
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    const int G = (int)gridDim.x;
+    const __amdgpu_buffer_rsrc_t fres = buffer_rsrc(
+        sync + kSyncFlags + (blockIdx.x % kFlagReplicas) * kStreamMaxGrid, (int64_t)G * 4);
+    auto poll = [&](uint32_t (&f)[kStreamMaxGrid / 64]) {
+#pragma unroll
+      for (int k = 0; k < kStreamMaxGrid / 64; ++k) {
+        const int w = 64 * k + lane;
+        f[k] = target;
+        if (64 * k < G)  // uniform
+          f[k] = __builtin_amdgcn_raw_buffer_load_b32(fres, w < G ? w * 4 : kOob, 0, kDeviceScope);
+      }
+    };
+    auto arrived = [&](const uint32_t (&f)[kStreamMaxGrid / 64]) {
+      bool mine = true;
+#pragma unroll
+      for (int k = 0; k < kStreamMaxGrid / 64; ++k)
+        mine = mine && (64 * k + lane >= G || (int)(f[k] - target) >= 0);
+      return __all(mine);
+    };
+    bool ok = true;
+    uint32_t fa[kStreamMaxGrid / 64], fb[kStreamMaxGrid / 64];
+    poll(fa);
+    for (int it = 0;; it += 2) {
+      poll(fb);
+      if (arrived(fa)) break;
+      poll(fa);
+      if (arrived(fb)) break;
+      if (load_device_u32(sync + kSyncError) != 0u) {
+        ok = false;
+        break;
+      }
+      if (it >= kSpinLimit) {
+        if (lane == 0) store_device_u32(sync + kSyncError, 1u);
+        ok = false;
+        break;
+      }
+    }
+    if (lane == 0) s_ok = ok ? 1u : 0u;
+  }
+  __syncthreads();
+  return s_ok != 0u;
+}
+
+template <bool kHiLo>
+__device__ __forceinline__ void stream_task(const StreamSeg &g, int b, int task,
+                                            const SignRegs &pre) {
+  const int local = task - g.task_begin;
+  const int group = local % g.groups;
+  const int slab = local / g.groups;
+  if (g.kind == 0) {
+    if (g.rt_log2 > 0)
+      stage_body<true, false, kHiLo, true, true, true>(g.M, g.in, g.s_in, g.row_scale, g.rows, g.wpr,
+                                                 g.slab_words, b, g.rt_log2, g.nslabs, g.mode,
+                                                 g.in_parts, g.out, g.part, g.cnt, group, slab,
+                                                 g.red_off, &pre);
+    else
+      stage_body<true, false, kHiLo, false, true, true>(g.M, g.in, g.s_in, g.row_scale, g.rows, g.wpr,
+                                                  g.slab_words, b, 0, g.nslabs, g.mode,
+                                                  g.in_parts, g.out, g.part, g.cnt, group, slab,
+                                                  g.red_off, &pre);
+  } else {
+    if (g.rt_log2 > 0)
+      stage_body<false, true, kHiLo, true, true, true>(g.M, g.in, g.s_in, g.row_scale, g.rows, g.wpr,
+                                                 g.slab_words, b, g.rt_log2, g.nslabs, g.mode,
+                                                 g.in_parts, g.out, g.part, g.cnt, group, slab,
+                                                 g.red_off, &pre);
+    else
+      stage_body<false, true, kHiLo, false, true, true>(g.M, g.in, g.s_in, g.row_scale, g.rows, g.wpr,
+                                                  g.slab_words, b, 0, g.nslabs, g.mode,
+                                                  g.in_parts, g.out, g.part, g.cnt, group, slab,
+                                                  g.red_off, &pre);
+  }
+}
+
+// The persistent walk over the plan's phases.  Task t of a phase runs on
+// workgroup t mod grid; a workgroup with no task in a phase goes straight to
+// the barrier.  A workgroup reads the plan entry of its next task and loads
+// that task's sign words as soon as it has arrived at the barrier before it
+// (weights do not depend on the phase's outputs), so the HBM latency of the
+// signs overlaps the wait.  The epoch (the arrival value of the call's first
+// barrier minus one) is read by every workgroup before its first arrival,
+// and advanced by workgroup 0 once every workgroup has passed the first
+// barrier.
+template <bool kHiLo>
+__global__ __launch_bounds__(kStreamThreads, 2) void stream_kernel(const uint8_t *__restrict__ plan,
+                                                                   uint32_t *__restrict__ sync) {
+  const StreamHeader *h = reinterpret_cast<const StreamHeader *>(plan);
+  const StreamPhase *phases = reinterpret_cast<const StreamPhase *>(plan + sizeof(StreamHeader));
+  const StreamSeg *segs =
+      reinterpret_cast<const StreamSeg *>(plan + sizeof(StreamHeader) +
+                                          (size_t)h->nphases * sizeof(StreamPhase));
+  const int nphases = h->nphases, b = h->b;
+  const int G = (int)gridDim.x;
+  const uint32_t epoch = load_device_u32(sync + kSyncEpoch);
+  if (load_device_u32(sync + kSyncError) != 0u) return;
+  // next task of this workgroup: phase np, task nt (np == nphases: none)
+  int np = 0, nt = (int)blockIdx.x;
+  auto advance = [&]() {
+    while (np < nphases && nt >= phases[np].tasks) {
+      ++np;
+      nt = (int)blockIdx.x;
+    }
+  };
+  StreamSeg nseg;
+  SignRegs nsig;
+  auto prefetch = [&]() {
+    advance();
+    if (np >= nphases) return;
+    const StreamPhase ph = phases[np];
+    int sg = ph.seg_begin;
+    while (sg + 1 < ph.seg_end && nt >= segs[sg].task_end) ++sg;
+    nseg = segs[sg];
+    const int local = nt - nseg.task_begin;
+    stage_signs(nsig, nseg.M, nseg.rows, nseg.wpr, nseg.slab_words, nseg.rt_log2,
+                local % nseg.groups, local / nseg.groups, nseg.row_scale, b);
+  };
+  prefetch();
+  for (int p = 0; p < nphases; ++p) {
+    while (np == p) {
+      const StreamSeg seg = nseg;
+      const SignRegs sig = nsig;
+      const int task = nt;
+      nt += G;
+      stream_task<kHiLo>(seg, b, task, sig);
+      __syncthreads();  // LDS is reused by the next task
+      if (np == p && nt < phases[p].tasks) prefetch();  // another task in this phase
+      else break;
+    }
+    if (p + 1 < nphases) {
+      barrier_arrive(sync, epoch + (uint32_t)p + 1u);
+      if (np == p) prefetch();  // the next task lies in a later phase
+      if (!barrier_wait(sync, epoch + (uint32_t)p + 1u)) return;
+    }
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0 && nphases > 1)
+    store_device_u32(sync + kSyncEpoch, epoch + (uint32_t)nphases);
+}
+
+size_t seg_lds_bytes(const StagePlan &p, int64_t b, int wpr, int *red_off) {
+  const int sw = p.slab_words < wpr ? p.slab_words : wpr;
+  size_t lds = lds_bytes_for(b, sw);
+  *red_off = 0;
+  if (p.rt_log2 == 0) {
+    const size_t stage = (lds_stage_bytes(b, sw) + 15) & ~(size_t)15;
+    if (stage + kRedBytes <= (size_t)kLdsBudget) {
+      *red_off = (int)stage;
+      lds = stage + kRedBytes;
+    }
+  }
+  return lds;
+}
+
+struct PendingSeg {
+  int item, kind;
+  StagePlan p;
+};
+
+// A stage plan for the stream kernel: workgroups of 16 << rt rows, whole
+// rows of signs (a wave takes as many groups as it needs, in chunks), the
+// columns split only when the staged input would not fit the LDS; with
+// `halves`, a first product's columns are split in two partial results.
+StagePlan stream_stage_plan(int64_t wpr, int64_t b, int rt, bool halves) {
+  int64_t sw = ((kLdsBudget - 17 * kSlot) / b - 16) / kSlot;
+  sw -= sw % kGroupWords;
+  StagePlan p{rt, 0, 0, kModeFinal};
+  const int64_t full = ((wpr + kGroupWords - 1) / kGroupWords) * kGroupWords;
+  p.slab_words = (int)(sw < full ? sw : full);
+  p.nslabs = (int)((wpr + p.slab_words - 1) / p.slab_words);
+  if (p.nslabs > 1) {
+    p.mode = kModeLastSlab;
+    return p;
+  }
+  const int64_t groups = full / kGroupWords;
+  if (halves && rt == 0 && groups >= 2 && b <= 8) {
+    p.slab_words = (int)(((groups + 1) / 2) * kGroupWords);
+    p.nslabs = (int)((wpr + p.slab_words - 1) / p.slab_words);
+    p.mode = p.nslabs > 1 ? kModePartial : kModeFinal;
+  }
+  return p;
+}
+
+}  // namespace
+
+
+// The plan of a layer stream.  With plan_out == nullptr only the sizes are
+// computed (*plan_need, *ws_need); otherwise the plan is written with
+// pointers into the workspace at `ws` (plan_bytes must hold *plan_need).
+void stream_plan_impl(const af1_stream_item *items, int count, int64_t b, void *ws,
+                      void *plan_out, size_t *plan_need, size_t *ws_need) {
+  const int cus = device_cus();
+  const int grid = cus < kStreamMaxGrid ? cus : kStreamMaxGrid;  // one workgroup per CU
+  std::vector<StagePlan> p1(count), p2(count);
+  for (int i = 0; i < count; ++i) {
+    const af1_factorized_linear &L = items[i].L;
+    p1[i] = stream_stage_plan(L.n / 32, b, 0, false);
+    p2[i] = stream_stage_plan(L.r / 32, b, 0, false);
+  }
+  // layer groups: a new group at a layer that waits, or when the group is full
+  std::vector<int> gstart;
+  for (int i = 0; i < count; ++i)
+    if (i == 0 || items[i].wait != 0 || i - gstart.back() >= kStreamMaxGroupItems)
+      gstart.push_back(i);
+  gstart.push_back(count);
+  const int ngroups = (int)gstart.size() - 1;
+  // phases as lists of (item, kind)
+  std::vector<std::vector<PendingSeg>> ph;
+  auto add_stage = [&](std::vector<PendingSeg> &dst, int g, int kind) {
+    for (int i = gstart[g]; i < gstart[g + 1]; ++i)
+      dst.push_back(PendingSeg{i, kind, kind == 0 ? p1[i] : p2[i]});
+  };
+  ph.emplace_back();
+  add_stage(ph.back(), 0, 0);
+  for (int g = 0; g < ngroups; ++g) {
+    ph.emplace_back();
+    add_stage(ph.back(), g, 1);
+    if (g + 1 < ngroups) {
+      if (items[gstart[g + 1]].wait == 0) {
+        add_stage(ph.back(), g + 1, 0);
+      } else {
+        ph.emplace_back();
+        add_stage(ph.back(), g + 1, 0);
+      }
+    }
+  }
+  // Per phase: more rows per workgroup while the phase has more tasks than
+  // workgroups (each task beyond the grid is another round of latency),
+  // starting with the segment that has the most tasks; then, while the grid
+  // has room, first products split their columns in two (more workgroups
+  // share a latency-bound product), the segment with the fewest tasks
+  // first.
+  auto tasks_of = [&](const PendingSeg &sgm) {
+    const af1_factorized_linear &L = items[sgm.item].L;
+    const int64_t rows = sgm.kind == 0 ? L.r : L.m;
+    const int64_t rw = (int64_t)kTileRows << sgm.p.rt_log2;
+    return ((rows + rw - 1) / rw) * sgm.p.nslabs;
+  };
+  auto wpr_of = [&](const PendingSeg &sgm) {
+    const af1_factorized_linear &L = items[sgm.item].L;
+    return sgm.kind == 0 ? L.n / 32 : L.r / 32;
+  };
+  for (auto &phase : ph) {
+    auto total = [&]() {
+      int64_t t = 0;
+      for (const auto &sgm : phase) t += tasks_of(sgm);
+      return t;
+    };
+    for (int guard = 0; guard < 64 && total() > grid; ++guard) {
+      int best = -1;
+      int64_t best_tasks = 0;
+      for (int k = 0; k < (int)phase.size(); ++k) {
+        const PendingSeg &sgm = phase[k];
+        if (sgm.p.rt_log2 >= 3 || ((int64_t)kTileRows << (sgm.p.rt_log2 + 1)) * b >
+                                      (int64_t)kThreads * kMaxOutPerThread)
+          continue;
+        const int64_t t = tasks_of(sgm);
+        if (t > best_tasks) {
+          best_tasks = t;
+          best = k;
+        }
+      }
+      if (best < 0) break;
+      PendingSeg &sgm = phase[best];
+      sgm.p = stream_stage_plan(wpr_of(sgm), b, sgm.p.rt_log2 + 1, false);
+    }
+    for (int guard = 0; guard < 64; ++guard) {
+      int best = -1;
+      int64_t best_tasks = 0;
+      for (int k = 0; k < (int)phase.size(); ++k) {
+        const PendingSeg &sgm = phase[k];
+        if (sgm.kind != 0 || sgm.p.rt_log2 != 0 || sgm.p.mode != kModeFinal) continue;
+        const int64_t t = tasks_of(sgm);
+        if (best < 0 || t < best_tasks) {
+          best_tasks = t;
+          best = k;
+        }
+      }
+      if (best < 0) break;
+      PendingSeg trial = phase[best];
+      trial.p = stream_stage_plan(wpr_of(trial), b, 0, true);
+      if (trial.p.mode != kModePartial || total() - best_tasks + tasks_of(trial) > grid) break;
+      phase[best] = trial;
+    }
+    for (const auto &sgm : phase)
+      if (sgm.kind == 0) p1[sgm.item] = sgm.p;
+  }
+  // the second product's input parts follow the first product's final plan
+  int nsegs = 0;
+  for (const auto &phase : ph) nsegs += (int)phase.size();
+  const int nphases = (int)ph.size();
+  const size_t need = stream_plan_size(nphases, nsegs);
+  // workspace: header, then per item t (parts x b x r fp32), then per
+  // last-slab segment its counters and partial sums
+  size_t off = align256(kStreamHeaderBytes);
+  std::vector<size_t> t_off(count);
+  for (int i = 0; i < count; ++i) {
+    const int parts = p1[i].mode == kModePartial ? p1[i].nslabs : 1;
+    t_off[i] = off;
+    off += align256((size_t)parts * b * items[i].L.r * 4);
+  }
+  // without an output the segments go to a scratch copy (sizes only)
+  std::vector<uint8_t> scratch_plan;
+  uint8_t *out = static_cast<uint8_t *>(plan_out);
+  if (!out) {
+    scratch_plan.resize(need);
+    out = scratch_plan.data();
+  }
+  uint8_t *wsb = static_cast<uint8_t *>(ws);
+  StreamHeader *hd = reinterpret_cast<StreamHeader *>(out);
+  StreamPhase *phs = reinterpret_cast<StreamPhase *>(out + sizeof(StreamHeader));
+  StreamSeg *sg = reinterpret_cast<StreamSeg *>(out + sizeof(StreamHeader) +
+                                                (size_t)nphases * sizeof(StreamPhase));
+  std::memset(out, 0, need);
+  size_t lds_max = 0;
+  int max_tasks = 0, si = 0;
+  for (int pi = 0; pi < nphases; ++pi) {
+    phs[pi].seg_begin = si;
+    int task = 0;
+    for (const auto &sgm : ph[pi]) {
+      const af1_stream_item &it = items[sgm.item];
+      const af1_factorized_linear &L = it.L;
+      StreamSeg &g = sg[si];
+      const bool first = sgm.kind == 0;
+      g.kind = sgm.kind;
+      g.M = first ? L.Bv : L.Bu;
+      g.in = first ? static_cast<const void *>(it.x) : nullptr;  // t set below (base-relative)
+      g.s_in = first ? L.s_in : nullptr;
+      g.row_scale = first ? L.s_mid : L.s_out;
+      g.out = first ? nullptr : static_cast<void *>(it.y);
+      g.rows = (int)(first ? L.r : L.m);
+      g.wpr = (int)(first ? L.n / 32 : L.r / 32);
+      g.slab_words = sgm.p.slab_words;
+      g.rt_log2 = sgm.p.rt_log2;
+      g.nslabs = sgm.p.nslabs;
+      g.mode = sgm.p.mode;
+      g.in_parts = first ? 1 : (p1[sgm.item].mode == kModePartial ? p1[sgm.item].nslabs : 1);
+      const int64_t rw = (int64_t)kTileRows << g.rt_log2;
+      g.groups = (int)((g.rows + rw - 1) / rw);
+      g.task_begin = task;
+      task += g.groups * g.nslabs;
+      g.task_end = task;
+      int red_off = 0;
+      const size_t lds = seg_lds_bytes(sgm.p, b, g.wpr, &red_off);
+      g.red_off = red_off;
+      if (lds > lds_max) lds_max = lds;
+      // the item's t in the workspace
+      if (first)
+        g.out = wsb + t_off[sgm.item];
+      else
+        g.in = wsb + t_off[sgm.item];
+      if (g.mode == kModeLastSlab) {
+        g.cnt = reinterpret_cast<uint32_t *>(wsb + off);
+        off += align256((size_t)g.groups * 4);
+        g.part = reinterpret_cast<float *>(wsb + off);
+        off += align256((size_t)g.nslabs * b * g.rows * 4);
+      }
+      ++si;
+    }
+    phs[pi].seg_end = si;
+    phs[pi].tasks = task;
+    if (task > max_tasks) max_tasks = task;
+  }
+  hd->magic = kStreamMagic;
+  hd->version = 1;
+  hd->nphases = nphases;
+  hd->nsegs = nsegs;
+  hd->b = (int)b;
+  hd->lds_bytes = (int)lds_max;
+  hd->max_tasks = max_tasks;
+  hd->plan_bytes = need;
+  hd->ws_bytes = off;
+  hd->ws = ws;
+  *plan_need = need;
+  *ws_need = off;
+}
+
+int stream_plan_check(const void *plan, size_t plan_bytes) {
+  const StreamHeader *h = static_cast<const StreamHeader *>(plan);
+  if (!h || plan_bytes < sizeof(StreamHeader) || h->magic != kStreamMagic || h->version != 1 ||
+      h->nphases < 2 || h->nsegs < 2 || h->b < 1 || h->b > 16 || h->plan_bytes > plan_bytes ||
+      stream_plan_size(h->nphases, h->nsegs) != h->plan_bytes || !h->ws)
+    return -1;
+  return 0;
+}
+
+void *stream_plan_workspace(const void *plan) {
+  return static_cast<const StreamHeader *>(plan)->ws;
+}
+
+hipError_t launch_stream(const void *plan_dev, const void *plan_host, hipStream_t s) {
+  const StreamHeader *h = static_cast<const StreamHeader *>(plan_host);
+  void *ws = h->ws;
+  const int cus = device_cus();
+  const size_t lds = (size_t)h->lds_bytes;
+  auto go = [&](auto kernel) -> hipError_t {
+    int per_cu = 0;
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kStreamThreads,
+                                                                lds);
+    if (e != hipSuccess) return e;
+    if (per_cu < 1) return hipErrorInvalidConfiguration;
+    // every workgroup must be resident at once (they wait for each other):
+    // one per compute unit (the kernel takes up to 256 registers a lane)
+    int grid = cus;
+    if (grid > kStreamMaxGrid) grid = kStreamMaxGrid;
+    kernel<<<grid, kStreamThreads, lds, s>>>(static_cast<const uint8_t *>(plan_dev),
+                                             static_cast<uint32_t *>(ws));
+    return hipGetLastError();
+  };
+  return h->b <= 8 ? go(stream_kernel<true>) : go(stream_kernel<false>);
 }
 
 }  // namespace af1

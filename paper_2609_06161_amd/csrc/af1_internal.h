@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "af1.h"
+
 namespace af1 {
 
 // Compute units of the current device (queried once per device; 256 if the
@@ -33,6 +35,16 @@ hipError_t launch_gemv(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
 // (none when no stage splits its columns); a fill kernel, no memset node.
 hipError_t launch_gemv_clear_counters(int64_t m, int64_t n, int64_t r, int64_t b, void *ws,
                                       hipStream_t s);
+
+// Layer stream (one persistent launch for a sequence of layers).  The plan
+// is built on the host (sizes only when plan_out is null) with pointers into
+// the workspace `ws`; stream_plan_check validates a plan's header;
+// launch_stream runs the plan's device copy.
+void stream_plan_impl(const af1_stream_item *items, int count, int64_t b, void *ws,
+                      void *plan_out, size_t *plan_need, size_t *ws_need);
+int stream_plan_check(const void *plan, size_t plan_bytes);
+void *stream_plan_workspace(const void *plan);
+hipError_t launch_stream(const void *plan_dev, const void *plan_host, hipStream_t s);
 
 // Several layers that share n (count <= 4): two launches for all of them
 // when the plan allows, else one call per layer on the same workspace.

@@ -139,3 +139,37 @@ def gemv_multi(layers, x: torch.Tensor, ys=None, ws: torch.Tensor = None, stream
             ws = torch.zeros(max(need, 256), dtype=torch.uint8, device=x.device)
         af1.af1_linear_gemv_multi(descs, x, b, ys, ws, ws.numel(), stream)
     return ys
+
+
+class LayerStream:
+    """A decode pass over a sequence of layers in one persistent launch.
+
+    entries: (DeviceLayer, x, y, wait) tuples, x / y device tensors of bf16
+    patterns ([b, n] and [b, m]); wait=True makes an item start after every
+    earlier item has finished (it may read their outputs).  The plan is built
+    once here, bound to these buffers and to the zero-filled workspace, and
+    copied to the device; run() launches one pass."""
+
+    def __init__(self, entries, b, device="cuda"):
+        self.entries = list(entries)
+        self.b = int(b)
+        self.items = af1.stream_items([(L.desc, x, y, w) for L, x, y, w in self.entries])
+        ws_bytes = af1.af1_stream_workspace_bytes(self.items, self.b)
+        plan_bytes = af1.af1_stream_plan_bytes(self.items, self.b)
+        if ws_bytes == 0 or plan_bytes == 0:
+            # report the argument error through the plan call
+            af1.af1_stream_plan(self.items, self.b, None, 0, None, 0)
+        self.ws = torch.zeros(ws_bytes, dtype=torch.uint8, device=device)
+        # 16-byte aligned host buffer (numpy aligns large arrays further)
+        self._plan_buf = np.zeros(plan_bytes + 16, np.uint8)
+        off = (-self._plan_buf.ctypes.data) % 16
+        self.plan = self._plan_buf[off:off + plan_bytes]
+        af1.af1_stream_plan(self.items, self.b, self.ws, ws_bytes, self.plan, plan_bytes)
+        self.plan_dev = torch.from_numpy(self.plan.copy()).to(device)
+
+    def run(self, stream=None):
+        af1.af1_linear_stream(self.plan, self.plan_dev, stream)
+
+    def error_word(self) -> int:
+        """Non-zero when a barrier of an earlier pass timed out."""
+        return int(self.ws[4:8].view(torch.int32).item())

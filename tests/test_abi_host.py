@@ -434,3 +434,74 @@ def test_nabf_iteration_validation():
         E.AF1_ERR_NULL
     assert nabf.af1_nabf_export(S, None, None, W0, None, W2, stream=0, check=False) == \
         E.AF1_ERR_NULL
+
+
+# --------------------------------------------------------------------------
+# layer stream: planning and validation (host only; nothing is launched)
+# --------------------------------------------------------------------------
+
+def stream_entries(specs, base=BASE):
+    """(m, n, r, x, y, wait) -> stream items over fake, disjoint layer arrays."""
+    entries = []
+    for i, (m, n, r, x, y, wait) in enumerate(specs):
+        entries.append((fake_layer(m, n, r, base + 1024 * MB + i * 64 * MB), x, y, wait))
+    return af1.stream_items(entries)
+
+
+def test_stream_plan_sizes_and_validation():
+    q = (4096, 4096, 2016, X, Y, False)
+    o = (4096, 4096, 2016, Y, Y + 1 * MB, True)           # reads q's output, waits
+    items = stream_entries([q, o])
+    ws = af1.af1_stream_workspace_bytes(items, 1)
+    plan = af1.af1_stream_plan_bytes(items, 1)
+    assert ws >= 2 * 2016 * 4 and 0 < plan < 4096
+    buf = np.zeros(plan, np.uint8)
+    assert af1.af1_stream_plan(items, 1, WS, ws, buf, plan, check=False) == af1.AF1_OK
+    assert af1.af1_stream_plan(items, 1, WS, ws - 1, buf, plan, check=False) == \
+        af1.AF1_ERR_WORKSPACE
+    assert af1.af1_stream_plan(items, 1, WS, ws, buf, plan - 1, check=False) == \
+        af1.AF1_ERR_WORKSPACE
+    assert af1.af1_stream_plan(items, 0, WS, ws, buf, plan, check=False) == af1.AF1_ERR_BATCH
+    assert af1.af1_stream_plan(items, 17, WS, ws, buf, plan, check=False) == af1.AF1_ERR_BATCH
+    assert af1.af1_stream_plan(items, 1, WS, ws, buf, plan, count=0, check=False) == \
+        af1.AF1_ERR_SHAPE
+    assert af1.af1_stream_plan(None, 1, WS, ws, buf, plan, count=1, check=False) == \
+        af1.AF1_ERR_NULL
+    # o reading q's output without waiting: rejected
+    bad = stream_entries([q, (4096, 4096, 2016, Y, Y + 1 * MB, False)])
+    assert af1.af1_stream_plan(bad, 1, WS, ws, buf, plan, check=False) == af1.AF1_ERR_ALIAS
+    # two outputs on one buffer
+    bad = stream_entries([q, (4096, 4096, 2016, X, Y, False)])
+    assert af1.af1_stream_plan(bad, 1, WS, ws, buf, plan, check=False) == af1.AF1_ERR_ALIAS
+    # the workspace over an input
+    assert af1.af1_stream_plan(items, 1, X, ws, buf, plan, check=False) == af1.AF1_ERR_ALIAS
+    # a misaligned item
+    bad = stream_entries([(4096, 4096, 2016, X + 8, Y, False)])
+    assert af1.af1_stream_plan(bad, 1, WS, ws, buf, plan, check=False) == af1.AF1_ERR_ALIGN
+
+
+def test_stream_rejects_foreign_plans():
+    junk = np.zeros(4096, np.uint8)
+    assert af1.af1_linear_stream(junk, BASE, 0, check=False) == af1.AF1_ERR_PLAN
+    assert af1.af1_linear_stream(None, BASE, 0, check=False) == af1.AF1_ERR_NULL
+    assert af1.af1_linear_stream(junk, BASE + 8, 0, check=False) == af1.AF1_ERR_ALIGN
+
+
+def test_stream_plan_of_the_8b_stack_is_small():
+    """224 linears (the 32-layer stack): a plan of a few hundred kB at most
+    and a workspace of a few MB."""
+    entries = synth.draw_stack_ranks(77, 32, [("q", 4096, 4096, 2016), ("k", 1024, 4096, 800),
+                                              ("v", 1024, 4096, 800), ("o", 4096, 4096, 2016),
+                                              ("gate", 14336, 4096, 3136),
+                                              ("up", 14336, 4096, 3136),
+                                              ("down", 4096, 14336, 3136)],
+                                     af1.af1_storage_bits)
+    specs = []
+    for i, (name, m, n, r0, r) in enumerate(entries):
+        specs.append((m, n, r, X + (i % 7) * 256 * 1024, Y + i * 64 * 1024,
+                      name in ("q", "o", "gate", "down")))
+    items = af1.stream_items([(fake_layer(m, n, r, BASE + 2048 * MB + i * 32 * MB), x, y, w)
+                              for i, (m, n, r, x, y, w) in enumerate(specs)])
+    plan = af1.af1_stream_plan_bytes(items, 1)
+    ws = af1.af1_stream_workspace_bytes(items, 1)
+    assert 0 < plan < 512 * 1024 and 0 < ws < 16 * MB
