@@ -120,7 +120,7 @@ class DevicePool:
         self.m, self.n, self.r, self.count = m, n, r, count
 
 
-def decode_time(args, torch, stream, m, n, r, b, seed, steps):
+def decode_time(args, torch, stream, m, n, r, b, seed, steps, exact_steps=None):
     """µs per layer of the decode forward over a pool of distinct layers
     (> 2x the last-level cache), eager and as a replayed HIP graph of one
     pass over the pool."""
@@ -159,11 +159,30 @@ def decode_time(args, torch, stream, m, n, r, b, seed, steps):
     per = sorted(time_events(lambda i: graph.replay(), 1, stream) * 1e3 / pool
                  for _ in range(max(5, min(replays, 50))))
     pct = lambda q: per[min(len(per) - 1, int(q * (len(per) - 1) + 0.5))]
-    del graph, P
-    return dict(m=m, n=n, r=r, b=b, pool=pool, pool_mb=pool * layer_bytes / 2 ** 20,
-                steps_timed=replays * pool, us_graph=ms_graph * 1e3, us_eager=ms_eager * 1e3,
-                us_graph_p10=pct(0.1), us_graph_p50=pct(0.5), us_graph_p90=pct(0.9),
-                alg_bytes=gemv_algorithmic_bytes(m, n, r, b))
+    del graph
+    out = dict(m=m, n=n, r=r, b=b, pool=pool, pool_mb=pool * layer_bytes / 2 ** 20,
+               steps_timed=replays * pool, us_graph=ms_graph * 1e3, us_eager=ms_eager * 1e3,
+               us_graph_p10=pct(0.1), us_graph_p50=pct(0.5), us_graph_p90=pct(0.9),
+               alg_bytes=gemv_algorithmic_bytes(m, n, r, b))
+    if exact_steps:
+        # W warmup calls, then exactly K calls in one timed graph replay,
+        # walking the layer pool in order (a layer comes back only after
+        # the whole pool, more than twice the last-level cache, has passed)
+        K, W = exact_steps
+        gw = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gw):
+            for i in range(max(W, 1)):
+                step(i % pool)
+        g2 = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g2):
+            for i in range(K):
+                step((max(W, 1) + i) % pool)
+        gw.replay()
+        ms_k = time_events(lambda i: g2.replay(), 1, stream)
+        out.update(exact_steps=K, exact_warmup=W, exact_ms=ms_k)
+        del g2, gw
+    del P
+    return out
 
 
 def launch_floor(torch, stream, count=256, replays=20):
@@ -271,6 +290,119 @@ def bench_stack(args, torch, stream):
         del graph
     out["us_per_linear"] = round(out["us_per_decoder_layer"] / 7, 3)
     del pools
+    return out
+
+
+def bench_layer_stream(args, torch, stream):
+    """The layer stream (af1_linear_stream: one persistent launch for a
+    sequence of layers) on the 8B stack and on the 4096^2 pool, with two
+    schedules: every layer waiting for the earlier ones where a decoder
+    would (q, o, gate and down wait; for the pool, every layer), and the
+    workload as specified (each linear reads a fixed synthetic x, so no
+    linear waits for another; weights still stream in layer order)."""
+    from paper_2609_06161_amd import af1, synth
+    from paper_2609_06161_amd.layer import LayerStream, to_device
+
+    class Desc:
+        def __init__(self, d):
+            self.desc = d
+
+    def graph_ms(fn, reps=5):
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            fn()
+        time_events(lambda i: graph.replay(), 2, stream)
+        ms = time_events(lambda i: graph.replay(), reps, stream) / reps
+        del graph
+        return ms
+
+    out = {}
+    entries = synth.draw_stack_ranks(77, 32, STACK_LINEARS, af1.af1_storage_bits)
+    xs = {w: to_device(synth.make_activations(60 + w % 97, 1, w)) for w in (4096, 14336)}
+    pools = [DevicePool(torch, m, n, r, 1, 5000 + i) for i, (_, m, n, _, r) in
+             enumerate(entries)]
+    alg = sum(gemv_algorithmic_bytes(m, n, r, 1) for _, m, n, _, r in entries)
+    for label, waits in (("decoder_waits", ("q", "o", "gate", "down")), ("independent", ())):
+        items = [(Desc(P.desc[0]), xs[n], torch.empty((1, m), dtype=torch.int16, device="cuda"),
+                  name in waits) for P, (name, m, n, _, r) in zip(pools, entries)]
+        S = LayerStream(items, 1)
+        ms = graph_ms(S.run)
+        out[f"stack_{label}_us_per_decoder_layer"] = round(ms * 1e3 / 32, 3)
+        out[f"stack_{label}_gbs"] = round(alg / (ms * 1e-3) / 1e9, 1)
+        del S, items
+    del pools
+    m, n, r = synth.SHAPES["attn4096"]
+    pool = max(2, -(-POOL_BYTES // (r * (m + n) // 8)))
+    P = DevicePool(torch, m, n, r, pool, 1000)
+    x = to_device(synth.make_activations(1000, 1, n))
+    for label, wait in (("each_layer_waits", True), ("independent", False)):
+        items = [(Desc(P.desc[i]), x, torch.empty((1, m), dtype=torch.int16, device="cuda"),
+                  wait) for i in range(pool)]
+        S = LayerStream(items, 1)
+        ms = graph_ms(S.run)
+        us = ms * 1e3 / pool
+        out[f"sq4096_{label}_us_per_layer"] = round(us, 3)
+        out[f"sq4096_{label}_hbm_frac"] = round(gemv_algorithmic_bytes(m, n, r, 1) /
+                                                (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)
+        del S, items
+    del P
+    return out
+
+
+def bench_dense_decode(args, torch, stream, af1_us):
+    """Context for the paper's BF16-vs-AF1 decode ratio: the dense bf16
+    layers these factorizations replace, as torch.matmul of a [1, n] bf16
+    activation with a contiguous [n, m] bf16 weight (hipBLASLt/rocBLAS), over
+    pools of weights larger than twice the last-level cache, replayed in
+    HIP graphs.  af1_us is the headline AF1 time of the 4096^2 layer."""
+    out = {}
+
+    def graph_ms(fn, calls, reps=5):
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            fn()
+        time_events(lambda i: graph.replay(), 2, stream)
+        ms = time_events(lambda i: graph.replay(), reps, stream) / reps
+        del graph
+        return ms / calls
+
+    n = m = 4096
+    count = 16                               # 16 x 32 MB = 512 MB
+    W = [torch.randn((n, m), device="cuda", dtype=torch.bfloat16) for _ in range(count)]
+    x = torch.randn((1, n), device="cuda", dtype=torch.bfloat16)
+    ys = [None] * count
+
+    def run():
+        for i in range(count):
+            ys[i] = torch.matmul(x, W[i])
+    ms = graph_ms(run, count)
+    out["sq4096_b1_dense_bf16_us"] = round(ms * 1e3, 3)
+    out["sq4096_b1_dense_bf16_gbs"] = round(n * m * 2 / (ms * 1e-3) / 1e9, 1)
+    out["sq4096_b1_af1_speedup_vs_dense_bf16"] = round(ms * 1e3 / af1_us, 3)
+    del W, ys
+    # two decoder layers of the 8B shapes (872 MB of bf16 weights)
+    shapes = [(m_, n_) for _, m_, n_, _ in STACK_LINEARS]
+    Ws = [torch.randn((n_, m_), device="cuda", dtype=torch.bfloat16)
+          for _ in range(2) for m_, n_ in shapes]
+    xs = {w: torch.randn((1, w), device="cuda", dtype=torch.bfloat16) for w in (4096, 14336)}
+    outs = [None] * len(Ws)
+
+    def run_stack():
+        for i, Wd in enumerate(Ws):
+            outs[i] = torch.matmul(xs[Wd.shape[0]], Wd)
+    ms = graph_ms(run_stack, 2)
+    out["stack_dense_bf16_us_per_decoder_layer"] = round(ms * 1e3, 3)
+    del Ws, outs
     return out
 
 
@@ -576,23 +708,46 @@ def bench_pack(args, torch, stream):
     return out
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def bench_cpu_oracle(args):
+    """The fp64 oracle on the host: the 4096x4096 r=2016 layer at the bench's
+    batch, with every OpenMP thread, then with one."""
     import oracle
     from paper_2609_06161_amd import synth
     m, n, r = synth.SHAPES["attn4096"]
     lin = synth.make_linear(1000, m, n, r, args.batch)
-    oracle.forward(m, n, r, lin.Bu, lin.Bv, lin.s_out, lin.s_mid, lin.s_in, lin.x)  # warm
-    calls, t0 = 0, time.perf_counter()
-    while True:
-        oracle.forward(m, n, r, lin.Bu, lin.Bv, lin.s_out, lin.s_mid, lin.s_in, lin.x)
-        calls += 1
-        el = time.perf_counter() - t0
-        if el >= args.cpu_seconds:
-            break
-    return dict(value=el / calls * 1e6, unit="us/layer", cores=oracle.num_threads(),
-                kind="oracle",
+
+    def timed(seconds):
+        oracle.forward(m, n, r, lin.Bu, lin.Bv, lin.s_out, lin.s_mid, lin.s_in, lin.x)  # warm
+        calls, t0 = 0, time.perf_counter()
+        while True:
+            oracle.forward(m, n, r, lin.Bu, lin.Bv, lin.s_out, lin.s_mid, lin.s_in, lin.x)
+            calls += 1
+            el = time.perf_counter() - t0
+            if el >= seconds:
+                return calls, el
+    threads = oracle.num_threads()
+    calls, el = timed(args.cpu_seconds * 0.6)
+    oracle.set_num_threads(1)
+    try:
+        calls1, el1 = timed(args.cpu_seconds * 0.4)
+    finally:
+        oracle.set_num_threads(threads)
+    return dict(value=el / calls * 1e6, unit="us/layer", cores=threads, kind="oracle",
+                cpu_model=cpu_model(), value_1_thread=el1 / calls1 * 1e6,
                 sample=f"{calls} full fp64 forward calls of the 4096x4096 r=2016 b={args.batch} "
-                       f"layer in {el:.1f} s")
+                       f"layer in {el:.1f} s with {threads} threads; {calls1} calls in "
+                       f"{el1:.1f} s with 1 thread")
 
 
 def main():
@@ -625,7 +780,10 @@ def main():
 
     from paper_2609_06161_amd import synth
     m, n, r = synth.SHAPES["attn4096"]
-    g = decode_time(args, torch, stream, m, n, r, args.batch, 1000, args.steps)
+    g = decode_time(args, torch, stream, m, n, r, args.batch, 1000, args.steps,
+                    exact_steps=(args.steps, args.warmup))
+    # steady state: whole passes over the weight pool (the requested step
+    # count rounded up to whole passes), graph-replayed back to back
     g["ms_per_step"] = g["us_graph"] * 1e-3
     us = g["us_graph"]
     achieved = g["alg_bytes"] / (g["ms_per_step"] * 1e-3) / 1e9
@@ -646,7 +804,12 @@ def main():
                                f"(1.0 BPW, fp16 scales, bf16 x/y), weights rotated over "
                                f"{g['pool']} distinct layers ({g['pool_mb']:.0f} MB)",
                    "m": g["m"], "n": g["n"], "r": g["r"], "batch": g["b"],
-                   "timing": "hip graph of one pass over the weight pool, replayed",
+                   "timing": "HIP graph of one pass over the weight pool (two launches per "
+                             "layer), replayed back to back; the requested step count is "
+                             "rounded up to whole passes (steps = layers timed)",
+                   "steps_requested": args.steps,
+                   "us_per_layer_exact_requested_steps_one_replay": round(
+                       g["exact_ms"] * 1e3 / g["exact_steps"], 3),
                    "us_per_layer_p10_p50_p90": [round(g["us_graph_p10"], 3),
                                                 round(g["us_graph_p50"], 3),
                                                 round(g["us_graph_p90"], 3)],
@@ -660,6 +823,12 @@ def main():
     if not args.no_decode_table and args.only == "all":
         result["decode_table"] = bench_decode_table(args, torch, stream)
         result["decode_stack_8b"] = bench_stack(args, torch, stream)
+        result["decode_layer_stream"] = bench_layer_stream(args, torch, stream)
+        dense = bench_dense_decode(args, torch, stream, us)
+        dense["stack_af1_fused_speedup_vs_dense_bf16"] = round(
+            dense["stack_dense_bf16_us_per_decoder_layer"] /
+            result["decode_stack_8b"]["us_per_decoder_layer_fused_projections"], 3)
+        result["decode_dense_bf16_context"] = dense
     if args.only == "all":
         result["pack_16384x16384"] = bench_pack(args, torch, stream)
     if not args.no_gemm and args.only == "all":
