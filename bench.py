@@ -69,6 +69,9 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=10.0)
     p.add_argument("--only", choices=("all", "gemv", "gemm", "train", "nabf"), default="all",
                    help="profiling aid: run one part only")
+    p.add_argument("--shape", default="attn4096",
+                   help="profiling aid (with --only gemv): the decode shape to time, one of "
+                        "the decode table's names")
     p.add_argument("--calibrate-copy", action="store_true",
                    help="profiling aid: first run a 64 MiB device copy five times, the "
                         "known-size reference for scaling hardware byte counters")
@@ -756,6 +759,10 @@ def main():
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the "
               "multi-GPU sharding of this layer is described but not built.", file=sys.stderr)
         sys.exit(2)
+    if args.shape != "attn4096" and args.only != "gemv":
+        print("--shape applies to --only gemv (the headline is the 4096x4096 layer)",
+              file=sys.stderr)
+        sys.exit(2)
     import torch
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
@@ -778,8 +785,7 @@ def main():
         print(json.dumps({"nabf": bench_nabf(args, torch, stream)}), flush=True)
         return
 
-    from paper_2609_06161_amd import synth
-    m, n, r = synth.SHAPES["attn4096"]
+    m, n, r = shape_of(args.shape)
     g = decode_time(args, torch, stream, m, n, r, args.batch, 1000, args.steps,
                     exact_steps=(args.steps, args.warmup))
     # steady state: whole passes over the weight pool (the requested step

@@ -62,7 +62,11 @@ constexpr int kThreads = kWaves * 64;
 constexpr int kTileRows = 16;        // MFMA M
 constexpr int kGroupWords = 8;       // one 8-byte load per lane covers 16 rows x 8 words
 constexpr int kMaxGroups = 8;        // groups per wave (single pass)
-constexpr int kSlot = 144;           // LDS bytes per (batch row, word): 64 hi + 64 lo + 16 pad
+// LDS bytes per (batch row, word): for each half h of the word's 16 pairs,
+// 32 bytes of hi then 32 of lo, then 16 bytes of pad.  A staging unit (one
+// half) is 64 contiguous bytes, so the units of consecutive lanes (word w,
+// half h at 9w + 4h sixteen-byte lines) never share a bank group.
+constexpr int kSlot = 144;
 
 // LDS bytes between the staged slots of consecutive batch rows: the words
 // of one row, plus 16 bytes when needed to make the stride an odd multiple
@@ -72,7 +76,11 @@ __host__ __device__ constexpr int row_stride(int w_count) {
   return w_count * kSlot + ((w_count & 1) ? 0 : 16);
 }
 constexpr int kLdsBudget = 160 * 1024;  // LDS of one gfx950 compute unit
-constexpr int kRedBytes = kWaves * 64 * 16;
+// Cross-wave sums: each wave's 64 lanes x 16 bytes, one 16-byte pad after
+// every 16 lanes, so that the 4 rows x 16 columns read by consecutive
+// output threads spread over the banks.
+constexpr int kRedLanes = 68;
+constexpr int kRedBytes = kWaves * kRedLanes * 16;
 constexpr int kMaxOutPerThread = 4;  // outputs (row, batch row) written per thread
 constexpr int kMaxSlabsLoaded = 8;   // partial sums loaded at once by the last slab
 constexpr int kDeviceScope = 16;     // buffer cache policy sc1: coherent across XCDs
@@ -193,10 +201,10 @@ __device__ __forceinline__ void store_unit(uint8_t *slot_base, int h, const floa
     lo[d] = pack_bf16x2(v[d] - bf16_to_f32(hi[d] & 0xffffu), v[8 + d] - bf16_to_f32(hi[d] >> 16));
   }
   uint4 *slot = reinterpret_cast<uint4 *>(slot_base);
-  slot[2 * h] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
-  slot[2 * h + 1] = make_uint4(hi[4], hi[5], hi[6], hi[7]);
-  slot[4 + 2 * h] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
-  slot[4 + 2 * h + 1] = make_uint4(lo[4], lo[5], lo[6], lo[7]);
+  slot[4 * h] = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+  slot[4 * h + 1] = make_uint4(hi[4], hi[5], hi[6], hi[7]);
+  slot[4 * h + 2] = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+  slot[4 * h + 3] = make_uint4(lo[4], lo[5], lo[6], lo[7]);
 }
 
 // Output modes of a stage launch.
@@ -415,7 +423,7 @@ __device__ __forceinline__ void stage_body(
         const int wl = (R.cw + R.wpt * (c0 + i)) * kGroupWords + (rem >> 1);
         const int col = (w_begin + wl) * 32 + 8 * (rem & 1) + 2 * qq;
         const bool valid = wl < w_count;
-        dst_off[i] = valid ? wl * kSlot + 32 * (rem & 1) + 8 * qq : -1;
+        dst_off[i] = valid ? wl * kSlot + 64 * (rem & 1) + 8 * qq : -1;
         if constexpr (kInX) {
           const int xo = valid ? col * 2 : kOob;
           ra[i][0] = __builtin_amdgcn_raw_buffer_load_b32(xres, xo, 0, kInAux);
@@ -460,9 +468,9 @@ __device__ __forceinline__ void stage_body(
             pack_bf16x2(v[0] - bf16_to_f32(h0 & 0xffffu), v[2] - bf16_to_f32(h0 >> 16));
         const uint32_t l1 =
             pack_bf16x2(v[1] - bf16_to_f32(h1 & 0xffffu), v[3] - bf16_to_f32(h1 >> 16));
-        uint8_t *dst = dst_off[i] >= 0 ? xs + dst_off[i] : junk + 32 * (rem & 1) + 8 * qq;
+        uint8_t *dst = dst_off[i] >= 0 ? xs + dst_off[i] : junk + 64 * (rem & 1) + 8 * qq;
         *reinterpret_cast<uint2 *>(dst) = make_uint2(h0, h1);
-        *reinterpret_cast<uint2 *>(dst + 64) = make_uint2(l0, l1);
+        *reinterpret_cast<uint2 *>(dst + 32) = make_uint2(l0, l1);
       }
       }
     } else {
@@ -565,11 +573,17 @@ __device__ __forceinline__ void stage_body(
 #pragma unroll
     for (int hl = 0; hl < kChains; ++hl) acc[t][hl] = floatx4{0.f, 0.f, 0.f, 0.f};
   const bool b_lane = beta < b;
+  // LDS offset of B operand k = 4 * hl + t (pair quad t of the hi or lo part)
+  // within a slot: quads 0, 1 are half 0 and quads 2, 3 half 1
+  auto b_off = [](int k) {
+    const int hl = kHiLoCols ? 0 : (k >> 2), t = k & 3;
+    return 16 * (4 * (t >> 1) + 2 * hl + (t & 1));
+  };
   // the products of the wave's groups c0 .. c0 + kMaxGroups - 1 (sign words w)
   auto products = [&](const u32x2 (&w)[kMaxGroups], int c0, int nsteps) {
     auto b_ptr = [&](int st) -> const uint8_t * {
       const int wl = (R.cw + R.wpt * (c0 + (st >> 1))) * kGroupWords + 2 * q + (st & 1);
-      return wl < w_count ? xs + (size_t)beta * row_stride(w_count) + wl * kSlot + 64 * hl_col
+      return wl < w_count ? xs + (size_t)beta * row_stride(w_count) + wl * kSlot + 32 * hl_col
                           : lds;
     };
     uint4 bop[2][kReads];
@@ -578,7 +592,7 @@ __device__ __forceinline__ void stage_body(
     if (nsteps > 0 && b_lane) {
       const uint8_t *bs = b_ptr(0);
 #pragma unroll
-      for (int k = 0; k < kReads; ++k) bop[0][k] = *reinterpret_cast<const uint4 *>(bs + 16 * k);
+      for (int k = 0; k < kReads; ++k) bop[0][k] = *reinterpret_cast<const uint4 *>(bs + b_off(k));
     }
     static_for<kMaxGroups * 2>([&](auto ST) {
       constexpr int st = decltype(ST)::value;
@@ -588,7 +602,7 @@ __device__ __forceinline__ void stage_body(
           const uint8_t *bs = b_ptr(st + 1);
 #pragma unroll
           for (int k = 0; k < kReads; ++k)
-            bop[cur ^ 1][k] = *reinterpret_cast<const uint4 *>(bs + 16 * k);
+            bop[cur ^ 1][k] = *reinterpret_cast<const uint4 *>(bs + b_off(k));
         }
         const uint32_t wd = w[st >> 1][st & 1];
 #pragma unroll
@@ -635,7 +649,7 @@ __device__ __forceinline__ void stage_body(
   //    With red_off > 0 the tiles go to their own LDS region past the staged
   //    input, and only one barrier is needed.
   if (red_off == 0) __syncthreads();  // uniform
-  reinterpret_cast<float4 *>(lds + red_off)[wave * 64 + lane] =
+  reinterpret_cast<float4 *>(lds + red_off)[wave * kRedLanes + lane + (lane >> 4)] =
       make_float4(tot[0], tot[1], tot[2], tot[3]);
   __syncthreads();
   const float *redf = reinterpret_cast<const float *>(lds + red_off);
@@ -655,8 +669,9 @@ __device__ __forceinline__ void stage_body(
       for (int c = 0; c < kWaves; ++c) {
         if (c >= R.wpt) break;
         const int wv2 = rt * R.wpt + c;
-        sum[k] += redf[(wv2 * 64 + l0) * 4 + (orow_l & 3)];
-        if constexpr (kHiLoCols) sum[k] += redf[(wv2 * 64 + l0 + 1) * 4 + (orow_l & 3)];
+        const int ri = (wv2 * kRedLanes + l0 + (l0 >> 4)) * 4 + (orow_l & 3);
+        sum[k] += redf[ri];
+        if constexpr (kHiLoCols) sum[k] += redf[ri + 4];  // column l0 + 1, same 16 lanes
       }
     }
   }
