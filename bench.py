@@ -34,8 +34,8 @@ POOL_BYTES = 512 << 20          # > 2 x 256 MB MALL
 # the source hash differs.
 GEMV_TRAFFIC = {"sources": ("paper_2609_06161_amd/csrc/af1_gemv.hip",
                             "paper_2609_06161_amd/csrc/af1_device.h"),
-                "sha256": "4d444f6c6528d26dd01e7dedab272ac03fbf52066bb524e759818d0f07e6a3d8",
-                "bytes_per_call": 2784727}
+                "sha256": "263dd9d384cb3a7830162d5c1c8a45288320b00f15ca5758cacee40b6d42414d",
+                "bytes_per_call": 2845047}
 
 
 def measured_gemv_traffic():
