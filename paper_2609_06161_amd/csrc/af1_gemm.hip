@@ -235,8 +235,8 @@ __device__ __forceinline__ int saved_v_shift(const float *__restrict__ tinfo, in
 //  2. p = x 2^e1 s_in: the largest |p| and sum |p|, which give e2;
 //  3. xp = fp16(p 2^e2), e_t = e1 + e2.
 // Rows of up to 2048 units (1024 threads, two units each) are loaded once
-// (x and s_in together) and kept in registers through the three steps;
-// wider rows are read again.
+// and kept in registers through the three steps (prep_stream_kernel); wider
+// rows are read three times (prep_kernel, the later passes hit the caches).
 // Block T stores max |s_mid| instead.  A unit is 16 columns: 8 columns
 // c .. c+7 and their partners c+16 .. c+23, which become the pair dwords
 // 8h .. 8h+7 of their group.
@@ -267,6 +267,48 @@ __device__ __forceinline__ void block_sum_max(float &sum, float &mx, float *red)
   sum = red[0];
   mx = red[16];
   for (int w = 1; w < waves; ++w) {
+    sum += red[w];
+    mx = fmaxf(mx, red[16 + w]);
+  }
+}
+
+// The same reduction for workgroups that keep global loads in flight across
+// it (the next token's prefetch): the barriers wait for LDS operations only,
+// and the lanes are combined by DPP within 16-lane rows, then the four rows
+// through lanes 0, 16, 32, 48 (a fixed order).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+template <int kCtrl>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), kCtrl, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float lane_f32(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+template <int kWaves>
+__device__ __forceinline__ void block_sum_max_async(float &sum, float &mx, float *red) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  sum += dpp_f32<0xB1>(sum);
+  mx = fmaxf(mx, dpp_f32<0xB1>(mx));
+  sum += dpp_f32<0x4E>(sum);
+  mx = fmaxf(mx, dpp_f32<0x4E>(mx));
+  sum += dpp_f32<0x124>(sum);
+  mx = fmaxf(mx, dpp_f32<0x124>(mx));
+  sum += dpp_f32<0x128>(sum);
+  mx = fmaxf(mx, dpp_f32<0x128>(mx));
+  sum = (lane_f32(sum, 0) + lane_f32(sum, 16)) + (lane_f32(sum, 32) + lane_f32(sum, 48));
+  mx = fmaxf(fmaxf(lane_f32(mx, 0), lane_f32(mx, 16)), fmaxf(lane_f32(mx, 32), lane_f32(mx, 48)));
+  lds_barrier();  // red may still be read from a previous call
+  if (lane == 0) {
+    red[wave] = sum;
+    red[16 + wave] = mx;
+  }
+  lds_barrier();
+  sum = red[0];
+  mx = red[16];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) {
     sum += red[w];
     mx = fmaxf(mx, red[16 + w]);
   }
@@ -336,11 +378,8 @@ __device__ __forceinline__ uint32_t unit_maxbits(const u32x4 &lo, const u32x4 &h
   return mb;
 }
 
-// kU > 0: the row's units (at most kU per thread) stay in registers, and x
-// and s_in are loaded once, together, before the first reduction.  kU = 0:
-// any width, three passes over the row (the second and third hit the caches).
-template <int kU, int kThreads>
-__global__ __launch_bounds__(kThreads) void prep_kernel(
+// Any row width: three passes over the row, one token a workgroup.
+__global__ __launch_bounds__(256) void prep_kernel(
     const uint16_t *__restrict__ x, const uint16_t *__restrict__ s_in,
     uint16_t *__restrict__ xp, int T, int K, float *__restrict__ tinfo,
     const uint16_t *__restrict__ s_mid, int r) {
@@ -352,86 +391,139 @@ __global__ __launch_bounds__(kThreads) void prep_kernel(
   }
   const int units = K / 16;
   const uint16_t *row = x + (size_t)t * K;
+  uint32_t mb = 0;
+  for (int u = threadIdx.x; u < units; u += 256) {
+    u32x4 lo, hi;
+    load_x_unit(row, unit_col(u), lo, hi);
+    mb = max(mb, unit_maxbits(lo, hi));
+  }
+  float sum = 0.f, mx = __uint_as_float(mb);  // a non-negative pattern orders as its value
+  block_sum_max(sum, mx, red);
+  const int e1 = prep_e1(__float_as_uint(mx));
   float l1 = 0.f, pmax = 0.f;
-  int e1, e2;
-  if constexpr (kU > 0) {
-    u32x4 xl[kU], xh[kU], sl[kU], sh[kU];
+  for (int u = threadIdx.x; u < units; u += 256) {
+    const int c = unit_col(u);
+    u32x4 lo, hi;
+    load_x_unit(row, c, lo, hi);
+    float v[16];
+    prep_values(lo, hi, *reinterpret_cast<const u32x4 *>(s_in + c),
+                *reinterpret_cast<const u32x4 *>(s_in + c + 16), e1, v);
 #pragma unroll
-    for (int i = 0; i < kU; ++i) {
-      const int u = threadIdx.x + kThreads * i;
-      if (u < units) {
-        const int c = unit_col(u);
-        load_x_unit(row, c, xl[i], xh[i]);
-        sl[i] = *reinterpret_cast<const u32x4 *>(s_in + c);
-        sh[i] = *reinterpret_cast<const u32x4 *>(s_in + c + 16);
-      } else {
-        xl[i] = xh[i] = sl[i] = sh[i] = u32x4{0u, 0u, 0u, 0u};
-      }
+    for (int k = 0; k < 16; ++k) {
+      pmax = fmaxf(pmax, fabsf(v[k]));
+      l1 += fabsf(v[k]);
     }
-    uint32_t mb = 0;
-#pragma unroll
-    for (int i = 0; i < kU; ++i) mb = max(mb, unit_maxbits(xl[i], xh[i]));
-    {
-      float sum = 0.f, mx = __uint_as_float(mb);  // a non-negative pattern orders as its value
-      block_sum_max(sum, mx, red);
-      e1 = prep_e1(__float_as_uint(mx));
-    }
-    float v[kU][16];
-#pragma unroll
-    for (int i = 0; i < kU; ++i) {
-      prep_values(xl[i], xh[i], sl[i], sh[i], e1, v[i]);
-#pragma unroll
-      for (int k = 0; k < 16; ++k) {
-        pmax = fmaxf(pmax, fabsf(v[i][k]));
-        l1 += fabsf(v[i][k]);
-      }
-    }
-    block_sum_max(l1, pmax, red);
-    e2 = prep_e2(pmax);
-#pragma unroll
-    for (int i = 0; i < kU; ++i) {
-      const int u = threadIdx.x + kThreads * i;
-      if (u < units) prep_store(xp, t, K, unit_col(u), v[i], e2);
-    }
-  } else {
-    uint32_t mb = 0;
-    for (int u = threadIdx.x; u < units; u += kThreads) {
-      u32x4 lo, hi;
-      load_x_unit(row, unit_col(u), lo, hi);
-      mb = max(mb, unit_maxbits(lo, hi));
-    }
-    {
-      float sum = 0.f, mx = __uint_as_float(mb);
-      block_sum_max(sum, mx, red);
-      e1 = prep_e1(__float_as_uint(mx));
-    }
-    for (int u = threadIdx.x; u < units; u += kThreads) {
-      const int c = unit_col(u);
-      u32x4 lo, hi;
-      load_x_unit(row, c, lo, hi);
-      float v[16];
-      prep_values(lo, hi, *reinterpret_cast<const u32x4 *>(s_in + c),
-                  *reinterpret_cast<const u32x4 *>(s_in + c + 16), e1, v);
-#pragma unroll
-      for (int k = 0; k < 16; ++k) {
-        pmax = fmaxf(pmax, fabsf(v[k]));
-        l1 += fabsf(v[k]);
-      }
-    }
-    block_sum_max(l1, pmax, red);
-    e2 = prep_e2(pmax);
-    for (int u = threadIdx.x; u < units; u += kThreads) {
-      const int c = unit_col(u);
-      u32x4 lo, hi;
-      load_x_unit(row, c, lo, hi);
-      float v[16];
-      prep_values(lo, hi, *reinterpret_cast<const u32x4 *>(s_in + c),
-                  *reinterpret_cast<const u32x4 *>(s_in + c + 16), e1, v);
-      prep_store(xp, t, K, c, v, e2);
-    }
+  }
+  block_sum_max(l1, pmax, red);
+  const int e2 = prep_e2(pmax);
+  for (int u = threadIdx.x; u < units; u += 256) {
+    const int c = unit_col(u);
+    u32x4 lo, hi;
+    load_x_unit(row, c, lo, hi);
+    float v[16];
+    prep_values(lo, hi, *reinterpret_cast<const u32x4 *>(s_in + c),
+                *reinterpret_cast<const u32x4 *>(s_in + c + 16), e1, v);
+    prep_store(xp, t, K, c, v, e2);
   }
   if (threadIdx.x == 0)
     reinterpret_cast<float2 *>(tinfo)[t] = make_float2(ldexpf(l1, e2), __int_as_float(e1 + e2));
+}
+
+// The same preparation for rows of up to kU * kThreads units, persistent:
+// workgroup w < W takes tokens w, w + W, w + 2W, ... and loads the next
+// token's row while it reduces and stores the current one, so the row loads
+// and the xp stores of different tokens overlap.  s_in is loaded once.  The
+// two row buffers alternate in a loop unrolled by two (the first pair
+// peeled, so the loop is entered with the same memory operations in flight
+// as it is repeated with); a thread whose unit index passes the row's end
+// holds a copy of the row's last unit, kept out of the reductions and
+// stored back unchanged, so that no load or store sits in a branch.  The
+// arithmetic and the order of each token's results are those of
+// prep_kernel except the order in which the reductions add.  Workgroup W
+// stores max |s_mid|.
+template <int kU>
+struct PrepRow {
+  u32x4 lo[kU], hi[kU];
+};
+
+template <int kU, int kThreads>
+__device__ __forceinline__ void prep_row_load(const uint16_t *__restrict__ x, int t, int K,
+                                              int units, PrepRow<kU> &b) {
+  const uint16_t *row = x + (size_t)t * K;
+#pragma unroll
+  for (int i = 0; i < kU; ++i)
+    load_x_unit(row, unit_col(min((int)threadIdx.x + kThreads * i, units - 1)), b.lo[i], b.hi[i]);
+}
+
+template <int kU, int kThreads>
+__device__ __forceinline__ void prep_row_token(const PrepRow<kU> &b, const u32x4 (&sl)[kU],
+                                               const u32x4 (&sh)[kU], uint16_t *__restrict__ xp,
+                                               float *__restrict__ tinfo, int t, int K,
+                                               int units, float *red) {
+  uint32_t mb = 0;
+#pragma unroll
+  for (int i = 0; i < kU; ++i) {
+    const uint32_t m = unit_maxbits(b.lo[i], b.hi[i]);
+    mb = max(mb, (int)threadIdx.x + kThreads * i < units ? m : 0u);
+  }
+  float sum = 0.f, mx = __uint_as_float(mb);
+  block_sum_max_async<kThreads / 64>(sum, mx, red);
+  const int e1 = prep_e1(__float_as_uint(mx));
+  float v[kU][16], l1 = 0.f, pmax = 0.f;
+#pragma unroll
+  for (int i = 0; i < kU; ++i) {
+    prep_values(b.lo[i], b.hi[i], sl[i], sh[i], e1, v[i]);
+    const float keep = (int)threadIdx.x + kThreads * i < units ? 1.f : 0.f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      pmax = fmaxf(pmax, keep * fabsf(v[i][k]));
+      l1 += keep * fabsf(v[i][k]);
+    }
+  }
+  block_sum_max_async<kThreads / 64>(l1, pmax, red);
+  const int e2 = prep_e2(pmax);
+#pragma unroll
+  for (int i = 0; i < kU; ++i)
+    prep_store(xp, t, K, unit_col(min((int)threadIdx.x + kThreads * i, units - 1)), v[i], e2);
+  // every lane stores the token's record (the same value, one write a wave)
+  reinterpret_cast<float2 *>(tinfo)[t] = make_float2(ldexpf(l1, e2), __int_as_float(e1 + e2));
+}
+
+template <int kU, int kThreads>
+__global__ __launch_bounds__(kThreads) void prep_stream_kernel(
+    const uint16_t *__restrict__ x, const uint16_t *__restrict__ s_in,
+    uint16_t *__restrict__ xp, int T, int K, float *__restrict__ tinfo,
+    const uint16_t *__restrict__ s_mid, int r) {
+  __shared__ float red[32];
+  const int W = (int)gridDim.x - 1;
+  if ((int)blockIdx.x == W) {
+    prep_smax(s_mid, r, T, tinfo, red);
+    return;
+  }
+  const int units = K / 16;
+  u32x4 sl[kU], sh[kU];
+#pragma unroll
+  for (int i = 0; i < kU; ++i) {
+    const int c = unit_col(min((int)threadIdx.x + kThreads * i, units - 1));
+    sl[i] = *reinterpret_cast<const u32x4 *>(s_in + c);
+    sh[i] = *reinterpret_cast<const u32x4 *>(s_in + c + 16);
+  }
+  PrepRow<kU> a, b;
+  int t = blockIdx.x;  // < T: the grid has at most T workers
+  prep_row_load<kU, kThreads>(x, t, K, units, a);
+  prep_row_load<kU, kThreads>(x, min(t + W, T - 1), K, units, b);
+  prep_row_token<kU, kThreads>(a, sl, sh, xp, tinfo, t, K, units, red);
+  t += W;
+  if (t >= T) return;
+  prep_row_load<kU, kThreads>(x, min(t + W, T - 1), K, units, a);
+  prep_row_token<kU, kThreads>(b, sl, sh, xp, tinfo, t, K, units, red);
+  for (t += W; t < T; t += 2 * W) {
+    prep_row_load<kU, kThreads>(x, min(t + W, T - 1), K, units, b);
+    prep_row_token<kU, kThreads>(a, sl, sh, xp, tinfo, t, K, units, red);
+    if (t + W >= T) break;
+    prep_row_load<kU, kThreads>(x, min(t + 2 * W, T - 1), K, units, a);
+    prep_row_token<kU, kThreads>(b, sl, sh, xp, tinfo, t + W, K, units, red);
+  }
 }
 
 // C = rowscale * (A_pairorder x sign(W)^T), in the forms listed under Mode.
@@ -1469,6 +1561,11 @@ hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *
   return hipGetLastError();
 }
 
+// Worker waves of the preparation a compute unit: with a row and the next
+// one in registers (107 to 126 VGPRs) the register file holds four waves a
+// SIMD.
+constexpr int kPrepWavesPerCU = 16;
+
 // fp16(s_in .* x 2^e_t) in pair order, the A operand of G1, and the
 // per-token range-guard record (see prep_kernel).
 hipError_t prepare_forward(int64_t n, const uint16_t *s_in, const uint16_t *x, int64_t T,
@@ -1476,17 +1573,29 @@ hipError_t prepare_forward(int64_t n, const uint16_t *s_in, const uint16_t *x, i
                            hipStream_t s) {
   // a row in registers: at most two units a thread, 256 to 1024 threads
   const int64_t units = n / 16;
-  const dim3 g((unsigned)(T + 1));
+  if (T == 0) {
+    prep_kernel<<<1, 256, 0, s>>>(x, s_in, xp, 0, (int)n, tinfo, s_mid, (int)r);
+    return hipGetLastError();
+  }
+  const auto grid = [&](int threads) {
+    const int64_t w = (int64_t)device_cus() * std::max(1, kPrepWavesPerCU * 64 / threads);
+    return dim3((unsigned)(std::min<int64_t>(T, w) + 1));
+  };
   if (units <= 256)
-    prep_kernel<1, 256><<<g, 256, 0, s>>>(x, s_in, xp, (int)T, (int)n, tinfo, s_mid, (int)r);
+    prep_stream_kernel<1, 256><<<grid(256), 256, 0, s>>>(x, s_in, xp, (int)T, (int)n, tinfo,
+                                                          s_mid, (int)r);
   else if (units <= 512)
-    prep_kernel<2, 256><<<g, 256, 0, s>>>(x, s_in, xp, (int)T, (int)n, tinfo, s_mid, (int)r);
+    prep_stream_kernel<2, 256><<<grid(256), 256, 0, s>>>(x, s_in, xp, (int)T, (int)n, tinfo,
+                                                          s_mid, (int)r);
   else if (units <= 1024)
-    prep_kernel<2, 512><<<g, 512, 0, s>>>(x, s_in, xp, (int)T, (int)n, tinfo, s_mid, (int)r);
+    prep_stream_kernel<2, 512><<<grid(512), 512, 0, s>>>(x, s_in, xp, (int)T, (int)n, tinfo,
+                                                          s_mid, (int)r);
   else if (units <= 2048)
-    prep_kernel<2, 1024><<<g, 1024, 0, s>>>(x, s_in, xp, (int)T, (int)n, tinfo, s_mid, (int)r);
+    prep_stream_kernel<2, 1024><<<grid(1024), 1024, 0, s>>>(x, s_in, xp, (int)T, (int)n, tinfo,
+                                                             s_mid, (int)r);
   else
-    prep_kernel<0, 256><<<g, 256, 0, s>>>(x, s_in, xp, (int)T, (int)n, tinfo, s_mid, (int)r);
+    prep_kernel<<<dim3((unsigned)(T + 1)), 256, 0, s>>>(x, s_in, xp, (int)T, (int)n, tinfo,
+                                                        s_mid, (int)r);
   return hipGetLastError();
 }
 

@@ -208,3 +208,18 @@ def test_gemm_wide_rows_scaled(oracle, n, T):
     lin = synth.make_linear(4800 + n, m, n, r, T)
     x = scaled_x(lin.x, token_factors(4801, T))
     check(oracle, lin, x, run("gemm", lin, x))
+
+
+@pytest.mark.parametrize("n,T", [(4096, 3077), (8192, 4101), (16384, 1800), (24576, 900)],
+                         ids=["units256", "units512", "units1024", "units1536"])
+def test_gemm_prep_several_tokens_per_worker(oracle, n, T):
+    """The persistent preparation (one row in registers, the next one
+    loading) at token counts where each worker takes three to five tokens
+    and the last round is ragged (on 256 compute units: 1024, 1024, 512 and
+    256 workers for these widths), with token scales spanning 10^12 so that
+    a token prepared with another token's range-guard shift fails.  Every
+    token against the oracle."""
+    m, r = 96, 64
+    lin = synth.make_linear(4900 + n, m, n, r, T)
+    x = scaled_x(lin.x, token_factors(4901 + n, T))
+    check(oracle, lin, x, run("gemm", lin, x))
