@@ -314,11 +314,34 @@ __device__ __forceinline__ void block_sum_max_async(float &sum, float &mx, float
   }
 }
 
+// The largest |s_mid[k]| over this thread's share of the r entries (r a
+// multiple of 8, s_mid 16-byte aligned): 16-byte loads, eight in flight per
+// round, so a rank of up to 64 * threads entries costs one memory round trip
+// (a load per entry and iteration would wait for each in turn: r / threads
+// round trips).
+__device__ __forceinline__ float smid_absmax_part(const uint16_t *__restrict__ s_mid, int r,
+                                                  int threads) {
+  float mx = 0.f;
+  for (int c0 = (int)threadIdx.x * 8; c0 < r; c0 += 64 * threads) {
+    u32x4 v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int c = c0 + 8 * threads * q;
+      v[q] = c < r ? *reinterpret_cast<const u32x4 *>(s_mid + c) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        mx = fmaxf(mx, fmaxf(fabsf(f16_lo(v[q][e])), fabsf(f16_hi(v[q][e]))));
+  }
+  return mx;
+}
+
 // Block T: max |s_mid| into tinfo[2T].
 __device__ __forceinline__ void prep_smax(const uint16_t *__restrict__ s_mid, int r, int T,
                                           float *__restrict__ tinfo, float *red) {
-  float sum = 0.f, mx = 0.f;
-  for (int k = threadIdx.x; k < r; k += blockDim.x) mx = fmaxf(mx, fabsf(f16_to_f32(s_mid[k])));
+  float sum = 0.f, mx = smid_absmax_part(s_mid, r, (int)blockDim.x);
   block_sum_max(sum, mx, red);
   if (threadIdx.x == 0) tinfo[2 * T] = mx;
 }
@@ -952,7 +975,7 @@ __global__ __launch_bounds__(256) void bwd_rowstat_kernel(const uint16_t *__rest
   const int t = blockIdx.x;
   float mx = 0.f, l1 = 0.f;
   if (t == T) {
-    for (int k = threadIdx.x; k < r; k += 256) mx = fmaxf(mx, fabsf(f16_to_f32(s_mid[k])));
+    mx = smid_absmax_part(s_mid, r, 256);
   } else {
     const uint16_t *row = dy + (size_t)t * m;
     for (int c0 = threadIdx.x * 8; c0 < m; c0 += 4 * 2048) {
