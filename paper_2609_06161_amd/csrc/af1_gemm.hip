@@ -1184,19 +1184,84 @@ __global__ __launch_bounds__(256) void bwd_finish_kernel(
   }
 }
 
+// Adds the S fp32 partials of two float4 runs (columns cl and ch of row
+// base, partial s at base + s * stride) in split order.  The loads of a
+// batch are all issued before any add: indices past S load the last
+// partial again and add zero (an add of +0 leaves a sum that started at +0
+// unchanged), so no branch sits between a load and the next one (behind a
+// conditional add the compiler moves each load next to its use, one memory
+// round trip per split).  The launch picks the batch from S (4, 8 or 16):
+// a batch far above S would load the last partial many times over and hold
+// registers that limit the waves in flight.
+template <int kBatch>
+__device__ __forceinline__ void sum_partials(const float *__restrict__ base, size_t stride, int S,
+                                             int cl, int ch, float4 &lo, float4 &hi) {
+  lo = make_float4(0.f, 0.f, 0.f, 0.f);
+  hi = lo;
+  for (int s0 = 0; s0 < S; s0 += kBatch) {
+    float4 a[kBatch], b[kBatch];
+#pragma unroll
+    for (int q = 0; q < kBatch; ++q) {
+      const int sp = min(s0 + q, S - 1);
+      a[q] = *reinterpret_cast<const float4 *>(base + (size_t)sp * stride + cl);
+      b[q] = *reinterpret_cast<const float4 *>(base + (size_t)sp * stride + ch);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int q = 0; q < kBatch; ++q) {
+      const bool use = s0 + q < S;
+      lo.x += use ? a[q].x : 0.f;
+      lo.y += use ? a[q].y : 0.f;
+      lo.z += use ? a[q].z : 0.f;
+      lo.w += use ? a[q].w : 0.f;
+      hi.x += use ? b[q].x : 0.f;
+      hi.y += use ? b[q].y : 0.f;
+      hi.z += use ? b[q].z : 0.f;
+      hi.w += use ? b[q].w : 0.f;
+    }
+  }
+}
+
+// What finish8 reads besides the sums: the token's range-guard record and
+// max |s_mid| (kRecord; the kBwdIn reduction has no record and passes no
+// tinfo), and the row scales of the 8 positions (cl .. cl+3 and ch .. ch+3,
+// each run 8-byte aligned).  Loaded before the partial sums and kept raw
+// (nothing computed from them until the sums have arrived), so that their
+// round trip overlaps the sums' instead of following it.
+struct Fin8In {
+  float2 ti;
+  float smax;
+  uint2 rlo, rhi;
+};
+template <bool kRecord>
+__device__ __forceinline__ Fin8In finish8_load(int cl, int ch, int t, int T,
+                                               const uint16_t *__restrict__ rowscale,
+                                               const float *__restrict__ tinfo) {
+  Fin8In in;
+  in.ti = make_float2(0.f, 0.f);
+  in.smax = 0.f;
+  if constexpr (kRecord) {
+    in.ti = reinterpret_cast<const float2 *>(tinfo)[t];
+    in.smax = tinfo[2 * T];
+  }
+  in.rlo = *reinterpret_cast<const uint2 *>(rowscale + cl);
+  in.rhi = *reinterpret_cast<const uint2 *>(rowscale + ch);
+  return in;
+}
+
 // The forward modes' outputs for 8 consecutive output positions p .. p+7 of
 // token t from their fp32 sums: lo holds columns cl .. cl+3, hi columns
 // ch .. ch+3 (pair order interleaves the two runs, natural order
 // concatenates them).
 template <int kMode>
-__device__ __forceinline__ void finish8(const float4 &lo, const float4 &hi, int cl, int ch, int p,
-                                        int t, int T, int N, const uint16_t *__restrict__ rowscale,
-                                        uint16_t *__restrict__ C, uint16_t *__restrict__ V,
-                                        float *__restrict__ F, const float *__restrict__ tinfo) {
+__device__ __forceinline__ void finish8(const float4 &lo, const float4 &hi, const Fin8In &in,
+                                        int p, int t, int N, uint16_t *__restrict__ C,
+                                        uint16_t *__restrict__ V, float *__restrict__ F) {
   constexpr bool kPairOut = kMode == kMid || kMode == kMidSave;
   // the token's range-guard shift (see prep_kernel) before any rounding
-  const int sh = fwd_shift<kPairOut>(tinfo, T, t);
-  const int es = kMode == kMidSave ? smax_exp(tinfo[2 * T]) : 0;
+  const int c_t = mid_exp(in.ti.x, in.smax);
+  const int sh = kPairOut ? -c_t : c_t - __float_as_int(in.ti.y);
+  const int es = kMode == kMidSave ? smax_exp(in.smax) : 0;
   const float l4[4] = {ldexpf(lo.x, sh), ldexpf(lo.y, sh), ldexpf(lo.z, sh), ldexpf(lo.w, sh)};
   const float h4[4] = {ldexpf(hi.x, sh), ldexpf(hi.y, sh), ldexpf(hi.z, sh), ldexpf(hi.w, sh)};
   float acc[8];
@@ -1205,18 +1270,20 @@ __device__ __forceinline__ void finish8(const float4 &lo, const float4 &hi, int 
     acc[kPairOut ? 2 * k : k] = l4[k];
     acc[kPairOut ? 2 * k + 1 : 4 + k] = h4[k];
   }
+  // row scales of columns cl .. cl+3 (rs[0..3]) and ch .. ch+3 (rs[4..7])
+  const uint32_t rw[4] = {in.rlo.x, in.rlo.y, in.rhi.x, in.rhi.y};
+  float rs[8];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    rs[2 * k] = f16_lo(rw[k]);
+    rs[2 * k + 1] = f16_hi(rw[k]);
+  }
   uint32_t c[4], v[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    int col0, col1;
-    if (kPairOut) {
-      col0 = cl + k;
-      col1 = ch + k;
-    } else {
-      col0 = p + 2 * k;
-      col1 = p + 2 * k + 1;
-    }
-    const float r0 = f16_to_f32(rowscale[col0]), r1 = f16_to_f32(rowscale[col1]);
+    // pair order: columns (cl + k, ch + k); natural: (p + 2k, p + 2k + 1)
+    // with cl = p, ch = p + 4
+    const float r0 = kPairOut ? rs[k] : rs[2 * k], r1 = kPairOut ? rs[4 + k] : rs[2 * k + 1];
     const float a0 = acc[2 * k] * r0, a1 = acc[2 * k + 1] * r1;
     c[k] = kPairOut ? (uint32_t)f32_to_f16(a0) | ((uint32_t)f32_to_f16(a1) << 16)
                     : (uint32_t)f32_to_bf16(a0) | ((uint32_t)f32_to_bf16(a1) << 16);
@@ -1238,7 +1305,7 @@ __device__ __forceinline__ void finish8(const float4 &lo, const float4 &hi, int 
 // split order.  A thread takes 8 consecutive output positions of one token:
 // in pair order (kMid, kMidSave) positions 8u .. 8u+7 of a 32-column group
 // hold columns c0 .. c0+3 and c0+16 .. c0+19, interleaved.
-template <int kMode>
+template <int kMode, int kBatch>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *__restrict__ P, int S,
                                                             int T, int N,
                                                             const uint16_t *__restrict__ rowscale,
@@ -1260,30 +1327,10 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *__restr
     cl = p;
     ch = p + 4;
   }
-  // The loads of up to kReduceBatch splits are issued before any is added
-  // (one memory round trip per batch, not per split); adds stay in split
-  // order.
-  constexpr int kReduceBatch = 8;
-  float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
-  const size_t split_stride = (size_t)T * N;
-  const float *base = P + (size_t)t * N;
-  for (int s0 = 0; s0 < S; s0 += kReduceBatch) {
-    float4 a[kReduceBatch], b[kReduceBatch];
-#pragma unroll
-    for (int q = 0; q < kReduceBatch; ++q) {
-      const int sp = s0 + q < S ? s0 + q : S - 1;  // clamped: loaded, not added
-      const float *row = base + (size_t)sp * split_stride;
-      a[q] = *reinterpret_cast<const float4 *>(row + cl);
-      b[q] = *reinterpret_cast<const float4 *>(row + ch);
-    }
-#pragma unroll
-    for (int q = 0; q < kReduceBatch; ++q) {
-      if (s0 + q >= S) break;
-      lo.x += a[q].x; lo.y += a[q].y; lo.z += a[q].z; lo.w += a[q].w;
-      hi.x += b[q].x; hi.y += b[q].y; hi.z += b[q].z; hi.w += b[q].w;
-    }
-  }
-  finish8<kMode>(lo, hi, cl, ch, p, t, T, N, rowscale, C, V, F, tinfo);
+  const Fin8In in = finish8_load<true>(cl, ch, t, T, rowscale, tinfo);
+  float4 lo, hi;
+  sum_partials<kBatch>(P + (size_t)t * N, (size_t)T * N, S, cl, ch, lo, hi);
+  finish8<kMode>(lo, hi, in, p, t, N, C, V, F);
 }
 
 // The reduction of a mixed grid (forward modes): for each tile cut into
@@ -1315,22 +1362,30 @@ __global__ __launch_bounds__(256) void mixed_reduce_kernel(const float *__restri
     cl = pl;
     ch = pl + 4;
   }
+  const Fin8In in = finish8_load<true>(n0 + cl, n0 + ch, t, T, rowscale, tinfo);
   float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
   float4 a[4], b[4];
   const float *base = P + (size_t)h * S * (BM * BN) + row * BN;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {  // S <= 4
+  for (int q = 0; q < 4; ++q) {  // S <= 4; past S: the last partial again, added as zero
     const int sp = q < S ? q : S - 1;
     a[q] = *reinterpret_cast<const float4 *>(base + (size_t)sp * (BM * BN) + cl);
     b[q] = *reinterpret_cast<const float4 *>(base + (size_t)sp * (BM * BN) + ch);
   }
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    if (q >= S) break;
-    lo.x += a[q].x; lo.y += a[q].y; lo.z += a[q].z; lo.w += a[q].w;
-    hi.x += b[q].x; hi.y += b[q].y; hi.z += b[q].z; hi.w += b[q].w;
+    const bool use = q < S;
+    lo.x += use ? a[q].x : 0.f;
+    lo.y += use ? a[q].y : 0.f;
+    lo.z += use ? a[q].z : 0.f;
+    lo.w += use ? a[q].w : 0.f;
+    hi.x += use ? b[q].x : 0.f;
+    hi.y += use ? b[q].y : 0.f;
+    hi.z += use ? b[q].z : 0.f;
+    hi.w += use ? b[q].w : 0.f;
   }
-  finish8<kMode>(lo, hi, n0 + cl, n0 + ch, n0 + pl, t, T, N, rowscale, C, V, F, tinfo);
+  finish8<kMode>(lo, hi, in, n0 + pl, t, N, C, V, F);
 }
 
 // The reduction of a split-K backward contraction.  A workgroup takes 64
@@ -1340,13 +1395,12 @@ __global__ __launch_bounds__(256) void mixed_reduce_kernel(const float *__restri
 // the workgroup adds gradient * S over its 64 tokens in token order for the
 // per-tile sums F (one row per 64 tokens).
 constexpr int kBwdReduceCols = 32;
-template <int kMode>
+template <int kMode, int kBatch>
 __global__ __launch_bounds__(256) void splitk_bwd_reduce_kernel(
     const float *__restrict__ P, int S, int T, int N, const uint16_t *__restrict__ rowscale,
     const float *__restrict__ gscale, uint16_t *__restrict__ C, const uint16_t *__restrict__ Sv,
     float *__restrict__ F, const float *__restrict__ tinfo) {
   constexpr bool kPairOut = kMode == kBwdMid;
-  constexpr int kReduceBatch = 8;
   __shared__ float red[64][kBwdReduceCols + 1];
   const int u = threadIdx.x & 3, tk = threadIdx.x >> 2;
   const int tile = blockIdx.y;
@@ -1364,40 +1418,36 @@ __global__ __launch_bounds__(256) void splitk_bwd_reduce_kernel(
 #pragma unroll
   for (int k = 0; k < 8; ++k) g[k] = 0.f;
   if (t < T && p < N) {
-    float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
-    const size_t split_stride = (size_t)T * N;
-    const float *base = P + (size_t)t * N;
-    for (int s0 = 0; s0 < S; s0 += kReduceBatch) {
-      float4 a[kReduceBatch], b[kReduceBatch];
-#pragma unroll
-      for (int q = 0; q < kReduceBatch; ++q) {
-        const int sp = s0 + q < S ? s0 + q : S - 1;  // clamped: loaded, not added
-        a[q] = *reinterpret_cast<const float4 *>(base + (size_t)sp * split_stride + cl);
-        b[q] = *reinterpret_cast<const float4 *>(base + (size_t)sp * split_stride + ch);
-      }
-#pragma unroll
-      for (int q = 0; q < kReduceBatch; ++q) {
-        if (s0 + q >= S) break;
-        lo.x += a[q].x; lo.y += a[q].y; lo.z += a[q].z; lo.w += a[q].w;
-        hi.x += b[q].x; hi.y += b[q].y; hi.z += b[q].z; hi.w += b[q].w;
-      }
-    }
+    // the operands of the epilogue first (their round trip overlaps the sums')
     const float2 gs = reinterpret_cast<const float2 *>(gscale)[t >> 6];
+    const uint4 sq = *reinterpret_cast<const uint4 *>(Sv + (size_t)t * N + p);
+    const Fin8In in = finish8_load<kMode == kBwdMid>(cl, ch, t, T, rowscale, tinfo);
+    float4 lo, hi;
+    sum_partials<kBatch>(P + (size_t)t * N, (size_t)T * N, S, cl, ch, lo, hi);
     const float fg = kMode == kBwdMid ? gs.x : gs.x / gs.y;
     // kBwdMid: S is the saved intermediate at the forward's per-token scale
-    const int vsh = kMode == kBwdMid ? saved_v_shift(tinfo, T, t) : 0;
+    // (saved_v_shift from the prefetched record)
+    const int vsh = kMode == kBwdMid ? mid_exp(in.ti.x, in.smax) - smax_exp(in.smax) -
+                                           __float_as_int(in.ti.y)
+                                     : 0;
+    // row scales of columns cl .. cl+3 (rsv[0..3]) and ch .. ch+3 (rsv[4..7])
+    const uint32_t rw[4] = {in.rlo.x, in.rlo.y, in.rhi.x, in.rhi.y};
+    float rsv[8];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      rsv[2 * k] = f16_lo(rw[k]);
+      rsv[2 * k + 1] = f16_hi(rw[k]);
+    }
     const float l4[4] = {lo.x, lo.y, lo.z, lo.w}, h4[4] = {hi.x, hi.y, hi.z, hi.w};
-    float acc[8];
-    int col[8];
+    float acc[8], rse[8];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       acc[kPairOut ? 2 * k : k] = l4[k];
       acc[kPairOut ? 2 * k + 1 : 4 + k] = h4[k];
-      col[kPairOut ? 2 * k : k] = cl + k;
-      col[kPairOut ? 2 * k + 1 : 4 + k] = ch + k;
+      rse[kPairOut ? 2 * k : k] = rsv[k];          // column cl + k
+      rse[kPairOut ? 2 * k + 1 : 4 + k] = rsv[4 + k];  // column ch + k
     }
     // S is stored like C: fp16 in pair order (kBwdMid), bf16 natural (kBwdIn)
-    const uint4 sq = *reinterpret_cast<const uint4 *>(Sv + (size_t)t * N + p);
     const uint32_t sw[4] = {sq.x, sq.y, sq.z, sq.w};
     uint32_t c[4];
 #pragma unroll
@@ -1409,7 +1459,7 @@ __global__ __launch_bounds__(256) void splitk_bwd_reduce_kernel(
         const uint32_t sbits = h ? sw[k] >> 16 : sw[k] & 0xffffu;
         const float sval = kMode == kBwdMid ? f16_to_f32((uint16_t)sbits) : bf16_to_f32(sbits);
         g[e] = kMode == kBwdMid ? ldexpf(acc[e] * fg * sval, vsh) : acc[e] * fg * sval;
-        const float rs = f16_to_f32(rowscale[col[e]]);
+        const float rs = rse[e];
         o[h] = kMode == kBwdMid ? acc[e] * rs * gs.y : acc[e] * fg * rs;
       }
       c[k] = kMode == kBwdMid
@@ -1568,8 +1618,15 @@ hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *
     if constexpr (kMode == kBwdMid || kMode == kBwdIn) {
       const dim3 gr((unsigned)((N + kBwdReduceCols - 1) / kBwdReduceCols),
                     (unsigned)((T + 63) / 64));
-      splitk_bwd_reduce_kernel<kMode><<<gr, 256, 0, s>>>(P, p.splits, (int)T, (int)N, rs,
-                                                          gscale, C, S, F, tinfo);
+      auto go = [&](auto kernel) {
+        kernel<<<gr, 256, 0, s>>>(P, p.splits, (int)T, (int)N, rs, gscale, C, S, F, tinfo);
+      };
+      if (p.splits <= 4)
+        go(splitk_bwd_reduce_kernel<kMode, 4>);
+      else if (p.splits <= 8)
+        go(splitk_bwd_reduce_kernel<kMode, 8>);
+      else
+        go(splitk_bwd_reduce_kernel<kMode, 16>);
     } else {
       // A reduction that would occupy at most half the compute units with
       // 256-thread blocks runs 64-thread blocks: the partial loads of a few
@@ -1577,8 +1634,16 @@ hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *
       // against 33.7 with 256-thread blocks throughout).
       const int64_t units = T * (N / 8);
       const int rt = (units + 255) / 256 <= device_cus() / 2 ? 64 : 256;
-      splitk_reduce_kernel<kMode><<<(unsigned)((units + rt - 1) / rt), rt, 0, s>>>(
-          P, p.splits, (int)T, (int)N, rs, C, V, F, tinfo);
+      auto go = [&](auto kernel) {
+        kernel<<<(unsigned)((units + rt - 1) / rt), rt, 0, s>>>(P, p.splits, (int)T, (int)N, rs,
+                                                               C, V, F, tinfo);
+      };
+      if (p.splits <= 4)
+        go(splitk_reduce_kernel<kMode, 4>);
+      else if (p.splits <= 8)
+        go(splitk_reduce_kernel<kMode, 8>);
+      else
+        go(splitk_reduce_kernel<kMode, 16>);
     }
   }
   return hipGetLastError();
