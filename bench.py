@@ -34,8 +34,8 @@ POOL_BYTES = 512 << 20          # > 2 x 256 MB MALL
 # the source hash differs.
 GEMV_TRAFFIC = {"sources": ("paper_2609_06161_amd/csrc/af1_gemv.hip",
                             "paper_2609_06161_amd/csrc/af1_device.h"),
-                "sha256": "263dd9d384cb3a7830162d5c1c8a45288320b00f15ca5758cacee40b6d42414d",
-                "bytes_per_call": 2845047}
+                "sha256": "6dbab119a29a29dd51989cf645f31e954fdbf7ecde110a0f82b5e6f9b5191ab7",
+                "bytes_per_call": 2849141}
 
 
 def measured_gemv_traffic():
