@@ -1049,18 +1049,40 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const uint16_t *__restric
   const int c = (ur >> 1) * 32 + 8 * (ur & 1);               // first of its columns
   const int tb = blockIdx.y;
   const bool live = c < m;
-  float so[16];
-  if (live) {
+  const int cl = live ? c : 0;  // loads stay inside the arrays; results unused
+  // Every load is issued before any is waited for: wave 0's group
+  // statistics first (its wait then leaves the rows in flight), then s_out
+  // and the thread's four token rows of dy and z (rows past T load row T-1
+  // again and add nothing), so a block costs one memory round trip.
+  float st_mx = 0.f, st_l1 = 0.f, st_smax = 0.f;
+  const int ts = tb * kPrepTokens + (int)threadIdx.x;
+  if (threadIdx.x < 64) {  // wave-uniform
+    const int tc = min(ts, T - 1);
+    st_mx = tstat[2 * tc];
+    st_l1 = tstat[2 * tc + 1];
+    st_smax = tstat[2 * T];
+  }
+  const u32x4 so_lo = *reinterpret_cast<const u32x4 *>(s_out + cl);
+  const u32x4 so_hi = *reinterpret_cast<const u32x4 *>(s_out + cl + 16);
+  constexpr int kRows = kPrepTokens / 16;
+  u32x4 dlo[kRows], dhi[kRows];
+  float4 zq[kRows][4];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      so[q] = f16_to_f32(s_out[c + q]);
-      so[8 + q] = f16_to_f32(s_out[c + 16 + q]);
-    }
+  for (int q4 = 0; q4 < kRows; ++q4) {
+    const int tc = min(tb * kPrepTokens + ty + 16 * q4, T - 1);
+    const uint16_t *src = dy + (size_t)tc * m + cl;
+    dlo[q4] = *reinterpret_cast<const u32x4 *>(src);
+    dhi[q4] = *reinterpret_cast<const u32x4 *>(src + 16);
+    const float *zr = z + (size_t)tc * m + cl;
+    zq[q4][0] = *reinterpret_cast<const float4 *>(zr);
+    zq[q4][1] = *reinterpret_cast<const float4 *>(zr + 4);
+    zq[q4][2] = *reinterpret_cast<const float4 *>(zr + 16);
+    zq[q4][3] = *reinterpret_cast<const float4 *>(zr + 20);
   }
   // group exponents: wave 0 reduces the 64 tokens' statistics
   if (threadIdx.x < 64) {
-    const int t = tb * kPrepTokens + threadIdx.x;
-    float mx = t < T ? tstat[2 * t] : 0.f;
+    const bool tok = ts < T;
+    float mx = tok ? st_mx : 0.f;
     for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
     int e = 0, c = 0;
     if (mx > 0.f) {
@@ -1068,7 +1090,7 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const uint16_t *__restric
       frexpf(mx, &k);  // mx = f 2^k, f in [0.5, 1)
       e = 14 - k;
       e = e > kExpClamp ? kExpClamp : (e < -kExpClamp ? -kExpClamp : e);
-      float bound = t < T ? ldexpf(tstat[2 * t + 1], e) * tstat[2 * T] : 0.f;
+      float bound = tok ? ldexpf(st_l1, e) * st_smax : 0.f;
       for (int off = 32; off > 0; off >>= 1) bound = fmaxf(bound, __shfl_xor(bound, off, 64));
       frexpf(bound, &k);  // every 2^e L_t < 2^k
       c = k - 14;
@@ -1083,41 +1105,47 @@ __global__ __launch_bounds__(256) void bwd_prep_kernel(const uint16_t *__restric
       }
     }
   }
-  __syncthreads();
+  lds_barrier();  // gexp written; the row loads stay in flight
   const float up = ldexpf(1.f, gexp[0]);  // 2^e, exact
+  float so[16];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    so[2 * e] = f16_lo(so_lo[e]);
+    so[2 * e + 1] = f16_hi(so_lo[e]);
+    so[8 + 2 * e] = f16_lo(so_hi[e]);
+    so[8 + 2 * e + 1] = f16_hi(so_hi[e]);
+  }
   float acc[16];
 #pragma unroll
   for (int q = 0; q < 16; ++q) acc[q] = 0.f;
 #pragma unroll
-  for (int q4 = 0; q4 < kPrepTokens / 16; ++q4) {
+  for (int q4 = 0; q4 < kRows; ++q4) {
     const int t = tb * kPrepTokens + ty + 16 * q4;
-    if (!live || t >= T) continue;
-    const uint16_t *src = dy + (size_t)t * m + c;
-    const u32x4 lo = *reinterpret_cast<const u32x4 *>(src);
-    const u32x4 hi = *reinterpret_cast<const u32x4 *>(src + 16);
-    const float *zr = z + (size_t)t * m + c;
-    const float4 z0 = *reinterpret_cast<const float4 *>(zr);
-    const float4 z1 = *reinterpret_cast<const float4 *>(zr + 4);
-    const float4 z2 = *reinterpret_cast<const float4 *>(zr + 16);
-    const float4 z3 = *reinterpret_cast<const float4 *>(zr + 20);
-    const float zl[8] = {z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w};
-    const float zh[8] = {z2.x, z2.y, z2.z, z2.w, z3.x, z3.y, z3.z, z3.w};
+    const bool use = live && t < T;
+    const float zl[8] = {zq[q4][0].x, zq[q4][0].y, zq[q4][0].z, zq[q4][0].w,
+                         zq[q4][1].x, zq[q4][1].y, zq[q4][1].z, zq[q4][1].w};
+    const float zh[8] = {zq[q4][2].x, zq[q4][2].y, zq[q4][2].z, zq[q4][2].w,
+                         zq[q4][3].x, zq[q4][3].y, zq[q4][3].z, zq[q4][3].w};
+    const u32x4 lo = dlo[q4], hi = dhi[q4];
     uint32_t d[8];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const float g0 = __uint_as_float(lo[e] << 16), g1 = __uint_as_float(lo[e] & 0xffff0000u);
       const float h0 = __uint_as_float(hi[e] << 16), h1 = __uint_as_float(hi[e] & 0xffff0000u);
-      acc[2 * e] += g0 * zl[2 * e];
-      acc[2 * e + 1] += g1 * zl[2 * e + 1];
-      acc[8 + 2 * e] += h0 * zh[2 * e];
-      acc[8 + 2 * e + 1] += h1 * zh[2 * e + 1];
+      // rows past T (and units past m) add +0: a sum that started at +0 stays
+      acc[2 * e] += use ? g0 * zl[2 * e] : 0.f;
+      acc[2 * e + 1] += use ? g1 * zl[2 * e + 1] : 0.f;
+      acc[8 + 2 * e] += use ? h0 * zh[2 * e] : 0.f;
+      acc[8 + 2 * e + 1] += use ? h1 * zh[2 * e + 1] : 0.f;
       // pair dword: column c+k (low half) with its partner c+16+k (high)
       d[2 * e] = pack_f16x2(g0 * so[2 * e] * up, h0 * so[8 + 2 * e] * up);
       d[2 * e + 1] = pack_f16x2(g1 * so[2 * e + 1] * up, h1 * so[8 + 2 * e + 1] * up);
     }
-    uint4 *dst = reinterpret_cast<uint4 *>(A1 + (size_t)t * m + (c & ~31) + 2 * (c & 15));
-    dst[0] = make_uint4(d[0], d[1], d[2], d[3]);
-    dst[1] = make_uint4(d[4], d[5], d[6], d[7]);
+    if (use) {
+      uint4 *dst = reinterpret_cast<uint4 *>(A1 + (size_t)t * m + (c & ~31) + 2 * (c & 15));
+      dst[0] = make_uint4(d[0], d[1], d[2], d[3]);
+      dst[1] = make_uint4(d[4], d[5], d[6], d[7]);
+    }
   }
   // columns of this block: unit ux covers local columns lc .. lc+7 and
   // lc+16 .. lc+23 of the block's 256
