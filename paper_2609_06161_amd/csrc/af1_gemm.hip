@@ -705,28 +705,41 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       for (int i = 0; i < kTokBlocks; ++i)
         af[slot][i] = *reinterpret_cast<const half8 *>(abase + a_rd[ks] + 32 * i * kARow);
     };
+    // Sign operand of MFMA step ks for weight-row block j: the fp16 pair
+    // (+1, +1) XOR the sign bits moved to bits 15 and 31; words past the row
+    // end (a partial last K step) meet +-0.
+    auto expand = [&](int ks, int j) {
+      const uint32_t one = step * kWords + (ks >> 1) < kw ? kOnePair : 0u;
+      const uint32_t w = wj[j][ks >> 1];
+      uint32_t bd[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) bd[e] = one ^ ((w << sh[ks & 1][e]) & kSignMask);
+      return make_uint4(bd[0], bd[1], bd[2], bd[3]);
+    };
+    // Each group of MFMAs uses a sign operand expanded one group earlier
+    // (block 1's of step ks while block 0's MFMAs of ks run, block 0's of
+    // ks + 1 while block 1's run), and the next step's LDS reads are issued
+    // ahead too; the scheduling barriers keep that order, so no MFMA waits
+    // on the instructions just before it.
     read_ops(0, 0);
+    uint4 b0 = expand(0, 0), b1;
     static_for<2 * kWords>([&](auto KS) {
       constexpr int ks = decltype(KS)::value;
       constexpr int cur = ks & 1;
       if constexpr (ks + 1 < 2 * kWords) read_ops(ks + 1, cur ^ 1);
-      // Keep the next step's LDS reads ahead of this step's MFMAs (the
-      // scheduler would otherwise sink them next to their use).
+      b1 = expand(ks, 1);
       __builtin_amdgcn_sched_barrier(0);
-      // words past the row end (a partial last K step) meet +-0
-      const uint32_t one = step * kWords + (ks >> 1) < kw ? kOnePair : 0u;
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const uint32_t w = wj[j][ks >> 1];
-        uint32_t bd[4];
+      for (int i = 0; i < kTokBlocks; ++i)
+        acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[cur][i], __builtin_bit_cast(half8, b0),
+                                                           acc[i][0], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (ks + 1 < 2 * kWords) b0 = expand(ks + 1, 0);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) bd[e] = one ^ ((w << sh[ks & 1][e]) & kSignMask);
-        const uint4 bq = make_uint4(bd[0], bd[1], bd[2], bd[3]);
-#pragma unroll
-        for (int i = 0; i < kTokBlocks; ++i)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[cur][i], __builtin_bit_cast(half8, bq),
-                                                             acc[i][j], 0, 0, 0);
-      }
+      for (int i = 0; i < kTokBlocks; ++i)
+        acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[cur][i], __builtin_bit_cast(half8, b1),
+                                                           acc[i][1], 0, 0, 0);
     });
     // the next step's copies must have landed; with three stages the
     // copies of the step after it may stay in flight
