@@ -849,18 +849,24 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     for (int q = tid; q < kBM; q += kThreads)
       shl[q] = t0 + q < T ? fwd_shift<kMode == kMid || kMode == kMidSave>(tinfo, T, t0 + q) : 0;
     __syncthreads();
+    // The saving modes shift the accumulators in place (their saved outputs
+    // take the shifted values); kMid and kOut shift each value on its way
+    // into the output staging below (the same operations in the same order),
+    // so that the old and the new accumulators are never live together.
+    if constexpr (kMode == kMidSave || kMode == kOutSave) {
 #pragma unroll
-    for (int i = 0; i < kTokBlocks; ++i)
+      for (int i = 0; i < kTokBlocks; ++i)
 #pragma unroll
-      for (int e4 = 0; e4 < 4; ++e4) {
-        const int4 s4 = *reinterpret_cast<const int4 *>(shl + 32 * i + 8 * e4 + 4 * g);
-        const int sv[4] = {s4.x, s4.y, s4.z, s4.w};
+        for (int e4 = 0; e4 < 4; ++e4) {
+          const int4 s4 = *reinterpret_cast<const int4 *>(shl + 32 * i + 8 * e4 + 4 * g);
+          const int sv[4] = {s4.x, s4.y, s4.z, s4.w};
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+          for (int j = 0; j < 2; ++j)
 #pragma unroll
-          for (int e3 = 0; e3 < 4; ++e3)
-            acc[i][j][4 * e4 + e3] = ldexpf(acc[i][j][4 * e4 + e3], sv[e3]);
-      }
+            for (int e3 = 0; e3 < 4; ++e3)
+              acc[i][j][4 * e4 + e3] = ldexpf(acc[i][j][4 * e4 + e3], sv[e3]);
+        }
+    }
   }
   auto stage_tile = [&](auto value) {
 #pragma unroll
@@ -956,10 +962,40 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     }
     return;
   }
-  stage_tile([&](int i, int j, int e) {
-    const float v = acc[i][j][e] * rs[j];
-    return kPairOut ? f32_to_f16(v) : f32_to_bf16(v);
-  });
+  if constexpr (kMode == kMid || kMode == kOut) {
+    // stage_tile with the range-guard shift applied per value, a token
+    // block at a time (its 16 shifts read once for both column blocks)
+    const int *shl = reinterpret_cast<const int *>(lds + kW0);
+#pragma unroll
+    for (int i = 0; i < kTokBlocks; ++i) {
+      int sv[16];
+#pragma unroll
+      for (int e4 = 0; e4 < 4; ++e4) {
+        const int4 s4 = *reinterpret_cast<const int4 *>(shl + 32 * i + 8 * e4 + 4 * g);
+        sv[4 * e4] = s4.x;
+        sv[4 * e4 + 1] = s4.y;
+        sv[4 * e4 + 2] = s4.z;
+        sv[4 * e4 + 3] = s4.w;
+      }
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int cbyte = 2 * (cpos[j] & 7), chunk = (cpos[j] >> 3) ^ (4 * g);
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int row = 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
+          const float v = ldexpf(acc[i][j][e], sv[e]) * rs[j];
+          *reinterpret_cast<uint16_t *>(lds + row * 512 + chunk * 16 + cbyte) =
+              kPairOut ? f32_to_f16(v) : f32_to_bf16(v);
+        }
+      }
+    }
+    __syncthreads();
+  } else {
+    stage_tile([&](int i, int j, int e) {
+      const float v = acc[i][j][e] * rs[j];
+      return kPairOut ? f32_to_f16(v) : f32_to_bf16(v);
+    });
+  }
   store_tile(C);
   if constexpr (kMode == kMidSave) {
     __syncthreads();
