@@ -789,19 +789,39 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   // layout (one column per lane) it took 64-128 single-float stores a lane,
   // whose issue alone cost about 2 us per workgroup.  The LDS buffers must
   // be idle on entry.
-  auto store_f32_tile = [&](float *__restrict__ dst) {
-    constexpr int kRowF = 128 + 4;  // floats per staged token row
-    static_assert(kBM * kRowF * 4 <= kLdsBytes, "fp32 staging fits the LDS");
+  // The forward's per-token range-guard shifts (see prep_kernel) of the
+  // tile's tokens, a table at the end of the LDS (past every staging area
+  // below), filled before the epilogue's stores; the 16 shifts of token
+  // block i for this lane's rows 8(e/4) + 4(l/32) + (e mod 4).
+  constexpr int kRowF = 128 + 4;  // floats per staged fp32 token row
+  constexpr int kShl = kLdsBytes - 4 * kBM;
+  static_assert(kBM * kRowF * 4 <= kShl && kBM * 512 <= kShl, "staging clear of the shifts");
+  auto load_shifts = [&](int i, int (&sv)[16]) {
+    const int *shl = reinterpret_cast<const int *>(lds + kShl);
+#pragma unroll
+    for (int e4 = 0; e4 < 4; ++e4) {
+      const int4 s4 = *reinterpret_cast<const int4 *>(shl + 32 * i + 8 * e4 + 4 * g);
+      sv[4 * e4] = s4.x;
+      sv[4 * e4 + 1] = s4.y;
+      sv[4 * e4 + 2] = s4.z;
+      sv[4 * e4 + 3] = s4.w;
+    }
+  };
+  auto store_f32_tile = [&](float *__restrict__ dst, auto shifted) {
+    constexpr bool kShift = decltype(shifted)::value;
     float *stg = reinterpret_cast<float *>(lds);
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       if (j > 0) __syncthreads();  // the previous half has been read
 #pragma unroll
-      for (int i = 0; i < kTokBlocks; ++i)
+      for (int i = 0; i < kTokBlocks; ++i) {
+        int sv[16] = {};
+        if constexpr (kShift) load_shifts(i, sv);
 #pragma unroll
         for (int e = 0; e < 16; ++e)
           stg[(32 * i + 8 * (e >> 2) + 4 * g + (e & 3)) * kRowF + 32 * wave + (lane & 31)] =
-              acc[i][j][e];
+              kShift ? ldexpf(acc[i][j][e], sv[e]) : acc[i][j][e];
+      }
       __syncthreads();
 #pragma unroll
       for (int q = 0; q < kBM * 32 / kThreads; ++q) {
@@ -822,7 +842,7 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       // Split K: the fp32 partial of this tile over the workgroup's K steps,
       // natural column order; the reduction kernel adds the partials and
       // applies the mode's epilogue.
-      store_f32_tile(P + (size_t)blockIdx.z * T * N);
+      store_f32_tile(P + (size_t)blockIdx.z * T * N, std::false_type{});
       return;
     }
   }
@@ -840,33 +860,15 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     rs[j] = n < N ? (rowscale ? f16_to_f32(rowscale[n]) : 1.0f) : 0.f;
     cpos[j] = (kPairOut ? pair_pos(n) : n) - n0;
   }
-  // The forward's per-token range-guard shifts (see prep_kernel), applied to
-  // the accumulators before any rounding: a table of the tile's tokens in
-  // the idle sign buffers, read four consecutive tokens at a time (the rows
-  // 4(l/32) + (e mod 4) of an accumulator block).
+  // The range-guard shift table (see load_shifts).  The shifts are applied
+  // to each value on its way into an output staging (before any rounding),
+  // never to the accumulators in place: shifting in place kept old and new
+  // accumulators live together and spilled registers to scratch.
   if constexpr (!kBwd) {
-    int *shl = reinterpret_cast<int *>(lds + kW0);
+    int *shl = reinterpret_cast<int *>(lds + kShl);
     for (int q = tid; q < kBM; q += kThreads)
       shl[q] = t0 + q < T ? fwd_shift<kMode == kMid || kMode == kMidSave>(tinfo, T, t0 + q) : 0;
     __syncthreads();
-    // The saving modes shift the accumulators in place (their saved outputs
-    // take the shifted values); kMid and kOut shift each value on its way
-    // into the output staging below (the same operations in the same order),
-    // so that the old and the new accumulators are never live together.
-    if constexpr (kMode == kMidSave || kMode == kOutSave) {
-#pragma unroll
-      for (int i = 0; i < kTokBlocks; ++i)
-#pragma unroll
-        for (int e4 = 0; e4 < 4; ++e4) {
-          const int4 s4 = *reinterpret_cast<const int4 *>(shl + 32 * i + 8 * e4 + 4 * g);
-          const int sv[4] = {s4.x, s4.y, s4.z, s4.w};
-#pragma unroll
-          for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int e3 = 0; e3 < 4; ++e3)
-              acc[i][j][4 * e4 + e3] = ldexpf(acc[i][j][4 * e4 + e3], sv[e3]);
-        }
-    }
   }
   auto stage_tile = [&](auto value) {
 #pragma unroll
@@ -962,50 +964,41 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     }
     return;
   }
-  if constexpr (kMode == kMid || kMode == kOut) {
-    // stage_tile with the range-guard shift applied per value, a token
-    // block at a time (its 16 shifts read once for both column blocks)
-    const int *shl = reinterpret_cast<const int *>(lds + kW0);
+  // stage_tile with the range-guard shift: value(v, j) of v = the shifted
+  // accumulator, a token block at a time (its 16 shifts read once for both
+  // column blocks)
+  auto stage_shifted = [&](auto value) {
 #pragma unroll
     for (int i = 0; i < kTokBlocks; ++i) {
       int sv[16];
-#pragma unroll
-      for (int e4 = 0; e4 < 4; ++e4) {
-        const int4 s4 = *reinterpret_cast<const int4 *>(shl + 32 * i + 8 * e4 + 4 * g);
-        sv[4 * e4] = s4.x;
-        sv[4 * e4 + 1] = s4.y;
-        sv[4 * e4 + 2] = s4.z;
-        sv[4 * e4 + 3] = s4.w;
-      }
+      load_shifts(i, sv);
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const int cbyte = 2 * (cpos[j] & 7), chunk = (cpos[j] >> 3) ^ (4 * g);
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int row = 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
-          const float v = ldexpf(acc[i][j][e], sv[e]) * rs[j];
           *reinterpret_cast<uint16_t *>(lds + row * 512 + chunk * 16 + cbyte) =
-              kPairOut ? f32_to_f16(v) : f32_to_bf16(v);
+              value(ldexpf(acc[i][j][e], sv[e]), j);
         }
       }
     }
     __syncthreads();
-  } else {
-    stage_tile([&](int i, int j, int e) {
-      const float v = acc[i][j][e] * rs[j];
-      return kPairOut ? f32_to_f16(v) : f32_to_bf16(v);
-    });
-  }
+  };
+  stage_shifted([&](float v, int j) {
+    v *= rs[j];
+    return kPairOut ? f32_to_f16(v) : f32_to_bf16(v);
+  });
   store_tile(C);
   if constexpr (kMode == kMidSave) {
     __syncthreads();
     const int es = smax_exp(tinfo[2 * T]);
-    stage_tile([&](int i, int j, int e) { return f32_to_f16(ldexpf(acc[i][j][e], es)); });
+    stage_shifted([&](float v, int) { return f32_to_f16(ldexpf(v, es)); });
     store_tile(V);
   }
   if constexpr (kMode == kOutSave) {
     __syncthreads();  // every wave is done reading the staged C tile
-    store_f32_tile(F);
+    store_f32_tile(F, std::true_type{});
   }
 }
 
