@@ -226,9 +226,10 @@ __device__ __forceinline__ int saved_v_shift(const float *__restrict__ tinfo, in
   return mid_exp(ti.x, tinfo[2 * T]) - smax_exp(tinfo[2 * T]) - __float_as_int(ti.y);
 }
 
-// One token row per workgroup: x (bf16, [T][K]) and s (fp16, [K]) ->
-// xp = fp16(x .* s 2^e_t) ([T][K], pair order) and the token's record.
-// Three steps, each ending in a reduction over the workgroup:
+// The forward's preparation and range guard.  Each token row is prepared by
+// one workgroup: x (bf16, [T][K]) and s (fp16, [K]) -> xp = fp16(x .* s
+// 2^e_t) ([T][K], pair order) and the token's record.  Three steps, each
+// ending in a reduction over the workgroup:
 //  1. the largest |x| (bf16 magnitudes compare as integers), whose binary
 //     exponent gives a first shift e1 with |x 2^e1| < 1 (so x 2^e1 s_in is
 //     finite and exact for any bf16 x and fp16 s_in);
@@ -237,7 +238,7 @@ __device__ __forceinline__ int saved_v_shift(const float *__restrict__ tinfo, in
 // Rows of up to 2048 units (1024 threads, two units each) are loaded once
 // and kept in registers through the three steps (prep_stream_kernel); wider
 // rows are read three times (prep_kernel, the later passes hit the caches).
-// Block T stores max |s_mid| instead.  A unit is 16 columns: 8 columns
+// One more workgroup stores max |s_mid|.  A unit is 16 columns: 8 columns
 // c .. c+7 and their partners c+16 .. c+23, which become the pair dwords
 // 8h .. 8h+7 of their group.
 __device__ __forceinline__ void load_x_unit(const uint16_t *__restrict__ row, int c, u32x4 &lo,
@@ -731,15 +732,15 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < kTokBlocks; ++i)
-        acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[cur][i], __builtin_bit_cast(half8, b0),
-                                                           acc[i][0], 0, 0, 0);
+        acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
+            af[cur][i], __builtin_bit_cast(half8, b0), acc[i][0], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
       if constexpr (ks + 1 < 2 * kWords) b0 = expand(ks + 1, 0);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < kTokBlocks; ++i)
-        acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(af[cur][i], __builtin_bit_cast(half8, b1),
-                                                           acc[i][1], 0, 0, 0);
+        acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
+            af[cur][i], __builtin_bit_cast(half8, b1), acc[i][1], 0, 0, 0);
     });
     // the next step's copies must have landed; with three stages the
     // copies of the step after it may stay in flight
@@ -782,14 +783,7 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       return;
     }
   }
-  // A fp32 [T][N] output of the whole tile (a split partial, or the saved
-  // pre-scale output z): each half of the tile's columns (the j-th 32 of
-  // every wave's 64) is transposed through the idle LDS buffers and leaves
-  // in 16-byte stores along the columns.  Stored from the accumulator
-  // layout (one column per lane) it took 64-128 single-float stores a lane,
-  // whose issue alone cost about 2 us per workgroup.  The LDS buffers must
-  // be idle on entry.
-  // The forward's per-token range-guard shifts (see prep_kernel) of the
+  // The forward's per-token range-guard shifts (see prep_stream_kernel) of the
   // tile's tokens, a table at the end of the LDS (past every staging area
   // below), filled before the epilogue's stores; the 16 shifts of token
   // block i for this lane's rows 8(e/4) + 4(l/32) + (e mod 4).
@@ -807,6 +801,14 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       sv[4 * e4 + 3] = s4.w;
     }
   };
+  // A fp32 [T][N] output of the whole tile (a split partial, or the saved
+  // pre-scale output z): each half of the tile's columns (the j-th 32 of
+  // every wave's 64) is transposed through the idle LDS buffers and leaves
+  // in 16-byte stores along the columns.  Stored from the accumulator
+  // layout (one column per lane) it took 64-128 single-float stores a lane,
+  // whose issue alone cost about 2 us per workgroup.  The LDS buffers must
+  // be idle on entry.  shifted: apply the range-guard shifts (the saved z)
+  // or not (a split partial, shifted by its reduction).
   auto store_f32_tile = [&](float *__restrict__ dst, auto shifted) {
     constexpr bool kShift = decltype(shifted)::value;
     float *stg = reinterpret_cast<float *>(lds);
@@ -1328,7 +1330,7 @@ __device__ __forceinline__ void finish8(const float4 &lo, const float4 &hi, cons
                                         int p, int t, int N, uint16_t *__restrict__ C,
                                         uint16_t *__restrict__ V, float *__restrict__ F) {
   constexpr bool kPairOut = kMode == kMid || kMode == kMidSave;
-  // the token's range-guard shift (see prep_kernel) before any rounding
+  // the token's range-guard shift (see prep_stream_kernel) before any rounding
   const int c_t = mid_exp(in.ti.x, in.smax);
   const int sh = kPairOut ? -c_t : c_t - __float_as_int(in.ti.y);
   const int es = kMode == kMidSave ? smax_exp(in.smax) : 0;
@@ -1725,7 +1727,7 @@ hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *
 constexpr int kPrepWavesPerCU = 16;
 
 // fp16(s_in .* x 2^e_t) in pair order, the A operand of G1, and the
-// per-token range-guard record (see prep_kernel).
+// per-token range-guard record (see prep_stream_kernel).
 hipError_t prepare_forward(int64_t n, const uint16_t *s_in, const uint16_t *x, int64_t T,
                            uint16_t *xp, float *tinfo, const uint16_t *s_mid, int64_t r,
                            hipStream_t s) {
