@@ -97,14 +97,17 @@ constexpr int kATile = BM * kARow;           // 32 KiB
 constexpr int kWTile = BN * kWords * 4;      // 4 KiB
 // LDS map: A0 .. A(S-1) | W0 .. W(S-1) for S pipeline stages (the
 // activation buffers first, so operand reads are immediate offsets from one
-// address), for a token tile of kBM rows (128, or 64 for grids that would
-// give each compute unit at most one workgroup).
+// address), then the forward's per-token tables (the range-guard shift and
+// the row sum R of each of the tile's tokens), for a token tile of kBM rows
+// (128, or 64 for grids that would give each compute unit at most one
+// workgroup).
 template <int kBM, int kStages>
 struct Lds {
   static constexpr int kATileT = kBM * kARow;
   static constexpr int kA0 = 0;
   static constexpr int kW0 = kStages * kATileT;
-  static constexpr int kBytes = kW0 + kStages * kWTile;
+  static constexpr int kTab = kW0 + kStages * kWTile;
+  static constexpr int kBytes = kTab + 8 * kBM;
 };
 constexpr int kOob = (int)0x80000000u;
 static_assert(BM * kARow == 32 * 1024 && kThreads == 256, "eight 1 KiB copies per wave at BM");
@@ -176,47 +179,70 @@ __device__ __forceinline__ int pair_pos(int c) {
 // 2^-24 .. 65504, so both fp16 operands carry a power-of-two scale that is
 // undone in fp32:
 //   xp[t]  = fp16(s_in .* x[t] * 2^e_t), e_t putting the row's largest entry
-//            in [2^13, 2^14);
+//            in [2^-1, 1);
 //   Z[t]   = fp16(s_mid .* (Bv xp[t]) * 2^-c_t), where L_t = sum_j |s_in_j
 //            x_tj| 2^e_t bounds every |(Bv xp[t])_k| (the signs are +-1),
-//            and c_t makes L_t * max|s_mid| * 2^-c_t < 2^14;
+//            and c_t makes L_t * max|s_mid| * 2^-c_t < 1;
 //   y[t]   = bf16(s_out .* (Bu Z[t]) * 2^(c_t - e_t)).
-// Each rounding to fp16 is therefore a plain 2^-11 relative rounding with no
-// overflow, whatever the magnitude of x (entries far below a row's largest
-// one, under 2^-27 of it, keep fewer digits, as in any fp16 rounding).
-// Scaling by a power of two is exact, so for inputs inside fp16's range the
-// results differ from unscaled operands only where they would have been
-// subnormal.  The per-token record is
+// Both operands are stored with a further exact power-of-two factor per
+// column, 2^slot_exp(column mod 4) <= 2^14 (see the sign operands below), so
+// every stored fp16 value stays under 2^14: each rounding to fp16 is a plain
+// 2^-11 relative rounding with no overflow, whatever the magnitude of x
+// (entries far below a row's largest one, under about 2^-20 of it, keep
+// fewer digits, as in any fp16 rounding).  Scaling by a power of two is
+// exact, so for inputs inside fp16's range the results differ from unscaled
+// operands only where they would have been subnormal.  The per-token record
+// is
 //   tinfo[2t] = L_t (fp32),  tinfo[2t + 1] = e_t (int32 bits),
-//   tinfo[2T] = max_k |s_mid_k|.
+//   tinfo[2T] = max_k |s_mid_k|,
+//   tinfo[2T + 4 + t] = R1_t, tinfo[3T + 4 + t] = R2_t (the row sums of
+//   the two products' operands, see the sign operands below).
 // `tinfo_floats(T)` floats hold it.
-__host__ __device__ constexpr int64_t tinfo_floats(int64_t T) { return 2 * T + 4; }
+__host__ __device__ constexpr int64_t tinfo_floats(int64_t T) { return 4 * T + 4; }
+template <typename F>
+__device__ __forceinline__ F *tinfo_r1(F *tinfo, int T) { return tinfo + 2 * T + 4; }
+template <typename F>
+__device__ __forceinline__ F *tinfo_r2(F *tinfo, int T) { return tinfo + 3 * T + 4; }
 
-// Exponent c_t of the intermediate's scale: 2^-c_t L_t smax' < 2^14, with
+// Sign operands of the forward products.  The MFMA's sign operand is built
+// from the packed words with a rotation and a mask: a set bit (sign -1)
+// becomes a single fp16 exponent bit, the value 2^-slot_exp(e) with e the
+// operand register's index in its quad (bits 10 .. 13: 2^-14, 2^-13,
+// 2^-11, 2^-7), a clear bit zero.  The activation operand of column j
+// carries the matching factor 2^slot_exp(j mod 4) (the column's register
+// index in pair order is j mod 4), so the product accumulates
+// acc = sum_j a_j b_j, with a_j the activation as stored times
+// 2^-slot_exp and b_j the sign bit, and the signed product is
+// sum_j (1 - 2 b_j) a_j = R - 2 acc with the row sum R = sum_j a_j.  R1_t
+// (the G1 operand's, from the preparation) and R2_t (the intermediate's,
+// from G1's per-tile sums) are in the record above.  The mask keeps single
+// exponent bits because the matrix cores multiply normal fp16 powers of two
+// exactly, while single-bit subnormals lose precision.  (The backward keeps
+// the +-1 operands.)
+__host__ __device__ constexpr int slot_exp(int e) {
+  return e == 0 ? 14 : e == 1 ? 13 : e == 2 ? 11 : 7;
+}
+// G1's per-tile row sums of the intermediate: RS[t][b] = sum of a_k over the
+// 256 columns of tile b (the second product adds them up into R2_t), rows
+// of rs_ld(r) floats.
+__host__ __device__ constexpr int rs_ld(int64_t r) { return (int)((((r + 255) / 256) + 3) & ~3); }
+
+// Exponent c_t of the intermediate's scale: 2^-c_t L_t smax' < 1, with
 // smax' = max|s_mid| (1 when every s_mid is zero).  0 for an all-zero row.
 __device__ __forceinline__ int mid_exp(float L, float smax) {
   const float b = L * (smax > 0.f ? smax : 1.f);
   if (!(b > 0.f) || !__builtin_isfinite(b)) return 0;
   int k;
   frexpf(b, &k);  // b = f 2^k, f in [0.5, 1): b < 2^k
-  return k - 14;
-}
-
-// Exponent of max|s_mid|: smax' < 2^es (so 2^(es - c_t) L_t < 2^15).
-__device__ __forceinline__ int smax_exp(float smax) {
-  int k;
-  frexpf(smax > 0.f && __builtin_isfinite(smax) ? smax : 1.f, &k);
   return k;
 }
 
-// The token's shift of the forward output before its row scale: the first
-// product's accumulator (kMid modes) is scaled by 2^-c_t, the second's (kOut
-// modes) by 2^(c_t - e_t), which leaves the unscaled value.
-template <bool kFirst>
-__device__ __forceinline__ int fwd_shift(const float *__restrict__ tinfo, int T, int t) {
-  const float2 ti = reinterpret_cast<const float2 *>(tinfo)[t];
-  const int c = mid_exp(ti.x, tinfo[2 * T]);
-  return kFirst ? -c : c - __float_as_int(ti.y);
+// Scale exponent of the training forward's saved v: smax' < 2^(es - 14)
+// (so 2^(es - c_t) L_t < 2^15).
+__device__ __forceinline__ int smax_exp(float smax) {
+  int k;
+  frexpf(smax > 0.f && __builtin_isfinite(smax) ? smax : 1.f, &k);
+  return k + 14;
 }
 
 // The training forward saves V = fp16(v 2^(e_t - c_t + es)) (v = Bv (s_in
@@ -234,7 +260,10 @@ __device__ __forceinline__ int saved_v_shift(const float *__restrict__ tinfo, in
 //     exponent gives a first shift e1 with |x 2^e1| < 1 (so x 2^e1 s_in is
 //     finite and exact for any bf16 x and fp16 s_in);
 //  2. p = x 2^e1 s_in: the largest |p| and sum |p|, which give e2;
-//  3. xp = fp16(p 2^e2), e_t = e1 + e2.
+//  3. xp = fp16(p 2^(e2 + slot_exp(column mod 4))), e_t = e1 + e2, and the
+//     thread's part of R1_t, the sum of the stored values over their column
+//     factors (see the sign operands above), reduced with the next step 1
+//     of the workgroup (or on its own after its last token).
 // Rows of up to 2048 units (1024 threads, two units each) are loaded once
 // and kept in registers through the three steps (prep_stream_kernel); wider
 // rows are read three times (prep_kernel, the later passes hit the caches).
@@ -287,16 +316,28 @@ __device__ __forceinline__ float dpp_f32(float v) {
 __device__ __forceinline__ float lane_f32(float v, int l) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
 }
+// Sum of the 16 lanes of each DPP row, in every lane of the row.
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_f32<0xB1>(v);
+  v += dpp_f32<0x4E>(v);
+  v += dpp_f32<0x124>(v);
+  v += dpp_f32<0x128>(v);
+  return v;
+}
+// The sum of v over the 32 lanes of each half wave (all 64 lanes active),
+// in every lane: the DPP rows of 16, then the two rows of the half.
+__device__ __forceinline__ float half_wave_sum(float v) {
+  const float h = row16_sum(v);
+  return (threadIdx.x & 32) == 0 ? lane_f32(h, 0) + lane_f32(h, 16)
+                                 : lane_f32(h, 32) + lane_f32(h, 48);
+}
 template <int kWaves>
 __device__ __forceinline__ void block_sum_max_async(float &sum, float &mx, float *red) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  sum += dpp_f32<0xB1>(sum);
+  sum = row16_sum(sum);
   mx = fmaxf(mx, dpp_f32<0xB1>(mx));
-  sum += dpp_f32<0x4E>(sum);
   mx = fmaxf(mx, dpp_f32<0x4E>(mx));
-  sum += dpp_f32<0x124>(sum);
   mx = fmaxf(mx, dpp_f32<0x124>(mx));
-  sum += dpp_f32<0x128>(sum);
   mx = fmaxf(mx, dpp_f32<0x128>(mx));
   sum = (lane_f32(sum, 0) + lane_f32(sum, 16)) + (lane_f32(sum, 32) + lane_f32(sum, 48));
   mx = fmaxf(fmaxf(lane_f32(mx, 0), lane_f32(mx, 16)), fmaxf(lane_f32(mx, 32), lane_f32(mx, 48)));
@@ -358,26 +399,35 @@ __device__ __forceinline__ int prep_e1(uint32_t mb) {
   return e1;
 }
 
-// e2 from the largest |p|: pmax 2^e2 in [2^13, 2^14).
+// e2 from the largest |p|: pmax 2^e2 in [2^-1, 1).
 __device__ __forceinline__ int prep_e2(float pmax) {
   int e2 = 0;
   if (pmax > 0.f && __builtin_isfinite(pmax)) {
     frexpf(pmax, &e2);  // pmax = f 2^k, f in [0.5, 1)
-    e2 = 14 - e2;
+    e2 = -e2;
   }
   return e2;
 }
 
 // Pair-order dwords of one unit from its 16 values (v[d] = column c + d,
-// v[8 + d] = column c + 16 + d), stored at the unit's place in xp.
-__device__ __forceinline__ void prep_store(uint16_t *__restrict__ xp, int t, int K, int c,
-                                           const float (&v)[16], int e2) {
+// v[8 + d] = column c + 16 + d, c a multiple of 8, so both have the column
+// factor of d mod 4), stored at the unit's place in xp; returns the sum of
+// the stored values over their column factors.
+__device__ __forceinline__ float prep_store(uint16_t *__restrict__ xp, int t, int K, int c,
+                                            const float (&v)[16], int e2) {
   uint32_t d[8];
+  float r1 = 0.f;
 #pragma unroll
-  for (int k = 0; k < 8; ++k) d[k] = pack_f16x2(ldexpf(v[k], e2), ldexpf(v[8 + k], e2));
+  for (int k = 0; k < 8; ++k) {
+    const int sc = e2 + slot_exp(k & 3);
+    d[k] = pack_f16x2(ldexpf(v[k], sc), ldexpf(v[8 + k], sc));
+    const _Float16 f = (_Float16)(1.0f / (float)(1 << slot_exp(k & 3)));  // exact
+    r1 = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2v, d[k]), half2v{f, f}, r1, false);
+  }
   uint4 *dst = reinterpret_cast<uint4 *>(xp + (size_t)t * K + (c & ~31) + 2 * (c & 15));
   dst[0] = make_uint4(d[0], d[1], d[2], d[3]);
   dst[1] = make_uint4(d[4], d[5], d[6], d[7]);
+  return r1;
 }
 
 // p values of one unit: x 2^e1 s_in, v[d] = column c + d, v[8 + d] = c + 16 + d.
@@ -440,6 +490,7 @@ __global__ __launch_bounds__(256) void prep_kernel(
   }
   block_sum_max(l1, pmax, red);
   const int e2 = prep_e2(pmax);
+  float r1 = 0.f, unused = 0.f;
   for (int u = threadIdx.x; u < units; u += 256) {
     const int c = unit_col(u);
     u32x4 lo, hi;
@@ -447,10 +498,13 @@ __global__ __launch_bounds__(256) void prep_kernel(
     float v[16];
     prep_values(lo, hi, *reinterpret_cast<const u32x4 *>(s_in + c),
                 *reinterpret_cast<const u32x4 *>(s_in + c + 16), e1, v);
-    prep_store(xp, t, K, c, v, e2);
+    r1 += prep_store(xp, t, K, c, v, e2);
   }
-  if (threadIdx.x == 0)
+  block_sum_max(r1, unused, red);
+  if (threadIdx.x == 0) {
     reinterpret_cast<float2 *>(tinfo)[t] = make_float2(ldexpf(l1, e2), __int_as_float(e1 + e2));
+    tinfo_r1(tinfo, T)[t] = r1;
+  }
 }
 
 // The same preparation for rows of up to kU * kThreads units, persistent:
@@ -479,19 +533,24 @@ __device__ __forceinline__ void prep_row_load(const uint16_t *__restrict__ x, in
     load_x_unit(row, unit_col(min((int)threadIdx.x + kThreads * i, units - 1)), b.lo[i], b.hi[i]);
 }
 
+// carry: in, this thread's part of the previous token tp's R1 (tp < 0:
+// none), added up in the first reduction and stored; out, the part of this
+// token's.
 template <int kU, int kThreads>
 __device__ __forceinline__ void prep_row_token(const PrepRow<kU> &b, const u32x4 (&sl)[kU],
                                                const u32x4 (&sh)[kU], uint16_t *__restrict__ xp,
-                                               float *__restrict__ tinfo, int t, int K,
-                                               int units, float *red) {
+                                               float *__restrict__ tinfo, int t, int T,
+                                               int K, int units, float *red, float &carry,
+                                               int tp) {
   uint32_t mb = 0;
 #pragma unroll
   for (int i = 0; i < kU; ++i) {
     const uint32_t m = unit_maxbits(b.lo[i], b.hi[i]);
     mb = max(mb, (int)threadIdx.x + kThreads * i < units ? m : 0u);
   }
-  float sum = 0.f, mx = __uint_as_float(mb);
-  block_sum_max_async<kThreads / 64>(sum, mx, red);
+  float mx = __uint_as_float(mb);
+  block_sum_max_async<kThreads / 64>(carry, mx, red);
+  if (tp >= 0) tinfo_r1(tinfo, T)[tp] = carry;  // the same value in every lane
   const int e1 = prep_e1(__float_as_uint(mx));
   float v[kU][16], l1 = 0.f, pmax = 0.f;
 #pragma unroll
@@ -506,11 +565,24 @@ __device__ __forceinline__ void prep_row_token(const PrepRow<kU> &b, const u32x4
   }
   block_sum_max_async<kThreads / 64>(l1, pmax, red);
   const int e2 = prep_e2(pmax);
+  carry = 0.f;
 #pragma unroll
-  for (int i = 0; i < kU; ++i)
-    prep_store(xp, t, K, unit_col(min((int)threadIdx.x + kThreads * i, units - 1)), v[i], e2);
+  for (int i = 0; i < kU; ++i) {
+    const float r1 = prep_store(xp, t, K, unit_col(min((int)threadIdx.x + kThreads * i, units - 1)),
+                                v[i], e2);
+    carry += (int)threadIdx.x + kThreads * i < units ? r1 : 0.f;
+  }
   // every lane stores the token's record (the same value, one write a wave)
   reinterpret_cast<float2 *>(tinfo)[t] = make_float2(ldexpf(l1, e2), __int_as_float(e1 + e2));
+}
+
+// The last token's R1 (see prep_row_token).
+template <int kThreads>
+__device__ __forceinline__ void prep_r1_flush(float *__restrict__ tinfo, int T, int tp,
+                                              float carry, float *red) {
+  float unused = 0.f;
+  block_sum_max_async<kThreads / 64>(carry, unused, red);
+  tinfo_r1(tinfo, T)[tp] = carry;
 }
 
 template <int kU, int kThreads>
@@ -533,21 +605,30 @@ __global__ __launch_bounds__(kThreads) void prep_stream_kernel(
     sh[i] = *reinterpret_cast<const u32x4 *>(s_in + c + 16);
   }
   PrepRow<kU> a, b;
+  float carry = 0.f;  // R1 part of the last token prepared
   int t = blockIdx.x;  // < T: the grid has at most T workers
   prep_row_load<kU, kThreads>(x, t, K, units, a);
   prep_row_load<kU, kThreads>(x, min(t + W, T - 1), K, units, b);
-  prep_row_token<kU, kThreads>(a, sl, sh, xp, tinfo, t, K, units, red);
+  prep_row_token<kU, kThreads>(a, sl, sh, xp, tinfo, t, T, K, units, red, carry, -1);
   t += W;
-  if (t >= T) return;
+  if (t >= T) {
+    prep_r1_flush<kThreads>(tinfo, T, t - W, carry, red);
+    return;
+  }
   prep_row_load<kU, kThreads>(x, min(t + W, T - 1), K, units, a);
-  prep_row_token<kU, kThreads>(b, sl, sh, xp, tinfo, t, K, units, red);
+  prep_row_token<kU, kThreads>(b, sl, sh, xp, tinfo, t, T, K, units, red, carry, t - W);
   for (t += W; t < T; t += 2 * W) {
     prep_row_load<kU, kThreads>(x, min(t + W, T - 1), K, units, b);
-    prep_row_token<kU, kThreads>(a, sl, sh, xp, tinfo, t, K, units, red);
-    if (t + W >= T) break;
+    prep_row_token<kU, kThreads>(a, sl, sh, xp, tinfo, t, T, K, units, red, carry, t - W);
+    if (t + W >= T) {
+      prep_r1_flush<kThreads>(tinfo, T, t, carry, red);
+      return;
+    }
     prep_row_load<kU, kThreads>(x, min(t + 2 * W, T - 1), K, units, a);
-    prep_row_token<kU, kThreads>(b, sl, sh, xp, tinfo, t + W, K, units, red);
+    prep_row_token<kU, kThreads>(b, sl, sh, xp, tinfo, t + W, T, K, units, red, carry, t);
   }
+  // the loop ended after a token pair: t - W was prepared last
+  prep_r1_flush<kThreads>(tinfo, T, t - W, carry, red);
 }
 
 // C = rowscale * (A_pairorder x sign(W)^T), in the forms listed under Mode.
@@ -557,9 +638,10 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     const uint16_t *__restrict__ rowscale, uint16_t *__restrict__ C, uint16_t *__restrict__ V,
     const uint16_t *__restrict__ S, float *__restrict__ F, const float *__restrict__ gscale,
     int split_steps, float *__restrict__ P, int mix_full, int mix_splits, int mix_nN,
-    const float *__restrict__ tinfo) {
+    float *__restrict__ tinfo, float *__restrict__ RS) {
   constexpr bool kPairOut = kMode == kMid || kMode == kMidSave || kMode == kBwdMid;
   constexpr bool kBwd = kMode == kBwdMid || kMode == kBwdIn;
+  constexpr bool kFirst = kMode == kMid || kMode == kMidSave;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -652,6 +734,47 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   __syncthreads();
   issue(k0, 0);
   if (kStages == 3 && k0 + 1 < nk) issue(k0 + 1, 1);
+  // The forward's per-token tables, loaded while the first copies travel:
+  // the range-guard shift of the output (see prep_stream_kernel; the first
+  // product's accumulator is scaled by 2^-c_t, the second's by 2^(c_t - e_t),
+  // which leaves the unscaled value) and the operand's row sum R (R1 from the preparation for the first product; for
+  // the second, R2 added up from G1's per-tile sums in tile order, which the
+  // workgroups of the first column tile and K range also store in the
+  // record for the split and mixed reductions).
+  int tab_sh = 0;
+  float tab_r = 0.f;
+  if constexpr (!kBwd) {
+    const int q = tid < kBM ? tid : kBM - 1;
+    const int t = min(t0 + q, T - 1);
+    const float2 ti = reinterpret_cast<const float2 *>(tinfo)[t];
+    const float smax = tinfo[2 * T];
+    if constexpr (kFirst) {
+      tab_r = tinfo_r1(tinfo, T)[t];
+    } else {
+      const int nb = (K + 255) / 256, ld = rs_ld(K);
+      const float4 *rr = reinterpret_cast<const float4 *>(RS + (size_t)t * ld);
+      for (int b0 = 0; b0 < nb; b0 += 16) {
+        float4 v[4];
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) v[q4] = rr[min(b0 / 4 + q4, ld / 4 - 1)];
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const int b = b0 + 4 * q4;
+          tab_r += b < nb ? v[q4].x : 0.f;
+          tab_r += b + 1 < nb ? v[q4].y : 0.f;
+          tab_r += b + 2 < nb ? v[q4].z : 0.f;
+          tab_r += b + 3 < nb ? v[q4].w : 0.f;
+        }
+      }
+      if (L % nN == 0 && k0 == 0 && tid < kBM && t0 + q < T) tinfo_r2(tinfo, T)[t] = tab_r;
+    }
+    const int c = mid_exp(ti.x, smax);
+    tab_sh = kFirst ? -c : c - __float_as_int(ti.y);
+    if (t0 + q >= T) {
+      tab_sh = 0;
+      tab_r = 0.f;
+    }
+  }
 
   // This lane's weight rows: block j -> tile row 64*wave + 32*j + (l mod 32).
   const int wrow_l = 64 * wave + (lane & 31);
@@ -662,12 +785,16 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   int a_rd[8];
 #pragma unroll
   for (int ks = 0; ks < 8; ++ks) a_rd[ks] = (lane & 31) * kARow + (((2 * ks + g) ^ (lane & 15)) << 4);
-  // Shift that moves sign bit p = 8s + 4g + e of a word to bit 15.
+  // Shift that moves sign bit p = 8s + 4g + e of a word to bit 15 (the
+  // backward's +-1 operands); the forward's rotation right that moves bits
+  // 8s + 4g .. 8s + 4g + 3 (and the same 16 higher) to bits 10 .. 13 (and
+  // 26 .. 29).
   int sh[2][4];
 #pragma unroll
   for (int s = 0; s < 2; ++s)
 #pragma unroll
     for (int e = 0; e < 4; ++e) sh[s][e] = 15 - (8 * s + 4 * g + e);
+  const uint32_t rot[2] = {(uint32_t)(4 * g - 10) & 31u, (uint32_t)(8 + 4 * g - 10) & 31u};
 
   floatx16 acc[kTokBlocks][2];
 #pragma unroll
@@ -685,6 +812,12 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     wait_copies_but<kCopiesPerStep>();
   else
     wait_copies();
+  if constexpr (!kBwd) {
+    if (tid < kBM) {
+      reinterpret_cast<int *>(lds + LM::kTab)[tid] = tab_sh;
+      reinterpret_cast<float *>(lds + LM::kTab + 4 * kBM)[tid] = tab_r;
+    }
+  }
   __syncthreads();
 
   auto run_step = [&](int step, auto BUF) {
@@ -706,15 +839,24 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       for (int i = 0; i < kTokBlocks; ++i)
         af[slot][i] = *reinterpret_cast<const half8 *>(abase + a_rd[ks] + 32 * i * kARow);
     };
-    // Sign operand of MFMA step ks for weight-row block j: the fp16 pair
-    // (+1, +1) XOR the sign bits moved to bits 15 and 31; words past the row
-    // end (a partial last K step) meet +-0.
+    // Sign operand of MFMA step ks for weight-row block j.  Forward: the
+    // word rotated so that register e's two sign bits sit on bits 10 + e and
+    // 26 + e, masked to them (fp16 2^-slot_exp(e) or 0 in each half).
+    // Backward: the fp16 pair (+1, +1) XOR the sign bits moved to bits 15
+    // and 31.  Words past the row end (a partial last K step) meet zeros.
     auto expand = [&](int ks, int j) {
-      const uint32_t one = step * kWords + (ks >> 1) < kw ? kOnePair : 0u;
+      const bool live = step * kWords + (ks >> 1) < kw;
       const uint32_t w = wj[j][ks >> 1];
       uint32_t bd[4];
+      if constexpr (kBwd) {
+        const uint32_t one = live ? kOnePair : 0u;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) bd[e] = one ^ ((w << sh[ks & 1][e]) & kSignMask);
+        for (int e = 0; e < 4; ++e) bd[e] = one ^ ((w << sh[ks & 1][e]) & kSignMask);
+      } else {
+        const uint32_t wr = __builtin_amdgcn_alignbit(w, w, rot[ks & 1]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) bd[e] = wr & (live ? 0x04000400u << e : 0u);
+      }
       return make_uint4(bd[0], bd[1], bd[2], bd[3]);
     };
     // Each group of MFMAs uses a sign operand expanded one group earlier
@@ -783,22 +925,27 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       return;
     }
   }
-  // The forward's per-token range-guard shifts (see prep_stream_kernel) of the
-  // tile's tokens, a table at the end of the LDS (past every staging area
-  // below), filled before the epilogue's stores; the 16 shifts of token
-  // block i for this lane's rows 8(e/4) + 4(l/32) + (e mod 4).
+  // The forward's per-token tables (filled in the prologue, past every
+  // staging area below): the 16 range-guard shifts and row sums of token
+  // block i for this lane's rows 8(e/4) + 4(l/32) + (e mod 4).  A forward
+  // output is (R - 2 acc) 2^shift (see the sign operands).
   constexpr int kRowF = 128 + 4;  // floats per staged fp32 token row
-  constexpr int kShl = kLdsBytes - 4 * kBM;
-  static_assert(kBM * kRowF * 4 <= kShl && kBM * 512 <= kShl, "staging clear of the shifts");
-  auto load_shifts = [&](int i, int (&sv)[16]) {
-    const int *shl = reinterpret_cast<const int *>(lds + kShl);
+  static_assert(kBM * kRowF * 4 <= LM::kTab && kBM * 512 <= LM::kTab, "staging clear of the tables");
+  auto load_tabs = [&](int i, int (&sv)[16], float (&rv)[16]) {
+    const int *shl = reinterpret_cast<const int *>(lds + LM::kTab);
+    const float *rtl = reinterpret_cast<const float *>(lds + LM::kTab + 4 * kBM);
 #pragma unroll
     for (int e4 = 0; e4 < 4; ++e4) {
       const int4 s4 = *reinterpret_cast<const int4 *>(shl + 32 * i + 8 * e4 + 4 * g);
+      const float4 r4 = *reinterpret_cast<const float4 *>(rtl + 32 * i + 8 * e4 + 4 * g);
       sv[4 * e4] = s4.x;
       sv[4 * e4 + 1] = s4.y;
       sv[4 * e4 + 2] = s4.z;
       sv[4 * e4 + 3] = s4.w;
+      rv[4 * e4] = r4.x;
+      rv[4 * e4 + 1] = r4.y;
+      rv[4 * e4 + 2] = r4.z;
+      rv[4 * e4 + 3] = r4.w;
     }
   };
   // A fp32 [T][N] output of the whole tile (a split partial, or the saved
@@ -807,8 +954,9 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   // in 16-byte stores along the columns.  Stored from the accumulator
   // layout (one column per lane) it took 64-128 single-float stores a lane,
   // whose issue alone cost about 2 us per workgroup.  The LDS buffers must
-  // be idle on entry.  shifted: apply the range-guard shifts (the saved z)
-  // or not (a split partial, shifted by its reduction).
+  // be idle on entry.  shifted: the forward output (R - 2 acc) 2^shift (the
+  // saved z) or the raw accumulator (a split partial, finished by its
+  // reduction).
   auto store_f32_tile = [&](float *__restrict__ dst, auto shifted) {
     constexpr bool kShift = decltype(shifted)::value;
     float *stg = reinterpret_cast<float *>(lds);
@@ -818,11 +966,12 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
 #pragma unroll
       for (int i = 0; i < kTokBlocks; ++i) {
         int sv[16] = {};
-        if constexpr (kShift) load_shifts(i, sv);
+        float rv[16] = {};
+        if constexpr (kShift) load_tabs(i, sv, rv);
 #pragma unroll
         for (int e = 0; e < 16; ++e)
           stg[(32 * i + 8 * (e >> 2) + 4 * g + (e & 3)) * kRowF + 32 * wave + (lane & 31)] =
-              kShift ? ldexpf(acc[i][j][e], sv[e]) : acc[i][j][e];
+              kShift ? ldexpf(fmaf(-2.f, acc[i][j][e], rv[e]), sv[e]) : acc[i][j][e];
       }
       __syncthreads();
 #pragma unroll
@@ -854,23 +1003,17 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
   // at position c XOR 4 * ((row / 4) mod 2), so that the two lane halves
   // (tokens four apart) write distinct banks.  kMidSave
   // passes its second output V through the same buffer after C.
+  // rs: the row scale of the lane's column in each block; the first
+  // product's fp16 output also takes the column factor 2^slot_exp(n mod 4)
+  // of the second product's operand (n mod 4 = l mod 4).
   float rs[2];
   int cpos[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int n = wrow0 + 32 * j;
     rs[j] = n < N ? (rowscale ? f16_to_f32(rowscale[n]) : 1.0f) : 0.f;
+    if constexpr (kFirst) rs[j] = ldexpf(rs[j], slot_exp(lane & 3));
     cpos[j] = (kPairOut ? pair_pos(n) : n) - n0;
-  }
-  // The range-guard shift table (see load_shifts).  The shifts are applied
-  // to each value on its way into an output staging (before any rounding),
-  // never to the accumulators in place: shifting in place kept old and new
-  // accumulators live together and spilled registers to scratch.
-  if constexpr (!kBwd) {
-    int *shl = reinterpret_cast<int *>(lds + kShl);
-    for (int q = tid; q < kBM; q += kThreads)
-      shl[q] = t0 + q < T ? fwd_shift<kMode == kMid || kMode == kMidSave>(tinfo, T, t0 + q) : 0;
-    __syncthreads();
   }
   auto stage_tile = [&](auto value) {
 #pragma unroll
@@ -886,7 +1029,12 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     }
     __syncthreads();
   };
-  auto store_tile = [&](uint16_t *__restrict__ dst) {
+  // store_tile(dst, sums): with sums, also the first product's per-tile row
+  // sums of a_k (the stored fp16 value over its column factor; dword e of a
+  // chunk holds columns with factor index e) into RS, a token row's 32
+  // chunks being the 32 lanes of a half wave.
+  auto store_tile = [&](uint16_t *__restrict__ dst, auto sums) {
+    constexpr bool kSums = decltype(sums)::value;
     const int chunk = tid & 31;
     const bool col_ok = n0 + 8 * chunk < N;
 #pragma unroll 4
@@ -895,6 +1043,17 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
                                                        ((chunk ^ (4 * ((row >> 2) & 1))) << 4));
       if (col_ok && t0 + row < T)
         *reinterpret_cast<uint4 *>(dst + (size_t)(t0 + row) * N + n0 + 8 * chunk) = v;
+      if constexpr (kSums) {
+        const uint32_t d[4] = {v.x, v.y, v.z, v.w};
+        float a = 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const _Float16 f = (_Float16)(1.0f / (float)(1 << slot_exp(e)));  // exact
+          a = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2v, d[e]), half2v{f, f}, a, false);
+        }
+        const float rsum = half_wave_sum(a);
+        if (chunk == 0 && t0 + row < T) RS[(size_t)(t0 + row) * rs_ld(N) + n0 / BN] = rsum;
+      }
     }
   };
   if constexpr (kBwd) {
@@ -962,18 +1121,22 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
         if constexpr (kMode == kBwdMid) return f32_to_f16(acc[i][j][e] * rs[j] * fz[i]);
         else return f32_to_bf16(acc[i][j][e] * fg[i] * rs[j]);
       });
-      store_tile(C);
+      store_tile(C, std::false_type{});
     }
     return;
   }
-  // stage_tile with the range-guard shift: value(v, j) of v = the shifted
-  // accumulator, a token block at a time (its 16 shifts read once for both
-  // column blocks)
+  // stage_tile of the forward output: value(v, j) of v = (R - 2 acc) 2^shift,
+  // a token block at a time (its tables read once for both column blocks).
+  // The shifts are applied to each value on its way into the staging
+  // (before any rounding), never to the accumulators in place: shifting in
+  // place kept old and new accumulators live together and spilled registers
+  // to scratch.
   auto stage_shifted = [&](auto value) {
 #pragma unroll
     for (int i = 0; i < kTokBlocks; ++i) {
       int sv[16];
-      load_shifts(i, sv);
+      float rv[16];
+      load_tabs(i, sv, rv);
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const int cbyte = 2 * (cpos[j] & 7), chunk = (cpos[j] >> 3) ^ (4 * g);
@@ -981,7 +1144,7 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
         for (int e = 0; e < 16; ++e) {
           const int row = 32 * i + 8 * (e >> 2) + 4 * g + (e & 3);
           *reinterpret_cast<uint16_t *>(lds + row * 512 + chunk * 16 + cbyte) =
-              value(ldexpf(acc[i][j][e], sv[e]), j);
+              value(ldexpf(fmaf(-2.f, acc[i][j][e], rv[e]), sv[e]), j);
         }
       }
     }
@@ -991,12 +1154,12 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     v *= rs[j];
     return kPairOut ? f32_to_f16(v) : f32_to_bf16(v);
   });
-  store_tile(C);
+  store_tile(C, std::integral_constant<bool, kFirst>{});
   if constexpr (kMode == kMidSave) {
     __syncthreads();
     const int es = smax_exp(tinfo[2 * T]);
     stage_shifted([&](float v, int) { return f32_to_f16(ldexpf(v, es)); });
-    store_tile(V);
+    store_tile(V, std::false_type{});
   }
   if constexpr (kMode == kOutSave) {
     __syncthreads();  // every wave is done reading the staged C tile
@@ -1294,48 +1457,56 @@ __device__ __forceinline__ void sum_partials(const float *__restrict__ base, siz
   }
 }
 
-// What finish8 reads besides the sums: the token's range-guard record and
-// max |s_mid| (kRecord; the kBwdIn reduction has no record and passes no
-// tinfo), and the row scales of the 8 positions (cl .. cl+3 and ch .. ch+3,
-// each run 8-byte aligned).  Loaded before the partial sums and kept raw
-// (nothing computed from them until the sums have arrived), so that their
-// round trip overlaps the sums' instead of following it.
+// What finish8 reads besides the sums: the token's range-guard record, max
+// |s_mid| and the operand's row sum R (kRecord, the forward modes; the
+// kBwdIn reduction has no record and passes no tinfo), and the row scales
+// of the 8 positions (cl .. cl+3 and ch .. ch+3, each run 8-byte aligned).
+// Loaded before the partial sums and kept raw (nothing computed from them
+// until the sums have arrived), so that their round trip overlaps the sums'
+// instead of following it.
 struct Fin8In {
   float2 ti;
-  float smax;
+  float smax, rt;
   uint2 rlo, rhi;
 };
-template <bool kRecord>
+// kR: the row sum to load (0 none, 1 R1, 2 R2).
+template <bool kRecord, int kR>
 __device__ __forceinline__ Fin8In finish8_load(int cl, int ch, int t, int T,
                                                const uint16_t *__restrict__ rowscale,
                                                const float *__restrict__ tinfo) {
   Fin8In in;
   in.ti = make_float2(0.f, 0.f);
-  in.smax = 0.f;
+  in.smax = in.rt = 0.f;
   if constexpr (kRecord) {
     in.ti = reinterpret_cast<const float2 *>(tinfo)[t];
     in.smax = tinfo[2 * T];
   }
+  if constexpr (kR > 0) in.rt = (kR == 1 ? tinfo_r1(tinfo, T) : tinfo_r2(tinfo, T))[t];
   in.rlo = *reinterpret_cast<const uint2 *>(rowscale + cl);
   in.rhi = *reinterpret_cast<const uint2 *>(rowscale + ch);
   return in;
 }
 
 // The forward modes' outputs for 8 consecutive output positions p .. p+7 of
-// token t from their fp32 sums: lo holds columns cl .. cl+3, hi columns
-// ch .. ch+3 (pair order interleaves the two runs, natural order
-// concatenates them).
+// token t from their fp32 accumulator sums: lo holds columns cl .. cl+3, hi
+// columns ch .. ch+3 (pair order interleaves the two runs, natural order
+// concatenates them).  The first product's modes return the sum of their
+// 8 values a_k (the stored fp16 over its column factor) for the row sums
+// of the second product's operand; the others return 0.
 template <int kMode>
-__device__ __forceinline__ void finish8(const float4 &lo, const float4 &hi, const Fin8In &in,
-                                        int p, int t, int N, uint16_t *__restrict__ C,
-                                        uint16_t *__restrict__ V, float *__restrict__ F) {
+__device__ __forceinline__ float finish8(const float4 &lo, const float4 &hi, const Fin8In &in,
+                                         int p, int t, int N, uint16_t *__restrict__ C,
+                                         uint16_t *__restrict__ V, float *__restrict__ F,
+                                         bool live = true) {
   constexpr bool kPairOut = kMode == kMid || kMode == kMidSave;
-  // the token's range-guard shift (see prep_stream_kernel) before any rounding
+  // the token's range-guard shift (see prep_stream_kernel), applied to the
+  // signed product R - 2 acc before any rounding
   const int c_t = mid_exp(in.ti.x, in.smax);
   const int sh = kPairOut ? -c_t : c_t - __float_as_int(in.ti.y);
   const int es = kMode == kMidSave ? smax_exp(in.smax) : 0;
-  const float l4[4] = {ldexpf(lo.x, sh), ldexpf(lo.y, sh), ldexpf(lo.z, sh), ldexpf(lo.w, sh)};
-  const float h4[4] = {ldexpf(hi.x, sh), ldexpf(hi.y, sh), ldexpf(hi.z, sh), ldexpf(hi.w, sh)};
+  auto fin = [&](float a) { return ldexpf(fmaf(-2.f, a, in.rt), sh); };
+  const float l4[4] = {fin(lo.x), fin(lo.y), fin(lo.z), fin(lo.w)};
+  const float h4[4] = {fin(hi.x), fin(hi.y), fin(hi.z), fin(hi.w)};
   float acc[8];
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
@@ -1351,17 +1522,21 @@ __device__ __forceinline__ void finish8(const float4 &lo, const float4 &hi, cons
     rs[2 * k + 1] = f16_hi(rw[k]);
   }
   uint32_t c[4], v[4];
+  float asum = 0.f;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    // pair order: columns (cl + k, ch + k); natural: (p + 2k, p + 2k + 1)
-    // with cl = p, ch = p + 4
-    const float r0 = kPairOut ? rs[k] : rs[2 * k], r1 = kPairOut ? rs[4 + k] : rs[2 * k + 1];
+    // pair order: columns (cl + k, ch + k), column factor index k (cl is a
+    // multiple of 4); natural: (p + 2k, p + 2k + 1) with cl = p, ch = p + 4
+    const float r0 = kPairOut ? ldexpf(rs[k], slot_exp(k)) : rs[2 * k];
+    const float r1 = kPairOut ? ldexpf(rs[4 + k], slot_exp(k)) : rs[2 * k + 1];
     const float a0 = acc[2 * k] * r0, a1 = acc[2 * k + 1] * r1;
     c[k] = kPairOut ? (uint32_t)f32_to_f16(a0) | ((uint32_t)f32_to_f16(a1) << 16)
                     : (uint32_t)f32_to_bf16(a0) | ((uint32_t)f32_to_bf16(a1) << 16);
     v[k] = (uint32_t)f32_to_f16(ldexpf(acc[2 * k], es)) |
            ((uint32_t)f32_to_f16(ldexpf(acc[2 * k + 1], es)) << 16);
+    if constexpr (kPairOut) asum += ldexpf(f16_lo(c[k]) + f16_hi(c[k]), -slot_exp(k));
   }
+  if (!live) return 0.f;
   const size_t o = (size_t)t * N + p;
   *reinterpret_cast<uint4 *>(C + o) = make_uint4(c[0], c[1], c[2], c[3]);
   if constexpr (kMode == kMidSave)
@@ -1370,13 +1545,24 @@ __device__ __forceinline__ void finish8(const float4 &lo, const float4 &hi, cons
     *reinterpret_cast<float4 *>(F + o) = make_float4(l4[0], l4[1], l4[2], l4[3]);
     *reinterpret_cast<float4 *>(F + o + 4) = make_float4(h4[0], h4[1], h4[2], h4[3]);
   }
+  return asum;
+}
+
+
+// Output units (8 positions) per token row of a split-K reduction: the
+// first product's rows are padded to whole 256-column tiles (32 units, a
+// half wave, whose row sum goes to RS), the second's are not.
+__host__ __device__ constexpr int64_t reduce_units_per_row(bool first, int64_t N) {
+  return first ? (N + 255) / 256 * 32 : N / 8;
 }
 
 // The reduction of a split-K contraction (forward modes): C and its
 // companions from the S fp32 partials of the workgroups along K, added in
 // split order.  A thread takes 8 consecutive output positions of one token:
 // in pair order (kMid, kMidSave) positions 8u .. 8u+7 of a 32-column group
-// hold columns c0 .. c0+3 and c0+16 .. c0+19, interleaved.
+// hold columns c0 .. c0+3 and c0+16 .. c0+19, interleaved; there the 32
+// threads of a 256-column tile also add their values a_k for the tile's row
+// sum in RS (threads past N add zero and store nothing).
 template <int kMode, int kBatch>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *__restrict__ P, int S,
                                                             int T, int N,
@@ -1384,25 +1570,32 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float *__restr
                                                             uint16_t *__restrict__ C,
                                                             uint16_t *__restrict__ V,
                                                             float *__restrict__ F,
-                                                            const float *__restrict__ tinfo) {
+                                                            float *__restrict__ tinfo,
+                                                            float *__restrict__ RS) {
   constexpr bool kPairOut = kMode == kMid || kMode == kMidSave;
   const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int upr = N / 8;
-  if (u >= (int64_t)T * upr) return;
+  const int upr = (int)reduce_units_per_row(kPairOut, N);
+  if (u >= (int64_t)T * upr) return;  // whole half waves (upr is a multiple of 32 in pair order)
   const int t = (int)(u / upr);
   const int p = (int)(u % upr) * 8;  // first output position
+  const bool live = p < N;
+  const int pc = live ? p : 0;       // loads stay inside the arrays
   int cl, ch;                        // columns of the two float4 runs
   if (kPairOut) {
-    cl = (p & ~31) + ((p & 31) >> 1);
+    cl = (pc & ~31) + ((pc & 31) >> 1);
     ch = cl + 16;
   } else {
-    cl = p;
-    ch = p + 4;
+    cl = pc;
+    ch = pc + 4;
   }
-  const Fin8In in = finish8_load<true>(cl, ch, t, T, rowscale, tinfo);
+  const Fin8In in = finish8_load<true, kPairOut ? 1 : 2>(cl, ch, t, T, rowscale, tinfo);
   float4 lo, hi;
   sum_partials<kBatch>(P + (size_t)t * N, (size_t)T * N, S, cl, ch, lo, hi);
-  finish8<kMode>(lo, hi, in, p, t, N, C, V, F);
+  const float a = finish8<kMode>(lo, hi, in, pc, t, N, C, V, F, live);
+  if constexpr (kPairOut) {
+    const float rsum = half_wave_sum(a);
+    if ((u & 31) == 0) RS[(size_t)t * rs_ld(N) + p / 256] = rsum;
+  }
 }
 
 // The reduction of a mixed grid (forward modes): for each tile cut into
@@ -1417,15 +1610,19 @@ __global__ __launch_bounds__(256) void mixed_reduce_kernel(const float *__restri
                                                            uint16_t *__restrict__ C,
                                                            uint16_t *__restrict__ V,
                                                            float *__restrict__ F,
-                                                           const float *__restrict__ tinfo) {
+                                                           float *__restrict__ tinfo,
+                                                           float *__restrict__ RS) {
   constexpr bool kPairOut = kMode == kMid || kMode == kMidSave;
   const int h = blockIdx.x >> 4;
   const int unit = ((blockIdx.x & 15) << 8) + threadIdx.x;  // 0 .. 4095
-  const int row = unit >> 5, pl = (unit & 31) * 8;          // token row, first position
+  const int row = unit >> 5, ps = (unit & 31) * 8;          // token row, first position
   const int L = full + h;
   const int t = (L / nN) * BM + row;
   const int n0 = (L % nN) * BN;
-  if (t >= T || n0 + pl >= N) return;
+  if (t >= T) return;  // a whole half wave (one token row)
+  // positions past N add zero to the row sum and store nothing
+  const bool live = n0 + ps < N;
+  const int pl = live ? ps : 0;
   int cl, ch;  // tile-local columns of the two float4 runs
   if (kPairOut) {
     cl = (pl & ~31) + ((pl & 31) >> 1);
@@ -1434,7 +1631,7 @@ __global__ __launch_bounds__(256) void mixed_reduce_kernel(const float *__restri
     cl = pl;
     ch = pl + 4;
   }
-  const Fin8In in = finish8_load<true>(n0 + cl, n0 + ch, t, T, rowscale, tinfo);
+  const Fin8In in = finish8_load<true, kPairOut ? 1 : 2>(n0 + cl, n0 + ch, t, T, rowscale, tinfo);
   float4 lo = make_float4(0.f, 0.f, 0.f, 0.f), hi = lo;
   float4 a[4], b[4];
   const float *base = P + (size_t)h * S * (BM * BN) + row * BN;
@@ -1457,7 +1654,11 @@ __global__ __launch_bounds__(256) void mixed_reduce_kernel(const float *__restri
     hi.z += use ? b[q].z : 0.f;
     hi.w += use ? b[q].w : 0.f;
   }
-  finish8<kMode>(lo, hi, in, n0 + pl, t, N, C, V, F);
+  const float asum = finish8<kMode>(lo, hi, in, n0 + pl, t, N, C, V, F, live);
+  if constexpr (kPairOut) {
+    const float rsum = half_wave_sum(asum);
+    if ((unit & 31) == 0) RS[(size_t)t * rs_ld(N) + L % nN] = rsum;
+  }
 }
 
 // The reduction of a split-K backward contraction.  A workgroup takes 64
@@ -1493,7 +1694,7 @@ __global__ __launch_bounds__(256) void splitk_bwd_reduce_kernel(
     // the operands of the epilogue first (their round trip overlaps the sums')
     const float2 gs = reinterpret_cast<const float2 *>(gscale)[t >> 6];
     const uint4 sq = *reinterpret_cast<const uint4 *>(Sv + (size_t)t * N + p);
-    const Fin8In in = finish8_load<kMode == kBwdMid>(cl, ch, t, T, rowscale, tinfo);
+    const Fin8In in = finish8_load<kMode == kBwdMid, 0>(cl, ch, t, T, rowscale, tinfo);
     float4 lo, hi;
     sum_partials<kBatch>(P + (size_t)t * N, (size_t)T * N, S, cl, ch, lo, hi);
     const float fg = kMode == kBwdMid ? gs.x : gs.x / gs.y;
@@ -1655,12 +1856,17 @@ size_t split_bytes(const ContractionPlan &p, int64_t T, int64_t N) {
 // One contraction C[T, N] over K on the stream.  P: fp32 workspace for a
 // split K (nullptr never splits).  *tile_tokens receives the token count
 // per row of F's per-tile sums (the token-tile height, or 64 when split).
+// Forward modes: tinfo is the range-guard record (the second product
+// stores R2 into it) and RS the first product's per-tile row sums, written
+// by the first product and read by the second.  The backward only reads
+// tinfo.
 template <int kMode>
 hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *W, int64_t N,
                        const uint16_t *rs, uint16_t *C, uint16_t *V, const uint16_t *S,
                        float *F, hipStream_t s, int *tile_tokens = nullptr,
                        const float *gscale = nullptr, float *P = nullptr,
-                       const float *tinfo = nullptr) {
+                       const float *tinfo_in = nullptr, float *RS = nullptr) {
+  float *tinfo = const_cast<float *>(tinfo_in);
   constexpr bool kFwd = kMode == kMid || kMode == kMidSave || kMode == kOut || kMode == kOutSave;
   const ContractionPlan p = plan_contraction(T, K, N, P != nullptr, device_cus(), kFwd && P);
   if (p.splits > 1 && p.bm != 64) return hipErrorInvalidValue;  // see bingemm_kernel
@@ -1671,17 +1877,17 @@ hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *
   if (p.bm == 64)
     bingemm_kernel<kMode, 64, kStages64><<<g, kThreads, Lds<64, kStages64>::kBytes, s>>>(
         A, (int)T, (int)K, W, (int)N, rs, C, V, S, F, gscale, p.split_steps, P, p.mix_full,
-        p.mix_splits, (int)p.gx, tinfo);
+        p.mix_splits, (int)p.gx, tinfo, RS);
   else
     bingemm_kernel<kMode, BM, kStages128><<<g, kThreads, Lds<BM, kStages128>::kBytes, s>>>(
         A, (int)T, (int)K, W, (int)N, rs, C, V, S, F, gscale, p.split_steps, P, p.mix_full,
-        p.mix_splits, (int)p.gx, tinfo);
+        p.mix_splits, (int)p.gx, tinfo, RS);
   if (tile_tokens) *tile_tokens = p.splits > 1 ? 64 : p.bm;
   if (p.mix_full > 0) {
     if constexpr (kFwd) {
       const unsigned blocks = (unsigned)((tiles - p.mix_full) * 16);
       mixed_reduce_kernel<kMode><<<blocks, 256, 0, s>>>(P, p.mix_splits, p.mix_full, (int)p.gx,
-                                                         (int)T, (int)N, rs, C, V, F, tinfo);
+                                                         (int)T, (int)N, rs, C, V, F, tinfo, RS);
     } else {
       return hipErrorInvalidValue;  // planned for the forward modes only
     }
@@ -1704,11 +1910,11 @@ hipError_t contraction(const uint16_t *A, int64_t T, int64_t K, const uint32_t *
       // 256-thread blocks runs 64-thread blocks: the partial loads of a few
       // blocks are limited per unit (4096^2 at 64 tokens: 30.5 us a call
       // against 33.7 with 256-thread blocks throughout).
-      const int64_t units = T * (N / 8);
+      const int64_t units = T * reduce_units_per_row(kMode == kMid || kMode == kMidSave, N);
       const int rt = (units + 255) / 256 <= device_cus() / 2 ? 64 : 256;
       auto go = [&](auto kernel) {
         kernel<<<(unsigned)((units + rt - 1) / rt), rt, 0, s>>>(P, p.splits, (int)T, (int)N, rs,
-                                                               C, V, F, tinfo);
+                                                               C, V, F, tinfo, RS);
       };
       if (p.splits <= 4)
         go(splitk_reduce_kernel<kMode, 4>);
@@ -1761,9 +1967,12 @@ hipError_t prepare_forward(int64_t n, const uint16_t *s_in, const uint16_t *x, i
 
 size_t tinfo_bytes(int64_t T) { return align256((size_t)tinfo_floats(T) * 4); }
 
+size_t rowsum_bytes(int64_t r, int64_t T) { return align256((size_t)T * rs_ld(r) * 4); }
+
 struct FwdWs {
   uint16_t *xp, *Z;
   float *tinfo;  // the per-token range-guard record
+  float *RS;     // G1's per-tile row sums of Z
   float *P;      // split-K partials of G1 or G2 (one at a time)
 };
 
@@ -1776,6 +1985,8 @@ FwdWs forward_ws(void *ws, int64_t n, int64_t r, int64_t T) {
   base += align256((size_t)T * r * 2);
   w.tinfo = reinterpret_cast<float *>(base);
   base += tinfo_bytes(T);
+  w.RS = reinterpret_cast<float *>(base);
+  base += rowsum_bytes(r, T);
   w.P = reinterpret_cast<float *>(base);
   return w;
 }
@@ -1832,7 +2043,7 @@ size_t gemm_workspace_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
   const size_t p2 = split_bytes(g2, T, m) > mixed_bytes(g2, T, m) ? split_bytes(g2, T, m)
                                                                    : mixed_bytes(g2, T, m);
   return align256((size_t)T * (size_t)n * 2) + align256((size_t)T * (size_t)r * 2) +
-         tinfo_bytes(T) + (p1 > p2 ? p1 : p2);
+         tinfo_bytes(T) + rowsum_bytes(r, T) + (p1 > p2 ? p1 : p2);
 }
 
 hipError_t launch_gemm(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
@@ -1848,10 +2059,10 @@ hipError_t launch_gemm(int64_t m, int64_t n, int64_t r, const uint32_t *Bu,
   hipError_t e = prepare_forward(n, s_in, x, T, w.xp, w.tinfo, s_mid, r, s);
   if (e != hipSuccess) return e;
   e = contraction<kMid>(w.xp, T, n, Bv, r, s_mid, w.Z, nullptr, nullptr, nullptr, s, nullptr,
-                        nullptr, w.P, w.tinfo);
+                        nullptr, w.P, w.tinfo, w.RS);
   if (e != hipSuccess) return e;
   return contraction<kOut>(w.Z, T, r, Bu, m, s_out, y, nullptr, nullptr, nullptr, s, nullptr,
-                           nullptr, w.P, w.tinfo);
+                           nullptr, w.P, w.tinfo, w.RS);
 }
 
 size_t train_saved_bytes(int64_t m, int64_t n, int64_t r, int64_t T) {
@@ -1886,10 +2097,10 @@ hipError_t launch_forward_train(int64_t m, int64_t n, int64_t r, const uint32_t 
   // the same G1 as the inference forward, which also keeps fp16(v) at the
   // token's scale
   e = contraction<kMidSave>(w.xp, T, n, Bv, r, s_mid, w.Z, v, nullptr, nullptr, s, nullptr,
-                            nullptr, w.P, tinfo);
+                            nullptr, w.P, tinfo, w.RS);
   if (e != hipSuccess) return e;
   return contraction<kOutSave>(w.Z, T, r, Bu, m, s_out, y, nullptr, nullptr, z, s, nullptr,
-                               nullptr, w.P, tinfo);
+                               nullptr, w.P, tinfo, w.RS);
 }
 
 hipError_t launch_backward(int64_t m, int64_t n, int64_t r, const uint32_t *BuT,

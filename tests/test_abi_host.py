@@ -161,15 +161,18 @@ def test_gemm_token_and_workspace_validation():
 
 
 def test_gemm_workspace_holds_split_partials_only_for_few_tokens():
-    """The GEMM workspace is fp16(s_in .* x), Z and the per-token range-guard
-    record (two floats a token and four more, each part 256-byte aligned),
-    plus fp32 partials when a contraction splits its K steps, which happens
-    only when the tile grid leaves compute units idle (here no GPU is
-    present and the library plans for 256 compute units)."""
+    """The GEMM workspace is fp16(s_in .* x), Z, the per-token range-guard
+    record (four floats a token and four more) and the first product's row
+    sums of Z per 256-column tile (a row padded to a multiple of 4 floats),
+    each part 256-byte aligned, plus fp32 partials when a contraction splits
+    its K steps, which happens only when the tile grid leaves compute units
+    idle (here no GPU is present and the library plans for 256 compute
+    units)."""
     a = lambda v: (v + 255) // 256 * 256
     m = n = 4096
     r = 2016
-    base = lambda T: a(T * n * 2) + a(T * r * 2) + a((2 * T + 4) * 4)
+    ld = ((r + 255) // 256 + 3) // 4 * 4
+    base = lambda T: a(T * n * 2) + a(T * r * 2) + a((4 * T + 4) * 4) + a(T * ld * 4)
     assert af1.af1_gemm_workspace_bytes(m, n, r, 2048) == base(2048)
     few = af1.af1_gemm_workspace_bytes(m, n, r, 64)
     assert few > base(64)
