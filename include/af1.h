@@ -254,23 +254,28 @@ AF1_API af1_status af1_linear_stream(const void *plan, const void *plan_dev, voi
  *        kernels address operands with 32-bit byte offsets); otherwise
  *        AF1_ERR_BATCH.  A sign matrix of 2 GiB or more is AF1_ERR_SHAPE.
  *   ws : device workspace of at least af1_gemm_workspace_bytes(m, n, r, T)
- *        bytes; holds the fp16 operand s_in .* x, the [T, r] intermediate
- *        and, for token counts whose tile grid would leave compute units
- *        idle, the fp32 partial sums of a contraction split along K (added
- *        in a fixed order, so results repeat bit for bit).  The size depends
- *        on the current device's compute-unit count.
- * Arithmetic: both products run on fp16 MFMA with fp32 accumulation against
- * exact +-1 sign operands; each scale vector is applied outside them.
- * s_in .* x is rounded once to fp16 (the bf16 x fp16 product is exact in
- * fp32), the intermediate s_mid .* (Bv (s_in .* x)) is rounded once to fp16
- * before the second product, s_out is applied in fp32 and y is rounded to
- * bfloat16.  Range: each token's two fp16 operands carry a power of two
- * chosen from that token alone (its largest |s_in .* x| for the first, the
- * bound sum_j |s_in_j x_j| * max|s_mid| on the intermediate for the
- * second), undone in fp32 before s_out, so no fp16 operand overflows or
- * goes subnormal for any finite bf16 x: the GEMM is defined on the same
- * inputs as the GEMV.  Entries below 2^-27 of their token's largest one
- * keep fewer digits, as in any fp16 rounding.
+ *        bytes; holds the fp16 operand s_in .* x, the [T, r] intermediate,
+ *        a per-token record and the intermediate's per-tile row sums, and,
+ *        for token counts whose tile grid would leave compute units idle,
+ *        the fp32 partial sums of a contraction split along K (added in a
+ *        fixed order, so results repeat bit for bit).  The size depends on
+ *        the current device's compute-unit count.
+ * Arithmetic: both products run on fp16 MFMA with fp32 accumulation and
+ * exact products; each scale vector is applied outside them.  The sign
+ * operand holds, per sign, zero (+1) or a single fp16 exponent bit (-1),
+ * the activation operand the matching power of two, and the signed sum is
+ * formed in fp32 as R - 2 acc with R the token's row sum of the operand,
+ * so each product equals the sum of the fp16 operand times exact +-1 signs
+ * up to fp32 rounding.  s_in .* x is rounded once to fp16 (the bf16 x fp16
+ * product is exact in fp32), the intermediate s_mid .* (Bv (s_in .* x)) is
+ * rounded once to fp16 before the second product, s_out is applied in fp32
+ * and y is rounded to bfloat16.  Range: each token's two fp16 operands
+ * carry a power of two chosen from that token alone (its largest
+ * |s_in .* x| for the first, the bound sum_j |s_in_j x_j| * max|s_mid| on
+ * the intermediate for the second), undone in fp32 before s_out, so no
+ * fp16 operand overflows for any finite bf16 x: the GEMM is defined on the
+ * same inputs as the GEMV.  Entries below about 2^-20 of their token's
+ * largest one keep fewer digits, as in any fp16 rounding.
  * Defining passage: App. A.2.1 (Diag form, label eq:double_factor_equiv)
  * and Sec. 4.1 (label eq:final_reconstruction), as for af1_linear_gemv.
  */
