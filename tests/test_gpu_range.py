@@ -223,3 +223,43 @@ def test_gemm_prep_several_tokens_per_worker(oracle, n, T):
     lin = synth.make_linear(4900 + n, m, n, r, T)
     x = scaled_x(lin.x, token_factors(4901 + n, T))
     check(oracle, lin, x, run("gemm", lin, x))
+
+
+def biased_words(seed, rows, cols, p):
+    """Packed sign words whose bits are set with probability p (bit j of word
+    w is column 32 w + j)."""
+    bits = np.random.default_rng(seed).random((rows, cols)) < p
+    return np.packbits(bits, axis=1, bitorder="little").view(np.uint32).reshape(rows, cols // 32)
+
+
+@pytest.mark.parametrize("offset", [40.0, 1000.0], ids=["mean40sd", "mean1000sd"])
+@pytest.mark.parametrize("p", [0.5, 0.1, 0.9], ids=["fair", "bits0.1", "bits0.9"])
+@pytest.mark.parametrize("m,n,r,T", [(4096, 4096, 2016, 64), (4096, 4096, 2016, 17)])
+def test_gemm_offset_activations_and_biased_signs(oracle, offset, p, m, n, r, T):
+    """Activations with a common offset far above their spread (x = offset +
+    N(0,1), every entry positive) and sign matrices with biased bits.  The
+    forward forms each signed sum as R - 2 acc from the operand's row sum R
+    and the sum over set bits acc; with fair signs both are about sqrt(K)
+    times the result, the case where fp32 cancellation would show."""
+    lin = synth.make_linear(4800 + T, m, n, r, T)
+    lin.Bv = biased_words(4801, r, n, p)
+    lin.Bu = biased_words(4802, m, r, p)
+    z = np.random.default_rng(4803).standard_normal((T, n))
+    x = synth.f32_to_bf16_bits((offset + z).astype(np.float32))
+    check(oracle, lin, x, run("gemm", lin, x))
+
+
+@pytest.mark.parametrize("offset", [40.0, 1000.0], ids=["mean40sd", "mean1000sd"])
+def test_gemm_offset_activations_8192(oracle, offset):
+    """The same offset activations through 8192x8192 at 2048 tokens (K =
+    8192 in the first product, 64-token tiles), fair signs, on a seeded
+    sample of tokens."""
+    m, n, r = synth.SHAPES["sq8192"]
+    T = 2048
+    lin = synth.make_linear(4900, m, n, r, T)
+    z = np.random.default_rng(4901).standard_normal((T, n))
+    x = synth.f32_to_bf16_bits((offset + z).astype(np.float32))
+    y = run("gemm", lin, x)
+    idx = np.sort(np.random.default_rng(4902).choice(np.arange(1, T - 1), 6, replace=False))
+    idx = np.concatenate([[0], idx, [T - 1]])
+    check(oracle, lin, x, y, idx)
