@@ -859,31 +859,65 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
       }
       return make_uint4(bd[0], bd[1], bd[2], bd[3]);
     };
-    // Each group of MFMAs uses a sign operand expanded one group earlier
-    // (block 1's of step ks while block 0's MFMAs of ks run, block 0's of
-    // ks + 1 while block 1's run), and the next step's LDS reads are issued
-    // ahead too; the scheduling barriers keep that order, so no MFMA waits
-    // on the instructions just before it.
+    // Each group of MFMAs uses sign operands expanded one group earlier, and
+    // the next step's LDS reads are issued ahead too; the scheduling
+    // barriers keep that order, so no MFMA waits on the instructions just
+    // before it.  128-token tiles: both blocks' operands of step ks are
+    // ready before its first MFMA, those of ks + 1 are expanded between its
+    // two halves, and the MFMAs go token block by token block, so each
+    // activation operand meets both sign operands back to back (0.3-1.7%
+    // faster than block by block under the power limit; slower with
+    // 64-token tiles).  64-token tiles: block 1's operand of step ks is
+    // expanded while block 0's MFMAs of ks run, block 0's of ks + 1 while
+    // block 1's run.
+    auto mfma = [&](int i, int j, int slot, const uint4 &b) {
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
+          af[slot][i], __builtin_bit_cast(half8, b), acc[i][j], 0, 0, 0);
+    };
     read_ops(0, 0);
-    uint4 b0 = expand(0, 0), b1;
-    static_for<2 * kWords>([&](auto KS) {
-      constexpr int ks = decltype(KS)::value;
-      constexpr int cur = ks & 1;
-      if constexpr (ks + 1 < 2 * kWords) read_ops(ks + 1, cur ^ 1);
-      b1 = expand(ks, 1);
-      __builtin_amdgcn_sched_barrier(0);
+    if constexpr (kTokBlocks == 4) {
+      uint4 b0 = expand(0, 0), b1 = expand(0, 1), n0, n1;
+      static_for<2 * kWords>([&](auto KS) {
+        constexpr int ks = decltype(KS)::value;
+        constexpr int cur = ks & 1;
+        if constexpr (ks + 1 < 2 * kWords) read_ops(ks + 1, cur ^ 1);
+        __builtin_amdgcn_sched_barrier(0);
+        mfma(0, 0, cur, b0);
+        mfma(0, 1, cur, b1);
+        mfma(1, 0, cur, b0);
+        mfma(1, 1, cur, b1);
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (ks + 1 < 2 * kWords) {
+          n0 = expand(ks + 1, 0);
+          n1 = expand(ks + 1, 1);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        mfma(2, 0, cur, b0);
+        mfma(2, 1, cur, b1);
+        mfma(3, 0, cur, b0);
+        mfma(3, 1, cur, b1);
+        if constexpr (ks + 1 < 2 * kWords) {
+          b0 = n0;
+          b1 = n1;
+        }
+      });
+    } else {
+      uint4 b0 = expand(0, 0), b1;
+      static_for<2 * kWords>([&](auto KS) {
+        constexpr int ks = decltype(KS)::value;
+        constexpr int cur = ks & 1;
+        if constexpr (ks + 1 < 2 * kWords) read_ops(ks + 1, cur ^ 1);
+        b1 = expand(ks, 1);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int i = 0; i < kTokBlocks; ++i)
-        acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
-            af[cur][i], __builtin_bit_cast(half8, b0), acc[i][0], 0, 0, 0);
-      __builtin_amdgcn_sched_barrier(0);
-      if constexpr (ks + 1 < 2 * kWords) b0 = expand(ks + 1, 0);
-      __builtin_amdgcn_sched_barrier(0);
+        for (int i = 0; i < kTokBlocks; ++i) mfma(i, 0, cur, b0);
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (ks + 1 < 2 * kWords) b0 = expand(ks + 1, 0);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int i = 0; i < kTokBlocks; ++i)
-        acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
-            af[cur][i], __builtin_bit_cast(half8, b1), acc[i][1], 0, 0, 0);
-    });
+        for (int i = 0; i < kTokBlocks; ++i) mfma(i, 1, cur, b1);
+      });
+    }
     // the next step's copies must have landed; with three stages the
     // copies of the step after it may stay in flight
     if (kStages == 3 && step + 2 < nk)
@@ -1038,7 +1072,8 @@ __global__ __launch_bounds__(kThreads, 2) void bingemm_kernel(
     const int chunk = tid & 31;
     const bool col_ok = n0 + 8 * chunk < N;
 #pragma unroll 4
-    for (int row = tid >> 5; row < kBM; row += kThreads / 32) {
+    for (int it = 0; it < kBM / (kThreads / 32); ++it) {
+      const int row = (tid >> 5) + it * (kThreads / 32);
       const uint4 v = *reinterpret_cast<const uint4 *>(lds + row * 512 +
                                                        ((chunk ^ (4 * ((row >> 2) & 1))) << 4));
       if (col_ok && t0 + row < T)
