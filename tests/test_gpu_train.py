@@ -234,7 +234,9 @@ def test_backward_bench_size_dx_rows_and_token_additivity(oracle):
     shape is pinned to the oracle by the tests above).  The 64-token calls
     split their K steps over several workgroups where the full call does not,
     so a forward intermediate rounded to fp16 may land one unit apart
-    (2^-10 relative) between the two; the bar allows for those."""
+    (2^-10 relative) between the two.  Measured 1.0-1.1e-5 relative L2 on
+    the three gradients (the same every run: both paths add in fixed
+    orders); the bar, 3e-5, leaves a factor of about 2.7."""
     m, n, r = synth.SHAPES["sq8192"]
     T = 2048
     lin = synth.make_linear(101, m, n, r, T)
@@ -254,8 +256,10 @@ def test_backward_bench_size_dx_rows_and_token_additivity(oracle):
         L.backward(xs, d_dy[c0:c0 + chunk].contiguous(), sv, grads=tuple(total),
                    accumulate=True, ws=ws, want_dx=False)
     torch.cuda.synchronize()
-    for g, t in zip(grads, total):
-        assert rel_l2(f32(g), f32(t)) <= 1e-4
+    errs = [rel_l2(f32(g), f32(t)) for g, t in zip(grads, total)]
+    print("additivity rel-L2 (ds_out, ds_mid, ds_in):", errs, flush=True)
+    for e in errs:
+        assert e <= 3e-5
 
 
 def test_training_step_replays_in_a_hip_graph():
