@@ -68,8 +68,12 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 // What one launch of the contraction computes (the A operand, the sign
-// words and the tiling are the same in all of them; the B operand is +-1).
-//   kMid     forward G1: C = fp16(rowscale * acc), pair order.
+// words and the tiling are the same in all of them).  acc is the signed
+// product: in the forward modes R - 2 x (the MFMA sum over set sign bits,
+// see the sign operands below), scaled by the token's range-guard shift; in
+// the backward modes the MFMA sum against +-1 operands.
+//   kMid     forward G1: C = fp16(rowscale * acc) times the column factors,
+//            pair order, and the per-tile row sums of C into RS.
 //   kMidSave kMid, and V = fp16(acc) (pair order) for the backward.
 //   kOut     forward G2: C = bf16(rowscale * acc).
 //   kOutSave kOut, and F = acc (fp32, natural order) for the backward.
