@@ -41,6 +41,7 @@
 // so the result is deterministic.
 #include <atomic>
 #include <cstring>
+#include <mutex>
 #include <utility>
 #include <vector>
 
@@ -75,7 +76,13 @@ constexpr int kSlot = 144;
 __host__ __device__ constexpr int row_stride(int w_count) {
   return w_count * kSlot + ((w_count & 1) ? 0 : 16);
 }
-constexpr int kLdsBudget = 160 * 1024;  // LDS of one gfx950 compute unit
+constexpr int kLdsPerCu = 160 * 1024;  // LDS of one gfx950 compute unit
+// Dynamic LDS a stage workgroup may request: the compute unit's LDS less a
+// reserve for the kernels' own __shared__ variables (16 bytes in the stage
+// kernels, 32 in the stream kernel), which the launch adds to the dynamic
+// size.  launch_fits() checks the sum before every launch.
+constexpr int kStaticLdsReserve = 256;
+constexpr int kLdsBudget = kLdsPerCu - kStaticLdsReserve;
 // Cross-wave sums: each wave's 64 lanes x 16 bytes, one 16-byte pad after
 // every 16 lanes, so that the 4 rows x 16 columns read by consecutive
 // output threads spread over the banks.
@@ -806,6 +813,26 @@ size_t lds_bytes_for(int64_t b, int slab_words) {
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
+// Static LDS (the kernel's __shared__ variables) of a kernel, looked up once.
+int static_lds_bytes(const void *fn) {
+  static std::mutex mu;
+  static std::vector<std::pair<const void *, int>> known;
+  std::lock_guard<std::mutex> lock(mu);
+  for (const auto &e : known)
+    if (e.first == fn) return e.second;
+  hipFuncAttributes a{};
+  const int bytes = hipFuncGetAttributes(&a, fn) == hipSuccess ? (int)a.sharedSizeBytes : -1;
+  known.emplace_back(fn, bytes);
+  return bytes;
+}
+
+// A launch requests the kernel's static LDS plus `dynamic`; both must fit
+// one compute unit, or no workgroup could ever be placed.
+bool launch_fits(const void *fn, size_t dynamic) {
+  const int st = static_lds_bytes(fn);
+  return st >= 0 && (size_t)st + dynamic <= (size_t)kLdsPerCu;
+}
+
 // How one stage is split over workgroups.
 //  rt_log2: rows per workgroup = 16 << rt_log2.  More rows per workgroup
 //    share one staged copy of the input (its conversion and its reads are
@@ -937,23 +964,18 @@ hipError_t launch_stage(const StageArgs &a, const StagePlan &p, hipStream_t s) {
       lds = stage + kRedBytes;
     }
   }
-  auto go = [&](auto kernel) {
+  auto go = [&](auto kernel) -> hipError_t {
+    if (!launch_fits(reinterpret_cast<const void *>(kernel), lds)) return hipErrorInvalidValue;
     kernel<<<grid, kThreads, lds, s>>>(a.M, a.in, a.s_in, a.row_scale, a.rows, a.wpr,
                                        p.slab_words, a.b, p.rt_log2, p.nslabs, p.mode,
                                        a.in_parts, a.out, a.part, a.cnt, red_off);
+    return hipGetLastError();
   };
-  if (a.b <= 8) {
-    if (multi)
-      go(gemv_stage_kernel<kInX, kOutY, true, true>);
-    else
-      go(gemv_stage_kernel<kInX, kOutY, true, false>);
-  } else {
-    if (multi)
-      go(gemv_stage_kernel<kInX, kOutY, false, true>);
-    else
-      go(gemv_stage_kernel<kInX, kOutY, false, false>);
-  }
-  return hipGetLastError();
+  if (a.b <= 8)
+    return multi ? go(gemv_stage_kernel<kInX, kOutY, true, true>)
+                 : go(gemv_stage_kernel<kInX, kOutY, true, false>);
+  return multi ? go(gemv_stage_kernel<kInX, kOutY, false, true>)
+               : go(gemv_stage_kernel<kInX, kOutY, false, false>);
 }
 
 template <bool kInX, bool kOutY>
@@ -961,22 +983,17 @@ hipError_t launch_segs(const Segs &sg, const StagePlan &p, int b, int max_wpr, i
                        hipStream_t s) {
   const size_t lds = lds_bytes_for(b, p.slab_words < max_wpr ? p.slab_words : max_wpr);
   dim3 grid((unsigned)sg.group_end[sg.count - 1], (unsigned)p.nslabs);
-  auto go = [&](auto kernel) {
+  auto go = [&](auto kernel) -> hipError_t {
+    if (!launch_fits(reinterpret_cast<const void *>(kernel), lds)) return hipErrorInvalidValue;
     kernel<<<grid, kThreads, lds, s>>>(sg, p.slab_words, b, p.rt_log2, p.mode, in_parts);
+    return hipGetLastError();
   };
   const bool multi = p.rt_log2 > 0;
-  if (b <= 8) {
-    if (multi)
-      go(gemv_segs_kernel<kInX, kOutY, true, true>);
-    else
-      go(gemv_segs_kernel<kInX, kOutY, true, false>);
-  } else {
-    if (multi)
-      go(gemv_segs_kernel<kInX, kOutY, false, true>);
-    else
-      go(gemv_segs_kernel<kInX, kOutY, false, false>);
-  }
-  return hipGetLastError();
+  if (b <= 8)
+    return multi ? go(gemv_segs_kernel<kInX, kOutY, true, true>)
+                 : go(gemv_segs_kernel<kInX, kOutY, true, false>);
+  return multi ? go(gemv_segs_kernel<kInX, kOutY, false, true>)
+               : go(gemv_segs_kernel<kInX, kOutY, false, false>);
 }
 
 // Several layers sharing n in two launches: the stage plans are made for
@@ -1624,6 +1641,7 @@ hipError_t launch_stream(const void *plan_dev, const void *plan_host, hipStream_
   const int cus = device_cus();
   const size_t lds = (size_t)h->lds_bytes;
   auto go = [&](auto kernel) -> hipError_t {
+    if (!launch_fits(reinterpret_cast<const void *>(kernel), lds)) return hipErrorInvalidValue;
     int per_cu = 0;
     hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kStreamThreads,
                                                                 lds);
