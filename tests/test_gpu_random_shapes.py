@@ -15,8 +15,9 @@ the named-shape tests: decode outputs element-wise within
 within 2^-6 |ref| + 6e-3 rms(ref) (two fp16 operand roundings) and 5e-3;
 training dx within relative L2 5e-3 per token and each scale gradient
 within the larger of 1e-3 relative and four times the error predicted by a
-first-order model of the path's fp16 roundings (at short contractions the
-roundings alone reach 1e-3).  Where the decode workspace fits the
+first-order model of the path's fp16 roundings (tests/rounding_model.py,
+calibrated on the CPU; at short contractions the roundings alone reach
+1e-3).  Where the decode workspace fits the
 library's own array, the allocation-free entry point must give the same
 bits as af1_linear_gemv."""
 import numpy as np
@@ -26,12 +27,12 @@ import torch
 from paper_2609_06161_amd import af1, synth
 from paper_2609_06161_amd.layer import (DeviceLayer, LayerStream, bf16_bits_to_f64,
                                         gemv_multi, to_device)
+from rounding_model import rounding_noise
 
 pytestmark = pytest.mark.gpu
 
 TOL = 5e-3
 GRAD_TOL = 1e-3
-U2 = (2.0 ** -11) ** 2 / 3   # variance of one round-to-nearest fp16 relative error
 
 
 def _draw_cases(seed=20261202):
@@ -179,36 +180,6 @@ def run_stream(oracle, c):
     for k, ((_, x, y, _), lin) in enumerate(zip(entries, lins)):
         xin = x.detach().cpu().numpy().view(np.uint16)
         check_decode(bf16_bits_to_f64(y), oracle_y(oracle, lin, xin), ("item", k))
-
-
-def f16_bits(h):
-    return np.asarray(h, np.uint16).view(np.float16).astype(np.float64)
-
-
-def bf16_bits(h):
-    return (np.asarray(h, np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
-
-
-def rounding_noise(oracle, lin, dy):
-    """Predicted 2-norm error of (ds_out, ds_mid, ds_in) from the training
-    path's fp16 roundings, to first order, each an independent relative
-    error of variance U2: s_in.x and s_mid.v in the forward, the saved v, and
-    s_out.dy and s_mid.dt in the backward.  W = Bu diag(s_mid) Bv carries an
-    input-side rounding to the output side."""
-    Bu = oracle.unpack(lin.Bu, lin.r).astype(np.float64)
-    Bv = oracle.unpack(lin.Bv, lin.n).astype(np.float64)
-    s_out, s_mid, s_in = f16_bits(lin.s_out), f16_bits(lin.s_mid), f16_bits(lin.s_in)
-    x, g = bf16_bits(lin.x), bf16_bits(dy)
-    sx = x * s_in
-    v = sx @ Bv.T
-    a = g * s_out
-    dt = a @ Bu
-    W2 = ((Bu * s_mid) @ Bv) ** 2
-    row = lambda t: (t ** 2).sum(1, keepdims=True)
-    var_out = (g ** 2 * (row(v * s_mid) + (sx ** 2) @ W2.T)).sum()
-    var_mid = (dt ** 2 * (row(sx) + v ** 2) + v ** 2 * row(a)).sum()
-    var_in = (x ** 2 * ((a ** 2) @ W2 + row(dt * s_mid))).sum()
-    return [float(np.sqrt(U2 * t)) for t in (var_out, var_mid, var_in)]
 
 
 def run_train(oracle, c):
