@@ -38,13 +38,27 @@ GEMV_TRAFFIC = {"sources": ("paper_2609_06161_amd/csrc/af1_gemv.hip",
                 "bytes_per_call": 2849213}
 
 
-def measured_gemv_traffic():
+# HBM bytes of the prefill leg's three calls at 2048 tokens (8192^2 r=4064,
+# 28672x8192 and 8192x28672 at r=6336), the sum over every kernel of each
+# call of the same scaled counters (see profiles/gemm_prefill_T2048_70b_shapes.md:
+# 268.8 + 1027.4 + 1116.5 MB).  Same validity rule as GEMV_TRAFFIC.
+GEMM_TRAFFIC = {"sources": ("paper_2609_06161_amd/csrc/af1_gemm.hip",
+                            "paper_2609_06161_amd/csrc/af1_device.h"),
+                "sha256": "557d167b5d1ef153e7186b9cf302c71b38688d3f244e1703685c612c43df3709",
+                "bytes_per_call": 2412700000}
+
+
+def measured_traffic(record):
     import hashlib
     h = hashlib.sha256()
-    for rel in GEMV_TRAFFIC["sources"]:
+    for rel in record["sources"]:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
-    return GEMV_TRAFFIC["bytes_per_call"] if h.hexdigest() == GEMV_TRAFFIC["sha256"] else None
+    return record["bytes_per_call"] if h.hexdigest() == record["sha256"] else None
+
+
+def measured_gemv_traffic():
+    return measured_traffic(GEMV_TRAFFIC)
 
 
 def gemv_algorithmic_bytes(m, n, r, b):
@@ -505,11 +519,12 @@ def bench_gemm(args, torch, stream):
     out["few_tokens"] = sweep
     # MFMA roofline of the prefill leg: algorithmic flops 2*T*r*(m+n) of the
     # three calls over their summed time, against the dense fp16 peak (the
-    # contractions run on fp16 operands).
+    # contractions run on fp16 operands); traffic: HBM bytes of the three
+    # calls together.
     out["roofline"] = {"bound": "mfma", "achieved": round(out["all3_tflops"], 1),
                        "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
                        "frac": round(out["all3_tflops"] / MFMA_F16_PEAK_TFLOPS, 4),
-                       "traffic": None}
+                       "traffic": measured_traffic(GEMM_TRAFFIC)}
     return out
 
 
