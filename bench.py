@@ -48,6 +48,12 @@ GEMM_TRAFFIC = {"sources": ("paper_2609_06161_amd/csrc/af1_gemm.hip",
                 "bytes_per_call": 2412700000}
 
 
+# HBM bytes of one backward call of the training leg (8192^2 r=4064, T=2048:
+# row statistics, preparation, both contractions, finish), same counters (see
+# profiles/train_scale_only_sq8192_T2048.md).  Same validity rule.
+TRAIN_BWD_TRAFFIC = dict(GEMM_TRAFFIC, bytes_per_call=422053879)
+
+
 def measured_traffic(record):
     import hashlib
     h = hashlib.sha256()
@@ -577,7 +583,7 @@ def bench_train(args, torch, stream):
                                   "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
                                   "frac": round(flops / (ms_b * 1e-3) / 1e12
                                                 / MFMA_F16_PEAK_TFLOPS, 4),
-                                  "traffic": None}}
+                                  "traffic": measured_traffic(TRAIN_BWD_TRAFFIC)}}
 
 
 def bench_nabf(args, torch, stream):
